@@ -1,0 +1,160 @@
+"""CPU oracle of MoNe test-time learning (TTL) — TEST INFRASTRUCTURE, NOT PART OF THE PRODUCT.
+
+Only the test-suite, the package's smoke check and the benchmark's CPU-baseline leg may import
+this module.  The product path (the HIP library and its Python binding) never calls it, and it
+imports nothing from the product package: its inputs are plain arrays.
+
+What it computes (MoNe, Sec. 3): a long context is split into segments of T tokens (Sec. 3.1).
+Every layer l owns a fast-weight memory M(.; W^(l)).  For each segment s in order, and for every
+layer independently, the memory takes one gradient step on the associative loss of that segment,
+evaluated at W_{s-1} (Sec. 3.4, layer-localised gradient; Eq. update).  After the last segment
+the memory is read on query-side inputs without any update (Eq. read).
+
+The memory, loss and optimiser are the configuration-mode ones (a plain, fully specified variant
+of the paper's richer defaults; each choice is stated where it is made):
+  * M(x) = W2 . SiLU(W1 . x): a 2-layer MLP d -> h -> D with SiLU and no biases.  The paper's
+    memory is a SwiGLU MLP per fast-weight head (Eq. swiglu); the configuration keeps its
+    structure (input matrix, SiLU, output matrix) without the gate branch.  W1 = W_in is [h, d]
+    and W2 = W_out^T is [D, h], both acting on column vectors as in the paper.
+  * targets: t_j = [W_k x_j ; W_v x_j] (Eq. proj), frozen projections, raw (no SiLU/L2 norm/RoPE).
+  * per-token loss l_j = ||M(x_j) - t_j||^2 summed over the D outputs ("mse_sum"), or divided by
+    D ("mse_mean"); segment loss L_s = (1/T) sum_j l_j (the segment-level average of Sec. 3.3).
+  * update: W_s = W_{s-1} - lr * grad L_s(W_{s-1})  (Eq. update with mu_s = lr * gradient).
+
+Everything is float64 NumPy.  Matrix products use numpy's matmul as a library primitive; there is
+no blocking, fusion or reordering beyond the definitions.
+
+Pins (tests in tests/test_oracle_*.py): hand-derived scalar case, central finite differences,
+torch.autograd (float64, CPU), brute-force loops, first-order descent, and invariants (lr = 0,
+zero residual, token duplication under the segment average, segment order, incremental ==
+one-shot, layer independence).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+LOSSES = ("mse_sum", "mse_mean")
+
+
+def sigmoid(z):
+    """Logistic function, evaluated without overflow for large |z|."""
+    z = np.asarray(z, dtype=np.float64)
+    e = np.exp(-np.abs(z))
+    return np.where(z >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
+
+
+def silu(z):
+    """SiLU(z) = z * sigmoid(z) (the activation of Eq. swiglu)."""
+    z = np.asarray(z, dtype=np.float64)
+    return z * sigmoid(z)
+
+
+def silu_grad(z):
+    """d SiLU / dz = sigmoid(z) * (1 + z * (1 - sigmoid(z)))."""
+    z = np.asarray(z, dtype=np.float64)
+    s = sigmoid(z)
+    return s * (1.0 + z * (1.0 - s))
+
+
+def _f64(a):
+    return np.asarray(a, dtype=np.float64)
+
+
+def memory_forward(x, w1, w2):
+    """Memory MLP on the rows of x ([n, d]): returns (Z, A, Y) with
+    Z = x W1^T ([n, h]), A = SiLU(Z), Y = A W2^T ([n, D]) -- i.e. y_j = W2 SiLU(W1 x_j)."""
+    x, w1, w2 = _f64(x), _f64(w1), _f64(w2)
+    z = x @ w1.T
+    a = silu(z)
+    y = a @ w2.T
+    return z, a, y
+
+
+def targets(x, wkv):
+    """Associative targets of Eq. proj, stacked per token: t_j = [W_k x_j ; W_v x_j] = W_kv x_j."""
+    return _f64(x) @ _f64(wkv).T
+
+
+def _loss_scale(n: int, d_out: int, loss: str) -> float:
+    """Factor c with dL_s/dY = c * (Y - targets)."""
+    if loss == "mse_sum":
+        return 2.0 / n
+    if loss == "mse_mean":
+        return 2.0 / (n * d_out)
+    raise ValueError(loss)
+
+
+def segment_loss(x, w1, w2, wkv, loss: str = "mse_sum") -> float:
+    """L_s = (1/T) sum_j l_j for the T rows of x (segment-level average, Sec. 3.3)."""
+    x = _f64(x)
+    n = x.shape[0]
+    if n == 0:
+        return 0.0
+    _, _, y = memory_forward(x, w1, w2)
+    r = y - targets(x, wkv)
+    per_token = np.sum(r * r, axis=1)
+    if loss == "mse_mean":
+        per_token = per_token / r.shape[1]
+    elif loss != "mse_sum":
+        raise ValueError(loss)
+    return float(np.sum(per_token) / n)
+
+
+def segment_grad(x, w1, w2, wkv, loss: str = "mse_sum"):
+    """Gradient of L_s with respect to this layer's own fast weights only (Sec. 3.4).
+
+    Returns (dL/dW1 [h, d], dL/dW2 [D, h], L_s).  Backpropagation through the two matrices:
+      G  = dL/dY = c (Y - targets)
+      dL/dW2 = G^T A
+      dZ = (G W2) * SiLU'(Z)
+      dL/dW1 = dZ^T x
+    An empty segment has no tokens and contributes a zero gradient.
+    """
+    x, w1, w2, wkv = _f64(x), _f64(w1), _f64(w2), _f64(wkv)
+    n = x.shape[0]
+    if n == 0:
+        return np.zeros_like(w1), np.zeros_like(w2), 0.0
+    z, a, y = memory_forward(x, w1, w2)
+    r = y - targets(x, wkv)
+    c = _loss_scale(n, w2.shape[0], loss)
+    g = c * r
+    gw2 = g.T @ a
+    dz = (g @ w2) * silu_grad(z)
+    gw1 = dz.T @ x
+    per_token = np.sum(r * r, axis=1)
+    if loss == "mse_mean":
+        per_token = per_token / r.shape[1]
+    return gw1, gw2, float(np.sum(per_token) / n)
+
+
+def ttl_step(x, w1, w2, wkv, lr: float, loss: str = "mse_sum"):
+    """One test-time-learning step of one layer on one segment (Eq. update):
+    both matrices move along the gradient taken at W_{s-1}.  Returns (W1_s, W2_s, L_s)."""
+    gw1, gw2, ls = segment_grad(x, w1, w2, wkv, loss)
+    return _f64(w1) - lr * gw1, _f64(w2) - lr * gw2, ls
+
+
+def ttl_run(segments, w1, w2, wkv, lr: float, loss: str = "mse_sum"):
+    """Sequential TTL of one layer: W_0 -> W_1 -> ... -> W_S over the segments in the given order.
+    Returns (W1_S, W2_S, [L_1, ..., L_S])."""
+    w1, w2 = _f64(w1), _f64(w2)
+    losses = []
+    for x in segments:
+        w1, w2, ls = ttl_step(x, w1, w2, wkv, lr, loss)
+        losses.append(ls)
+    return w1, w2, losses
+
+
+def ttl_run_layers(segments_per_layer, w1s, w2s, wkvs, lr: float, loss: str = "mse_sum"):
+    """TTL of several layers.  The gradient of layer l's loss with respect to any other layer's
+    fast weights is zero (Sec. 3.4), so every layer runs its own chain; nothing crosses layers."""
+    out = []
+    for segs, w1, w2, wkv in zip(segments_per_layer, w1s, w2s, wkvs):
+        out.append(ttl_run(segs, w1, w2, wkv, lr, loss))
+    return out
+
+
+def memory_kv(xq, w1, w2):
+    """Read of the final state (Eq. read): the memory's output on the query-side inputs,
+    [q, D] with K in columns [0, d_kv) and V in [d_kv, D).  Nothing is updated."""
+    return memory_forward(xq, w1, w2)[2]

@@ -1,0 +1,71 @@
+"""Workload configurations of the MoNe test-time-learning (TTL) hot path.
+
+Every configuration is a frozen-backbone shape with a 2-layer SiLU memory MLP per layer,
+``d_model -> d_hidden -> 2*d_kv`` producing ``[K | V]``, trained at test time by plain SGD on
+an MSE loss against the frozen layer's key/value projections (MoNe, Sec. 3.3-3.4), one step per
+segment of ``seg_len`` tokens (Sec. 3.1).
+
+Where a workload leaves a detail open the smaller workloads' stated defaults are inherited:
+MSE with the per-token squared error summed over the 2*d_kv output channels and averaged over the
+segment's tokens (Sec. 3.3, segment-level average), learning rate 1e-3, seed 0 and a 64-token query
+batch for the read step.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, replace
+
+
+@dataclass(frozen=True)
+class MoneConfig:
+    name: str
+    n_layers: int      # L: layers with a memory (one independent fast-weight MLP each)
+    d_model: int       # d: width of the segment hidden states x (memory input)
+    d_hidden: int      # h: memory MLP hidden width
+    d_kv: int          # width of K (and of V); the memory output is D = 2*d_kv = [K | V]
+    seg_len: int       # T: tokens per segment
+    n_context: int     # N: context tokens; S = N / T segments
+    act_dtype: str     # "f32" or "bf16": dtype of x, x_q, W_kv and stored intermediates
+    lr: float          # SGD learning rate
+    loss: str = "mse_sum"   # "mse_sum": c = 2/T ; "mse_mean": c = 2/(T*D)
+    n_query: int = 64  # Q: query tokens for the read step
+    seed: int = 0
+
+    @property
+    def d_out(self) -> int:
+        return 2 * self.d_kv
+
+    @property
+    def n_segments(self) -> int:
+        return self.n_context // self.seg_len
+
+    def flops_per_token_layer(self, with_targets: bool = True) -> int:
+        """Algorithmic FLOPs of one TTL step per context token per layer.
+
+        forward 1 (2dh) + forward 2 (2hD) + target projection (2dD) + backward to the hidden
+        layer (2hD) + the two weight gradients (2hD + 2dh).
+        """
+        d, h, D = self.d_model, self.d_hidden, self.d_out
+        f = 2 * (2 * d * h + 3 * h * D)
+        if with_targets:
+            f += 2 * d * D
+        return f
+
+    def flops_per_token(self, with_targets: bool = True) -> int:
+        return self.n_layers * self.flops_per_token_layer(with_targets)
+
+    def with_(self, **kw) -> "MoneConfig":
+        return replace(self, **kw)
+
+
+TINY = MoneConfig("tiny", n_layers=1, d_model=256, d_hidden=512, d_kv=128, seg_len=128,
+                  n_context=1024, act_dtype="f32", lr=1e-2)
+ONE_B = MoneConfig("1b", n_layers=16, d_model=2048, d_hidden=2048, d_kv=512, seg_len=512,
+                   n_context=32768, act_dtype="bf16", lr=1e-3)
+THREE_B = MoneConfig("3b", n_layers=28, d_model=3072, d_hidden=3072, d_kv=1024, seg_len=1024,
+                     n_context=131072, act_dtype="bf16", lr=1e-3)
+EIGHT_B = MoneConfig("8b", n_layers=32, d_model=4096, d_hidden=4096, d_kv=1024, seg_len=2048,
+                     n_context=131072, act_dtype="bf16", lr=1e-3)
+STRESS = MoneConfig("stress", n_layers=16, d_model=2048, d_hidden=2048, d_kv=512, seg_len=64,
+                    n_context=524288, act_dtype="bf16", lr=1e-3)
+
+CONFIGS = {c.name: c for c in (TINY, ONE_B, THREE_B, EIGHT_B, STRESS)}

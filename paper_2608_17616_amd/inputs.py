@@ -1,0 +1,101 @@
+"""Seeded synthetic inputs for the MoNe TTL hot path.
+
+This module holds input generation only and none of the method's arithmetic: both the CPU
+oracle's callers and the GPU path's callers draw their inputs here, so the two sides see the
+same numbers.
+
+Keyed generator: every block is drawn from its own NumPy PCG64 stream keyed by
+``(seed, kind, layer, index)``, so any layer or segment can be generated on its own (a parity
+test can check a subset of layers of a full-size run, and a segment can be regenerated without
+drawing the ones before it).  Draws are float64 standard normals, scaled, cast to float32, and,
+for bf16 activations, rounded to the nearest bf16 (ties to even).
+
+Distributions (the workloads' stated defaults):
+  x, x_q ~ N(0, 1)                           segment and query hidden states, per layer
+  W_k, W_v ~ N(0, 1/d)   stacked as W_kv = [W_k; W_v], shape [2*d_kv, d]
+  W1 ~ N(0, 1/d)         shape [h, d]      (variance 1/fan_in)
+  W2 ~ N(0, 1/h)         shape [2*d_kv, h] (variance 1/fan_in)
+"""
+from __future__ import annotations
+
+import numpy as np
+
+KIND_WK, KIND_WV, KIND_W1, KIND_W2, KIND_X, KIND_XQ = range(6)
+
+
+def normal(seed: int, kind: int, layer: int, index: int, shape, std: float) -> np.ndarray:
+    rng = np.random.default_rng([int(seed), int(kind), int(layer), int(index)])
+    return (rng.standard_normal(shape) * std).astype(np.float32)
+
+
+def bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round float32 values to bf16 (nearest, ties to even); returns the raw uint16 patterns.
+
+    Inputs are finite Gaussian draws, so no NaN/Inf handling is needed.
+    """
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return u.astype(np.uint16)
+
+
+def bf16_widen(bits: np.ndarray) -> np.ndarray:
+    """Exact float32 value of raw bf16 patterns."""
+    return (bits.astype(np.uint32) << 16).view(np.float32)
+
+
+def act_round(a: np.ndarray, act_dtype: str) -> np.ndarray:
+    """Activation-dtype values as float32 (bf16: nearest bf16, widened exactly)."""
+    if act_dtype == "f32":
+        return a
+    if act_dtype == "bf16":
+        return bf16_widen(bf16_bits(a))
+    raise ValueError(act_dtype)
+
+
+def layer_wkv(cfg, layer: int) -> np.ndarray:
+    """Frozen [W_k; W_v] of one layer, [2*d_kv, d], float32 (bf16-representable in bf16 mode)."""
+    d = cfg.d_model
+    wk = normal(cfg.seed, KIND_WK, layer, 0, (cfg.d_kv, d), 1.0 / np.sqrt(d))
+    wv = normal(cfg.seed, KIND_WV, layer, 0, (cfg.d_kv, d), 1.0 / np.sqrt(d))
+    return act_round(np.concatenate([wk, wv], axis=0), cfg.act_dtype)
+
+
+def layer_w1(cfg, layer: int) -> np.ndarray:
+    """Initial fast weight W1 (W_in) of one layer, [h, d], float32."""
+    return normal(cfg.seed, KIND_W1, layer, 0, (cfg.d_hidden, cfg.d_model),
+                  1.0 / np.sqrt(cfg.d_model))
+
+
+def layer_w2(cfg, layer: int) -> np.ndarray:
+    """Initial fast weight W2 (W_out) of one layer, [2*d_kv, h], float32."""
+    return normal(cfg.seed, KIND_W2, layer, 0, (cfg.d_out, cfg.d_hidden),
+                  1.0 / np.sqrt(cfg.d_hidden))
+
+
+def segment_x(cfg, layer: int, s: int, n_tokens: int | None = None) -> np.ndarray:
+    """Hidden states of segment s (0-based) at one layer, [n_tokens, d], float32."""
+    n = cfg.seg_len if n_tokens is None else n_tokens
+    return act_round(normal(cfg.seed, KIND_X, layer, s, (n, cfg.d_model), 1.0), cfg.act_dtype)
+
+
+def query_x(cfg, layer: int, q: int | None = None, index: int = 0) -> np.ndarray:
+    """Query-side memory input of one layer, [q, d], float32."""
+    q = cfg.n_query if q is None else q
+    return act_round(normal(cfg.seed, KIND_XQ, layer, index, (q, cfg.d_model), 1.0),
+                     cfg.act_dtype)
+
+
+def device_normal_(t, std: float, generator):
+    """Fill a device tensor in place with N(0, std^2) draws rounded to its dtype.
+
+    Used for benchmark inputs too large to draw on the host in reasonable time; the draws are
+    seeded through ``generator`` (a torch.Generator on the tensor's device).
+    """
+    import torch
+    if t.dtype == torch.float32:
+        t.normal_(0.0, std, generator=generator)
+    else:
+        tmp = torch.empty(t.shape, dtype=torch.float32, device=t.device)
+        tmp.normal_(0.0, std, generator=generator)
+        t.copy_(tmp)
+    return t
