@@ -1,0 +1,211 @@
+#!/usr/bin/env python3
+"""Throughput of the MoNe test-time-learning hot path on one MI355X.
+
+One step = the whole hot path over one synthetic context: every segment of the context goes
+through mone_ttl_segment (all layers, grouped launches), then mone_memory_kv reads the final
+state on a query batch.  The default workload is the 8B-class shape: 32 layers, d = h = 4096,
+D = 2048 (8 KV heads x 128 for K and for V), T = 2048, N = 131072 context tokens
+(64 segments), Q = 64 query tokens, bf16 activations, fp32 fast weights, lr 1e-3.
+
+The context is resident in HBM before timing starts (64 distinct segments, 32 GiB).  Inputs
+are seeded synthetic Gaussians: x ~ N(0, 1), W_k, W_v, W1 ~ N(0, 1/d), W2 ~ N(0, 1/h), drawn
+on the GPU with torch's generator.
+
+Prints one JSON line.  Per-stage kernel durations come from HIP events the library records on
+the launch stream around every stage during the timed steps.  The CPU baseline times the CPU
+oracle (float64 NumPy, as it stands) on one layer over as many segments as fit in about
+--cpu-seconds, scaled to all layers.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "context tokens/sec of test-time learning (all layers); % bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X dense fp32 matrix
+PEAK_HBM_GBS = 8000.0
+
+
+def stage_work(cfg, q):
+    """Algorithmic FLOPs and bytes of one launch of each stage (all layers)."""
+    L, d, h, D, T = cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out, cfg.seg_len
+    E = 2 if cfg.act_dtype == "bf16" else 4
+    return {
+        "xt": (0, L * T * d * E * 2),
+        "fwd1": (L * 2 * T * d * h, L * (T * d + h * d + T * h * 3) * E),
+        "fwd2": (L * 2 * T * D * (h + d), L * (T * h + D * h + T * d + D * d + 2 * T * D) * E),
+        "bwd": (L * 2 * T * D * h, L * (T * D + h * D + 2 * T * h) * E),
+        "upd": (L * (2 * T * D * h + 2 * T * h * d),
+                L * ((D * T + h * T + h * T + d * T) * E + (D * h + h * d) * 8)),
+        "kv1": (L * 2 * q * d * h, L * (q * d + h * d + q * h) * E),
+        "kv2": (L * 2 * q * h * D, L * (q * h + D * h) * E + L * q * D * 4),
+    }
+
+
+def cpu_baseline(cfg, w1, w2, wkv, xs, budget_s):
+    import numpy as np
+
+    import oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()
+                     if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    w1 = np.asarray(w1, np.float64)
+    w2 = np.asarray(w2, np.float64)
+    done, t0 = 0, time.perf_counter()
+    while True:
+        w1, w2, _ = orc.ttl_step(xs[done % len(xs)], w1, w2, wkv, cfg.lr, cfg.loss)
+        done += 1
+        if time.perf_counter() - t0 >= budget_s or done >= 64:
+            break
+    t = time.perf_counter() - t0
+    tok_s = done * cfg.seg_len / t / cfg.n_layers
+    return {"value": tok_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"layer 0, {done} consecutive segments of T={cfg.seg_len} tokens "
+                      f"({t:.1f} s, float64 NumPy), scaled to {cfg.n_layers} layers"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="8b")
+    ap.add_argument("--segments", type=int, default=0,
+                    help="context segments per step (default: the workload's N / T)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run one device copy of this size (HBM counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: --gpus {args.gpus} is not supported: this build measures one GPU "
+              "(the path would shard by layers with no communication during TTL).",
+              file=sys.stderr, flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_17616_amd import configs, inputs, mone
+
+    cfg = configs.CONFIGS[args.config]
+    L, d, h, D, T, Q = (cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out, cfg.seg_len,
+                        cfg.n_query)
+    S = args.segments or cfg.n_segments
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    act = torch.bfloat16 if cfg.act_dtype == "bf16" else torch.float32
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfg.seed)
+
+    w1 = inputs.device_normal_(torch.empty(L, h, d, dtype=torch.float32, device=dev),
+                               1 / np.sqrt(d), gen)
+    w2 = inputs.device_normal_(torch.empty(L, D, h, dtype=torch.float32, device=dev),
+                               1 / np.sqrt(h), gen)
+    wkv = inputs.device_normal_(torch.empty(L, D, d, dtype=act, device=dev), 1 / np.sqrt(d), gen)
+    ctx = torch.empty(S, L, T, d, dtype=act, device=dev)
+    for s in range(S):
+        inputs.device_normal_(ctx[s], 1.0, gen)
+    xq = inputs.device_normal_(torch.empty(L, Q, d, dtype=act, device=dev), 1.0, gen)
+    kv = torch.empty(L, Q, D, dtype=torch.float32, device=dev)
+    # CPU-baseline sample: layer 0 of the same workload, before any step changes the state
+    n_cpu = 0 if args.no_cpu_baseline else min(S, 4)
+    cpu_in = None
+    if n_cpu:
+        cpu_in = (w1[0].double().cpu().numpy(), w2[0].double().cpu().numpy(),
+                  wkv[0].double().cpu().numpy(),
+                  [ctx[s, 0].double().cpu().numpy() for s in range(n_cpu)])
+
+    stream = torch.cuda.current_stream(dev)
+    sess = mone.TtlSession(cfg, wkv, w1, w2, stream)
+    H = sess.handle
+    sptr = stream.cuda_stream
+
+    def step():
+        for s in range(S):
+            mone.mone_ttl_segment(H, ctx[s], T, sptr)
+        mone.mone_memory_kv(H, xq, Q, kv, mone.MONE_F32, sptr)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if args.calib_copy_mib:
+        nb = args.calib_copy_mib << 20
+        src = torch.empty(nb, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    mone.mone_ttl_set_stage_timing(H, args.steps * (S * 5 + 2))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stimes = mone.mone_ttl_stage_times(H)
+    finite = bool(torch.isfinite(w1).all().item() and torch.isfinite(w2).all().item()
+                  and torch.isfinite(kv).all().item())
+    sess.close()
+
+    tokens = args.steps * S * T
+    value = tokens / elapsed
+    flop_tok = cfg.flops_per_token()
+    peak = PEAK_BF16_TFLOPS if cfg.act_dtype == "bf16" else PEAK_F32_TFLOPS
+    mfma_pct = 100.0 * value * flop_tok / (peak * 1e12)
+    work = stage_work(cfg, Q)
+    stages = {}
+    for name, (ms, cnt) in stimes.items():
+        if cnt == 0:
+            continue
+        fl, by = work[name]
+        avg_s = ms / cnt / 1e3
+        stages[name] = {"launches": cnt, "avg_ms": round(ms / cnt, 4),
+                        "tflops": round(fl / avg_s / 1e12, 1),
+                        "gbs": round(by / avg_s / 1e9, 1)}
+    dom = max(stages, key=lambda k: stimes[k][0])
+    dfl, dby = work[dom]
+    davg = stimes[dom][0] / stimes[dom][1] / 1e3
+    if dfl > 0:
+        roof = {"kernel": f"gemm_nt_kernel ({dom})", "bound": "mfma",
+                "achieved": round(dfl / davg / 1e12, 1), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(dfl / davg / 1e12 / peak, 4), "traffic": None}
+    else:
+        roof = {"kernel": dom, "bound": "hbm", "achieved": round(dby / davg / 1e9, 1),
+                "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(dby / davg / 1e9 / PEAK_HBM_GBS, 4), "traffic": None}
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.act_dtype, "data": "synthetic",
+        "config": {"workload": f"{cfg.name}-class TTL: L={L} d={d} h={h} D={D} T={T} "
+                               f"N={S * T} ({S} segments) + read Q={Q}",
+                   "n_layers": L, "d_model": d, "d_hidden": h, "d_out": D, "seg_len": T,
+                   "n_context": S * T, "n_query": Q, "lr": cfg.lr},
+        "mfma_pct": round(mfma_pct, 2),
+        "flop_per_token": flop_tok,
+        "roofline": roof,
+        "stages": stages,
+        "finite": finite,
+    }
+    if cpu_in is not None:
+        out["cpu_baseline"] = cpu_baseline(cfg, *cpu_in, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

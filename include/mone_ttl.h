@@ -1,0 +1,158 @@
+/*
+ * mone_ttl.h -- C ABI of the MI355X (gfx950) MoNe test-time-learning library.
+ *
+ * MoNe (Modular Neural Memory) attaches a fast-weight memory network to every layer of a
+ * frozen Transformer.  A long context is consumed in segments of T tokens (Sec. 3.1); for each
+ * segment, every layer's memory takes one gradient step on an associative loss computed from
+ * that layer's own hidden states only (Sec. 3.3, Sec. 3.4), and after the last segment the
+ * memory is read on query tokens without being updated (Eq. read).
+ *
+ * The memory, loss and optimiser implemented here are a fully specified variant of the paper's:
+ *   memory   M(x) = W2 . SiLU(W1 . x), a 2-layer MLP d -> h -> D (D = 2*d_kv), no biases,
+ *            output [K | V] (the SwiGLU memory of Eq. swiglu without its gate branch);
+ *   targets  t = [W_k x ; W_v x] from the frozen projections (Eq. proj), no preprocessing;
+ *   loss     L_s = (1/n) sum_j ||M(x_j) - t_j||^2 over the n tokens of the segment
+ *            (segment-level average of Sec. 3.3; MONE_LOSS_MSE_MEAN also divides by D);
+ *   update   W <- W - lr * dL_s/dW for W1 and W2, both gradients taken at W_{s-1}
+ *            (Eq. update with a plain SGD step).
+ *
+ * Conventions for every call:
+ *   - Matrices are row-major.  W1 is [h][d] (acts on column vectors: z = W1 x), W2 is [D][h],
+ *     W_kv is [D][d] = [W_k ; W_v] (rows [0, d_kv) give K, rows [d_kv, D) give V).  A tensor
+ *     "[L][...]" holds the L layers back to back with no padding.
+ *   - Device pointers are HIP device addresses, 16-byte aligned, owned by the caller; the
+ *     library never allocates device memory.  Host pointers are marked "host".
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Calls only enqueue work on it,
+ *     except where a call says it synchronises.  A handle must not be used from two threads
+ *     at once.
+ *   - Every call returns a mone_status.  Arguments are validated on the host before any HIP
+ *     call; a failing call enqueues nothing and leaves the state untouched.
+ *     mone_ttl_last_error() returns a message for the last failure of the calling thread.
+ *   - GPU-path limits: d_model, d_hidden and d_kv must be multiples of 64 (MONE_EUNSUPPORTED
+ *     otherwise); seg_len is at most 65536.
+ */
+#ifndef MONE_TTL_H
+#define MONE_TTL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MONE_OK = 0,
+  MONE_EINVAL = -1,       /* bad argument: null/misaligned pointer, bad size, bad enum */
+  MONE_EUNSUPPORTED = -2, /* valid but outside the GPU path's limits */
+  MONE_EHIP = -3,         /* a HIP runtime call or kernel launch failed */
+  MONE_ESTATE = -4        /* the handle is not usable for this call */
+} mone_status;
+
+typedef enum { MONE_F32 = 0, MONE_BF16 = 1 } mone_dtype;
+
+typedef enum {
+  MONE_LOSS_MSE_SUM = 0,  /* l_j = ||y_j - t_j||^2; dL_s/dY = (2/n)(Y - T) */
+  MONE_LOSS_MSE_MEAN = 1  /* l_j = ||y_j - t_j||^2 / D; dL_s/dY = (2/(n D))(Y - T) */
+} mone_loss;
+
+typedef struct {
+  int32_t n_layers;  /* L >= 1: layers with a memory */
+  int32_t d_model;   /* d: width of the hidden states x (memory input) */
+  int32_t d_hidden;  /* h: memory hidden width */
+  int32_t d_kv;      /* width of K and of V; the memory output is D = 2*d_kv */
+  int32_t seg_len;   /* T: maximum tokens per segment */
+  int32_t act_dtype; /* mone_dtype of x, x_q, W_kv and stored intermediates; the fast weights
+                        are always fp32 */
+  int32_t loss;      /* mone_loss */
+  float lr;          /* SGD learning rate (finite, may be 0) */
+} mone_ttl_config;
+
+typedef struct mone_ttl mone_ttl; /* opaque host object */
+
+/* Number of workspace bytes a handle for `cfg` needs.  It depends on L, d, h, d_kv, T and the
+ * activation dtype only -- never on the context length N, which is not an argument anywhere:
+ * the memory's footprint is constant in N (Sec. 4.3).  Returns 0 if `cfg` is invalid or
+ * unsupported (mone_ttl_last_error() says why). */
+size_t mone_ttl_workspace_bytes(const mone_ttl_config* cfg);
+
+/* Create a handle over caller-owned state (the initial state W_0, s = 0 in Sec. 3.1).
+ *   wkv        [L][D][d] act_dtype, frozen; borrowed, must stay valid and unchanged while the
+ *              handle lives.
+ *   w1         [L][h][d] fp32 fast weights W1; borrowed and updated in place by
+ *              mone_ttl_segment.
+ *   w2         [L][D][h] fp32 fast weights W2; as w1.
+ *   workspace  device buffer of at least mone_ttl_workspace_bytes(cfg) bytes, owned by the
+ *              handle until mone_ttl_destroy; 256-byte aligned.
+ * Enqueues on `stream` the clearing of the workspace and the construction of the handle's
+ * internal copies of w1/w2 (activation-dtype and transposed copies).  Writing w1/w2 from
+ * outside while the handle lives makes those copies stale: create a new handle instead (a
+ * checkpoint is a copy of w1/w2; resuming is mone_ttl_init on the copy).
+ * On success *out receives the handle; on failure *out is left NULL. */
+int mone_ttl_init(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, float* w1,
+                  float* w2, void* workspace, size_t workspace_bytes, void* stream);
+
+/* One test-time-learning step of every layer on one segment (Eq. update; Sec. 3.4).
+ *   x         [L][n_tokens][d] act_dtype: the segment's hidden states at each layer.
+ *   n_tokens  0 <= n_tokens <= seg_len.  The loss averages over the n_tokens tokens present
+ *             (a short final segment); n_tokens = 0 is a no-op (an empty segment has no
+ *             gradient).
+ * For each layer l independently: Z = X W1^T, A = SiLU(Z), R = A W2^T - X W_kv^T,
+ * G = c R, W2 -= lr G^T A, W1 -= lr ((G W2) * SiLU'(Z))^T X, both gradients at the weights
+ * the call started from.  All L layers run as one grouped launch per stage.  Segments must be
+ * enqueued in context order (Sec. 3.4: W_0 -> W_1 -> ... -> W_S); `x` may be reused or freed
+ * once the enqueued work has completed on `stream`. */
+int mone_ttl_segment(mone_ttl* h, const void* x, int32_t n_tokens, void* stream);
+
+/* Read of the current state on query-side inputs, without any update (Eq. read; Sec. 3.4):
+ *   KV = W2 SiLU(W1 x_q) for every query row of every layer.
+ *   xq       [L][q][d] act_dtype.
+ *   q        >= 0 query rows (q = 0 is a no-op).
+ *   kv       [L][q][D] of kv_dtype (MONE_F32 or MONE_BF16); columns [0, d_kv) are K,
+ *            [d_kv, D) are V.
+ * The fast weights are not modified, so the call may be repeated (with identical results)
+ * and further segments may follow it (incremental extension, multi-query reuse).  It uses the
+ * handle's scratch space, so it must not overlap with another call on the same handle. */
+int mone_memory_kv(mone_ttl* h, const void* xq, int32_t q, void* kv, int32_t kv_dtype,
+                   void* stream);
+
+/* The segment loss L_s of the last mone_ttl_segment call, per layer, evaluated at the weights
+ * that step started from (the loss of Sec. 3.3 for that segment).  out_host: host float[L].
+ * Synchronises `stream`.  MONE_ESTATE if no non-empty segment has been processed yet. */
+int mone_ttl_loss(mone_ttl* h, float* out_host, void* stream);
+
+/* Destroy a handle (host memory only; the caller frees its device buffers afterwards, once
+ * the enqueued work has completed).  NULL is accepted. */
+int mone_ttl_destroy(mone_ttl* h);
+
+/* Message of the last failing call on this thread ("" if none).  Valid until the next call. */
+const char* mone_ttl_last_error(void);
+
+/* ---- measurement hooks ---------------------------------------------------------------- */
+
+/* Stages of one segment and of one read, in launch order. */
+#define MONE_STAGE_XT 0    /* X -> X^T staging copy (operand of the W1 gradient) */
+#define MONE_STAGE_FWD1 1  /* Z = X W1^T; A = SiLU(Z) */
+#define MONE_STAGE_FWD2 2  /* R = A W2^T - X W_kv^T; G = c R; loss partials */
+#define MONE_STAGE_BWD 3   /* dZ = (G W2) * SiLU'(Z) */
+#define MONE_STAGE_UPD 4   /* W2 -= lr G^T A and W1 -= lr dZ^T X (one grouped launch) */
+#define MONE_STAGE_KV1 5   /* read: A_q = SiLU(X_q W1^T) */
+#define MONE_STAGE_KV2 6   /* read: KV = A_q W2^T */
+#define MONE_N_STAGES 7
+
+/* Enable (max_records > 0) or disable (0) per-stage timing: each subsequent stage launch is
+ * bracketed by a pair of HIP events recorded on the call's stream, up to max_records pairs
+ * (further launches are not timed).  Creates the events on the current device (host call,
+ * no device allocation).  Enabling again discards earlier records. */
+int mone_ttl_set_stage_timing(mone_ttl* h, int32_t max_records);
+
+/* Synchronise on the recorded events and report, per stage, the summed elapsed milliseconds
+ * (ms_sum, host double[MONE_N_STAGES]) and the number of timed launches (count, host
+ * int32[MONE_N_STAGES]); then clear the records. */
+int mone_ttl_stage_times(mone_ttl* h, double* ms_sum, int32_t* count);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MONE_TTL_H */

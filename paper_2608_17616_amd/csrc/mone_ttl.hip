@@ -1,0 +1,556 @@
+// Host side of the MoNe test-time-learning library: argument validation, workspace layout and
+// the per-stage launches of a segment step and of the read.  The C ABI is declared in
+// include/mone_ttl.h.
+//
+// Data layout in HBM (row-major; "[L]" = the L layers back to back):
+//   caller state   W1 [L][h][d] fp32, W2 [L][D][h] fp32, W_kv [L][D][d] act
+//   workspace      W1c [L][h][d] act   (bf16 mode only: MFMA copy of W1; fp32 mode reads W1)
+//                  W2c [L][D][h] act   (bf16 mode only)
+//                  W2t [L][h][D] act   W2 transposed (B operand of the backward GEMM)
+//                  A   [L][Tp][h], A^T [L][h][Tp], SiLU'(Z) [L][Tp][h]
+//                  G   [L][Tp][D], G^T [L][D][Tp]
+//                  dZ^T [L][h][Tp], X^T [L][d][Tp]
+//                  loss partials [L][P], loss [L] fp32
+// Tp = seg_len rounded up to 256; rows and columns beyond the segment's n tokens are zero, so
+// the token-contracting GEMMs run over n rounded up to their K step with no masking.
+//
+// A segment step is five launches on the caller's stream, each grouped over all L layers:
+//   XT   X -> X^T
+//   FWD1 Z = X W1^T                      epilogue: A, A^T, SiLU'(Z)
+//   FWD2 R = [A | X] [W2 | W_kv]^T-split epilogue: G = c R, G^T, sum R^2 partials
+//   BWD  dA = G W2                       epilogue: dZ^T = (dA * SiLU'(Z))^T
+//   UPD  G^T A and dZ^T X (2 problems)   epilogue: fp32 SGD read-modify-write + copies
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/mone_ttl.h"
+#include "kernels.hpp"
+
+using namespace mone;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(MONE_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+long long round_up(long long v, long long a) { return (v + a - 1) / a * a; }
+
+struct Layout {
+  int Tp;
+  int loss_per_layer;
+  size_t w1c, w2c, w2t, a, at, ds, g, gt, dzt, xt, loss_part, loss_out, total;
+};
+
+int check_config(const mone_ttl_config* c) {
+  if (!c) return fail(MONE_EINVAL, "config is NULL");
+  if (c->n_layers < 1 || c->d_model < 1 || c->d_hidden < 1 || c->d_kv < 1 || c->seg_len < 1)
+    return fail(MONE_EINVAL, "config sizes must be >= 1 (L=%d d=%d h=%d d_kv=%d T=%d)",
+                c->n_layers, c->d_model, c->d_hidden, c->d_kv, c->seg_len);
+  if (c->act_dtype != MONE_F32 && c->act_dtype != MONE_BF16)
+    return fail(MONE_EINVAL, "act_dtype %d is not MONE_F32 or MONE_BF16", c->act_dtype);
+  if (c->loss != MONE_LOSS_MSE_SUM && c->loss != MONE_LOSS_MSE_MEAN)
+    return fail(MONE_EINVAL, "loss %d is not a mone_loss", c->loss);
+  if (!std::isfinite(c->lr)) return fail(MONE_EINVAL, "lr is not finite");
+  if (c->d_model % 64 || c->d_hidden % 64 || c->d_kv % 64)
+    return fail(MONE_EUNSUPPORTED, "d_model, d_hidden and d_kv must be multiples of 64");
+  if (c->seg_len > 65536) return fail(MONE_EUNSUPPORTED, "seg_len above 65536");
+  const long long Tp = round_up(c->seg_len, 256);
+  const long long d = c->d_model, h = c->d_hidden, D = 2LL * c->d_kv;
+  const long long mx = d > h ? (d > D ? d : D) : (h > D ? h : D);
+  if (h * d >= (1LL << 31) || D * h >= (1LL << 31) || D * d >= (1LL << 31) ||
+      Tp * mx >= (1LL << 31))
+    return fail(MONE_EUNSUPPORTED, "a per-layer matrix exceeds 2^31 elements");
+  return MONE_OK;
+}
+
+Layout make_layout(const mone_ttl_config* c) {
+  Layout L{};
+  const size_t E = c->act_dtype == MONE_BF16 ? 2 : 4;
+  const size_t nl = (size_t)c->n_layers;
+  const size_t d = c->d_model, h = c->d_hidden, D = 2 * (size_t)c->d_kv;
+  L.Tp = (int)round_up(c->seg_len, 256);
+  const size_t Tp = L.Tp;
+  // 4 wave partials per tile of the smallest tile shape (64 rows x 128 columns)
+  L.loss_per_layer = (int)(4 * (Tp / 64) * ((D + 127) / 128));
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, kAlign);
+    return o;
+  };
+  const bool bf = c->act_dtype == MONE_BF16;
+  L.w1c = bf ? take(nl * h * d * E) : 0;
+  L.w2c = bf ? take(nl * D * h * E) : 0;
+  L.w2t = take(nl * h * D * E);
+  L.a = take(nl * Tp * h * E);
+  L.at = take(nl * h * Tp * E);
+  L.ds = take(nl * Tp * h * E);
+  L.g = take(nl * Tp * D * E);
+  L.gt = take(nl * D * Tp * E);
+  L.dzt = take(nl * h * Tp * E);
+  L.xt = take(nl * d * Tp * E);
+  L.loss_part = take(nl * (size_t)L.loss_per_layer * 4);
+  L.loss_out = take(nl * 4);
+  L.total = off;
+  return L;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+enum TileShape { TILE_128x128 = 0, TILE_64x256 = 1 };
+
+// 64-row tiles for short token extents (short segments, query batches), 128 x 128 otherwise.
+TileShape pick_tile(int m, int n, int layers) {
+  (void)n;
+  (void)layers;
+  return m <= 64 ? TILE_64x256 : TILE_128x128;
+}
+
+// Host description of one grouped problem before the tile shape fixes its tiling.
+struct Spec {
+  Part part[2];
+  int nparts;
+  int m_extent;   // rows that are computed (tiles cover them)
+  int n;          // columns
+  int m_store;    // rows stored by the epilogue; -1 = every computed tile row
+};
+
+Opnd opnd(const void* p, long long lstride, int ld, int rows) {
+  Opnd o;
+  o.p = p;
+  o.lstride = lstride;
+  o.ld = ld;
+  o.rows = rows;
+  return o;
+}
+
+template <typename E, int BM, int BN, class Epi>
+hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi,
+                        hipStream_t s, int* tiles_per_layer0) {
+  GemmLaunch<Epi> G;
+  std::memset(&G, 0, sizeof G);
+  int begin = 0;
+  for (int i = 0; i < nspec; ++i) {
+    Problem& P = G.prob[i];
+    P.part[0] = specs[i].part[0];
+    P.part[1] = specs[i].part[1];
+    P.nparts = specs[i].nparts;
+    P.tiles_m = (specs[i].m_extent + BM - 1) / BM;
+    P.tiles_n = (specs[i].n + BN - 1) / BN;
+    P.M = specs[i].m_store >= 0 ? specs[i].m_store : P.tiles_m * BM;
+    P.N = specs[i].n;
+    P.tile_begin = begin;
+    begin += P.tiles_m * P.tiles_n * layers;
+  }
+  G.nprob = nspec;
+  G.epi = epi;
+  if (tiles_per_layer0) *tiles_per_layer0 = G.prob[0].tiles_m * G.prob[0].tiles_n;
+  if (begin == 0) return hipSuccess;
+  gemm_nt_kernel<E, BM, BN, Epi><<<dim3(begin), dim3(256), 0, s>>>(G);
+  return hipGetLastError();
+}
+
+template <typename E, class Epi>
+hipError_t launch_gemm(TileShape t, const Spec* specs, int nspec, int layers, const Epi& epi,
+                       hipStream_t s, int* tiles_per_layer0 = nullptr) {
+  if (t == TILE_64x256)
+    return launch_tiled<E, 64, 256>(specs, nspec, layers, epi, s, tiles_per_layer0);
+  return launch_tiled<E, 128, 128>(specs, nspec, layers, epi, s, tiles_per_layer0);
+}
+
+}  // namespace
+
+struct mone_ttl {
+  mone_ttl_config cfg;
+  Layout lay;
+  const void* wkv;
+  float* w1;
+  float* w2;
+  unsigned char* ws;
+  int last_n;           // tokens of the last non-empty segment (0: none yet)
+  int last_loss_count;  // loss partials per layer written by that segment
+  // stage timing
+  std::vector<hipEvent_t> ev;
+  std::vector<int> ev_stage;
+  int ev_cap = 0, ev_used = 0;
+
+  template <typename T>
+  T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+
+  void timing_begin(int stage, hipStream_t s) {
+    if (ev_used < ev_cap) (void)hipEventRecord(ev[2 * ev_used], s);
+    (void)stage;
+  }
+  void timing_end(int stage, hipStream_t s) {
+    if (ev_used < ev_cap) {
+      (void)hipEventRecord(ev[2 * ev_used + 1], s);
+      ev_stage[ev_used] = stage;
+      ++ev_used;
+    }
+  }
+  void destroy_events() {
+    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+    ev.clear();
+    ev_stage.clear();
+    ev_cap = ev_used = 0;
+  }
+};
+
+namespace {
+
+template <typename E>
+int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
+  const mone_ttl_config& c = H->cfg;
+  const Layout& Ly = H->lay;
+  const int Lc = c.n_layers, d = c.d_model, h = c.d_hidden, D = 2 * c.d_kv, Tp = Ly.Tp;
+  constexpr int BK = 8 * (16 / (int)sizeof(E));
+  const bool bf = sizeof(E) == 2;
+  const E* w1op = bf ? H->at<E>(Ly.w1c) : reinterpret_cast<const E*>(H->w1);
+  const E* w2op = bf ? H->at<E>(Ly.w2c) : reinterpret_cast<const E*>(H->w2);
+  E* w2t = H->at<E>(Ly.w2t);
+  E* A = H->at<E>(Ly.a);
+  E* At = H->at<E>(Ly.at);
+  E* dS = H->at<E>(Ly.ds);
+  E* Gm = H->at<E>(Ly.g);
+  E* Gt = H->at<E>(Ly.gt);
+  E* dZt = H->at<E>(Ly.dzt);
+  E* Xt = H->at<E>(Ly.xt);
+  const long long lsx = (long long)n * d;
+  const long long lth = (long long)Tp * h, ltd = (long long)Tp * D, ltx = (long long)Tp * d;
+  const int nz = (int)round_up(n, 64);  // zero-filled token extent of the transposed copies
+  hipError_t e;
+
+  // XT: X^T, the B operand of the W1 gradient (tokens become the contraction axis)
+  H->timing_begin(MONE_STAGE_XT, s);
+  transpose_kernel<E, E><<<dim3((d + 63) / 64, (nz + 63) / 64, Lc), dim3(256), 0, s>>>(
+      reinterpret_cast<const E*>(x), lsx, d, n, d, Xt, ltx, Tp, nz);
+  if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch XT");
+  H->timing_end(MONE_STAGE_XT, s);
+
+  // FWD1: Z = X W1^T  ->  A, A^T, SiLU'(Z)
+  {
+    Spec sp{};
+    sp.part[0].a = opnd(x, lsx, d, n);
+    sp.part[0].b = opnd(w1op, (long long)h * d, d, h);
+    sp.part[0].k_len = d;
+    sp.nparts = 1;
+    sp.m_extent = n;
+    sp.n = h;
+    sp.m_store = -1;
+    EpiFwd1<E> epi;
+    epi.a = A; epi.ds = dS; epi.at = At; epi.ls = lth; epi.h = h; epi.Tp = Tp; epi.n = n;
+    H->timing_begin(MONE_STAGE_FWD1, s);
+    if ((e = launch_gemm<E>(pick_tile(n, h, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch FWD1");
+    H->timing_end(MONE_STAGE_FWD1, s);
+  }
+  // FWD2: R = A W2^T - X W_kv^T  ->  G = c R, G^T, loss partials
+  {
+    Spec sp{};
+    sp.part[0].a = opnd(A, lth, h, n);
+    sp.part[0].b = opnd(w2op, (long long)D * h, h, D);
+    sp.part[0].k_len = h;
+    sp.part[1].a = opnd(x, lsx, d, n);
+    sp.part[1].b = opnd(H->wkv, (long long)D * d, d, D);
+    sp.part[1].k_len = d;
+    sp.nparts = 2;
+    sp.m_extent = n;
+    sp.n = D;
+    sp.m_store = -1;
+    EpiFwd2<E> epi;
+    epi.g = Gm; epi.gt = Gt; epi.loss_part = H->at<float>(Ly.loss_part); epi.ls = ltd;
+    epi.D = D; epi.Tp = Tp; epi.n = n; epi.parts_per_layer = Ly.loss_per_layer;
+    epi.c = c.loss == MONE_LOSS_MSE_SUM ? 2.0f / (float)n : 2.0f / ((float)n * (float)D);
+    int tiles = 0;
+    H->timing_begin(MONE_STAGE_FWD2, s);
+    if ((e = launch_gemm<E>(pick_tile(n, D, Lc), &sp, 1, Lc, epi, s, &tiles)) != hipSuccess)
+      return hip_fail(e, "launch FWD2");
+    H->timing_end(MONE_STAGE_FWD2, s);
+    H->last_loss_count = 4 * tiles;
+  }
+  // BWD: dA = G W2 (B operand W2^T, K-contiguous)  ->  dZ^T
+  {
+    Spec sp{};
+    sp.part[0].a = opnd(Gm, ltd, D, n);
+    sp.part[0].b = opnd(w2t, (long long)h * D, D, h);
+    sp.part[0].k_len = D;
+    sp.nparts = 1;
+    sp.m_extent = n;
+    sp.n = h;
+    sp.m_store = -1;
+    EpiBwd<E> epi;
+    epi.ds = dS; epi.dzt = dZt; epi.ls = lth; epi.h = h; epi.Tp = Tp; epi.n = n;
+    H->timing_begin(MONE_STAGE_BWD, s);
+    if ((e = launch_gemm<E>(pick_tile(n, h, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch BWD");
+    H->timing_end(MONE_STAGE_BWD, s);
+  }
+  // UPD: W2 -= lr G^T A  and  W1 -= lr dZ^T X, one grouped launch
+  {
+    const int kt = (int)round_up(n, BK);
+    Spec sp[2] = {};
+    sp[0].part[0].a = opnd(Gt, ltd, Tp, D);
+    sp[0].part[0].b = opnd(At, lth, Tp, h);
+    sp[0].part[0].k_len = kt;
+    sp[0].nparts = 1;
+    sp[0].m_extent = D;
+    sp[0].n = h;
+    sp[0].m_store = D;
+    sp[1].part[0].a = opnd(dZt, lth, Tp, h);
+    sp[1].part[0].b = opnd(Xt, ltx, Tp, d);
+    sp[1].part[0].k_len = kt;
+    sp[1].nparts = 1;
+    sp[1].m_extent = h;
+    sp[1].n = d;
+    sp[1].m_store = h;
+    EpiUpdate<E> epi;
+    epi.w2 = H->w2; epi.w2s = bf ? H->at<E>(Ly.w2c) : nullptr; epi.w2t = w2t;
+    epi.w1 = H->w1; epi.w1s = bf ? H->at<E>(Ly.w1c) : nullptr;
+    epi.ls2 = (long long)D * h; epi.ls1 = (long long)h * d;
+    epi.h = h; epi.d = d; epi.D = D; epi.shadows = bf ? 1 : 0; epi.lr = c.lr;
+    H->timing_begin(MONE_STAGE_UPD, s);
+    if ((e = launch_gemm<E>(pick_tile(D, h, Lc), sp, 2, Lc, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch UPD");
+    H->timing_end(MONE_STAGE_UPD, s);
+  }
+  H->last_n = n;
+  return MONE_OK;
+}
+
+template <typename E>
+int run_kv(mone_ttl* H, const void* xq, int q, void* kv, int kv_bf16, hipStream_t s) {
+  const mone_ttl_config& c = H->cfg;
+  const Layout& Ly = H->lay;
+  const int Lc = c.n_layers, d = c.d_model, h = c.d_hidden, D = 2 * c.d_kv, Tp = Ly.Tp;
+  const bool bf = sizeof(E) == 2;
+  const E* w1op = bf ? H->at<E>(Ly.w1c) : reinterpret_cast<const E*>(H->w1);
+  const E* w2op = bf ? H->at<E>(Ly.w2c) : reinterpret_cast<const E*>(H->w2);
+  E* A = H->at<E>(Ly.a);  // scratch for A_q (the TTL intermediates are dead between calls)
+  const long long lth = (long long)Tp * h;
+  const size_t kvE = kv_bf16 ? 2 : 4;
+  hipError_t e;
+  for (int q0 = 0; q0 < q; q0 += Tp) {
+    const int qc = q - q0 < Tp ? q - q0 : Tp;
+    const E* xc = reinterpret_cast<const E*>(xq) + (long long)q0 * d;
+    void* kvc = reinterpret_cast<unsigned char*>(kv) + (size_t)q0 * D * kvE;
+    {
+      Spec sp{};
+      sp.part[0].a = opnd(xc, (long long)q * d, d, qc);
+      sp.part[0].b = opnd(w1op, (long long)h * d, d, h);
+      sp.part[0].k_len = d;
+      sp.nparts = 1;
+      sp.m_extent = qc;
+      sp.n = h;
+      sp.m_store = -1;
+      EpiKv1<E> epi;
+      epi.a = A; epi.ls = lth; epi.h = h;
+      H->timing_begin(MONE_STAGE_KV1, s);
+      if ((e = launch_gemm<E>(pick_tile(qc, h, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
+        return hip_fail(e, "launch KV1");
+      H->timing_end(MONE_STAGE_KV1, s);
+    }
+    {
+      Spec sp{};
+      sp.part[0].a = opnd(A, lth, h, qc);
+      sp.part[0].b = opnd(w2op, (long long)D * h, h, D);
+      sp.part[0].k_len = h;
+      sp.nparts = 1;
+      sp.m_extent = qc;
+      sp.n = D;
+      sp.m_store = qc;
+      EpiKv2 epi;
+      epi.kv = kvc; epi.ls = (long long)q * D; epi.D = D; epi.bf16_out = kv_bf16;
+      H->timing_begin(MONE_STAGE_KV2, s);
+      if ((e = launch_gemm<E>(pick_tile(qc, D, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
+        return hip_fail(e, "launch KV2");
+      H->timing_end(MONE_STAGE_KV2, s);
+    }
+  }
+  return MONE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t mone_ttl_workspace_bytes(const mone_ttl_config* cfg) {
+  g_err[0] = 0;
+  if (check_config(cfg) != MONE_OK) return 0;
+  return make_layout(cfg).total;
+}
+
+int mone_ttl_init(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, float* w1,
+                  float* w2, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  if (!out) return fail(MONE_EINVAL, "out is NULL");
+  *out = nullptr;
+  int rc = check_config(cfg);
+  if (rc != MONE_OK) return rc;
+  if (!wkv || !w1 || !w2 || !workspace)
+    return fail(MONE_EINVAL, "wkv, w1, w2 and workspace must be non-NULL");
+  if (!aligned16(wkv) || !aligned16(w1) || !aligned16(w2))
+    return fail(MONE_EINVAL, "wkv, w1 and w2 must be 16-byte aligned");
+  if (((uintptr_t)workspace & (kAlign - 1)) != 0)
+    return fail(MONE_EINVAL, "workspace must be 256-byte aligned");
+  const Layout Ly = make_layout(cfg);
+  if (workspace_bytes < Ly.total)
+    return fail(MONE_EINVAL, "workspace has %zu bytes, %zu needed", workspace_bytes, Ly.total);
+
+  mone_ttl* H = new (std::nothrow) mone_ttl();
+  if (!H) return fail(MONE_EINVAL, "host allocation failed");
+  H->cfg = *cfg;
+  H->lay = Ly;
+  H->wkv = wkv;
+  H->w1 = w1;
+  H->w2 = w2;
+  H->ws = reinterpret_cast<unsigned char*>(workspace);
+  H->last_n = 0;
+  H->last_loss_count = 0;
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int Lc = cfg->n_layers, d = cfg->d_model, h = cfg->d_hidden, D = 2 * cfg->d_kv;
+  hipError_t e = hipMemsetAsync(workspace, 0, Ly.total, s);
+  if (e != hipSuccess) {
+    delete H;
+    return hip_fail(e, "clearing the workspace");
+  }
+  if (cfg->act_dtype == MONE_BF16) {
+    const long long n1 = (long long)Lc * h * d, n2 = (long long)Lc * D * h;
+    convert_bf16_kernel<<<dim3(2048), dim3(256), 0, s>>>(w1, H->at<bf16_t>(Ly.w1c), n1);
+    convert_bf16_kernel<<<dim3(2048), dim3(256), 0, s>>>(w2, H->at<bf16_t>(Ly.w2c), n2);
+    transpose_kernel<float, bf16_t><<<dim3((h + 63) / 64, (D + 63) / 64, Lc), dim3(256), 0, s>>>(
+        w2, (long long)D * h, h, D, h, H->at<bf16_t>(Ly.w2t), (long long)h * D, D, D);
+  } else {
+    transpose_kernel<float, float><<<dim3((h + 63) / 64, (D + 63) / 64, Lc), dim3(256), 0, s>>>(
+        w2, (long long)D * h, h, D, h, H->at<float>(Ly.w2t), (long long)h * D, D, D);
+  }
+  if ((e = hipGetLastError()) != hipSuccess) {
+    delete H;
+    return hip_fail(e, "building the weight copies");
+  }
+  *out = H;
+  return MONE_OK;
+}
+
+int mone_ttl_segment(mone_ttl* H, const void* x, int32_t n_tokens, void* stream) {
+  g_err[0] = 0;
+  if (!H) return fail(MONE_EINVAL, "handle is NULL");
+  if (n_tokens < 0 || n_tokens > H->cfg.seg_len)
+    return fail(MONE_EINVAL, "n_tokens %d outside [0, seg_len=%d]", n_tokens, H->cfg.seg_len);
+  if (n_tokens == 0) return MONE_OK;
+  if (!x) return fail(MONE_EINVAL, "x is NULL");
+  if (!aligned16(x)) return fail(MONE_EINVAL, "x must be 16-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  return H->cfg.act_dtype == MONE_BF16 ? run_segment<bf16_t>(H, x, n_tokens, s)
+                                       : run_segment<float>(H, x, n_tokens, s);
+}
+
+int mone_memory_kv(mone_ttl* H, const void* xq, int32_t q, void* kv, int32_t kv_dtype,
+                   void* stream) {
+  g_err[0] = 0;
+  if (!H) return fail(MONE_EINVAL, "handle is NULL");
+  if (q < 0) return fail(MONE_EINVAL, "q = %d is negative", q);
+  if (kv_dtype != MONE_F32 && kv_dtype != MONE_BF16)
+    return fail(MONE_EINVAL, "kv_dtype %d is not MONE_F32 or MONE_BF16", kv_dtype);
+  if (q == 0) return MONE_OK;
+  if (!xq || !kv) return fail(MONE_EINVAL, "xq and kv must be non-NULL");
+  if (!aligned16(xq) || !aligned16(kv)) return fail(MONE_EINVAL, "xq and kv must be 16-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int kvb = kv_dtype == MONE_BF16 ? 1 : 0;
+  return H->cfg.act_dtype == MONE_BF16 ? run_kv<bf16_t>(H, xq, q, kv, kvb, s)
+                                       : run_kv<float>(H, xq, q, kv, kvb, s);
+}
+
+int mone_ttl_loss(mone_ttl* H, float* out_host, void* stream) {
+  g_err[0] = 0;
+  if (!H || !out_host) return fail(MONE_EINVAL, "handle and out_host must be non-NULL");
+  if (H->last_n == 0) return fail(MONE_ESTATE, "no non-empty segment has been processed");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const mone_ttl_config& c = H->cfg;
+  const float n = (float)H->last_n;
+  const float scale = c.loss == MONE_LOSS_MSE_SUM ? 1.0f / n : 1.0f / (n * 2.0f * c.d_kv);
+  float* dev_out = H->at<float>(H->lay.loss_out);
+  loss_finalize_kernel<<<dim3(c.n_layers), dim3(256), 0, s>>>(
+      H->at<float>(H->lay.loss_part), H->lay.loss_per_layer, H->last_loss_count, scale, dev_out);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "launch loss");
+  if ((e = hipMemcpyAsync(out_host, dev_out, sizeof(float) * c.n_layers, hipMemcpyDeviceToHost,
+                          s)) != hipSuccess)
+    return hip_fail(e, "copy loss");
+  if ((e = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(e, "synchronise");
+  return MONE_OK;
+}
+
+int mone_ttl_destroy(mone_ttl* H) {
+  g_err[0] = 0;
+  if (!H) return MONE_OK;
+  H->destroy_events();
+  delete H;
+  return MONE_OK;
+}
+
+const char* mone_ttl_last_error(void) { return g_err; }
+
+int mone_ttl_set_stage_timing(mone_ttl* H, int32_t max_records) {
+  g_err[0] = 0;
+  if (!H) return fail(MONE_EINVAL, "handle is NULL");
+  if (max_records < 0) return fail(MONE_EINVAL, "max_records is negative");
+  H->destroy_events();
+  if (max_records == 0) return MONE_OK;
+  H->ev.assign(2 * (size_t)max_records, nullptr);
+  H->ev_stage.assign((size_t)max_records, 0);
+  for (size_t i = 0; i < H->ev.size(); ++i) {
+    hipError_t e = hipEventCreate(&H->ev[i]);
+    if (e != hipSuccess) {
+      H->ev.resize(i);
+      H->destroy_events();
+      return hip_fail(e, "hipEventCreate");
+    }
+  }
+  H->ev_cap = max_records;
+  H->ev_used = 0;
+  return MONE_OK;
+}
+
+int mone_ttl_stage_times(mone_ttl* H, double* ms_sum, int32_t* count) {
+  g_err[0] = 0;
+  if (!H || !ms_sum || !count) return fail(MONE_EINVAL, "NULL argument");
+  for (int i = 0; i < MONE_N_STAGES; ++i) {
+    ms_sum[i] = 0.0;
+    count[i] = 0;
+  }
+  for (int i = 0; i < H->ev_used; ++i) {
+    hipError_t e = hipEventSynchronize(H->ev[2 * i + 1]);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    float ms = 0.0f;
+    if ((e = hipEventElapsedTime(&ms, H->ev[2 * i], H->ev[2 * i + 1])) != hipSuccess)
+      return hip_fail(e, "hipEventElapsedTime");
+    ms_sum[H->ev_stage[i]] += ms;
+    count[H->ev_stage[i]] += 1;
+  }
+  H->ev_used = 0;
+  return MONE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,197 @@
+"""Python binding of libmone_ttl.so (the C ABI in include/mone_ttl.h).
+
+Argument marshalling only: every function forwards to the C call of the same name.  Device
+buffers are passed as torch tensors (their data_ptr()) or as raw integer addresses, streams as
+torch.cuda.Stream objects, raw hipStream_t integers, or None for torch's current stream.
+PyTorch is used only to own device memory and streams.
+
+The library must have been built (``python -m paper_2608_17616_amd.build``); loading fails
+loudly otherwise -- there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libmone_ttl.so")
+
+MONE_OK, MONE_EINVAL, MONE_EUNSUPPORTED, MONE_EHIP, MONE_ESTATE = 0, -1, -2, -3, -4
+MONE_F32, MONE_BF16 = 0, 1
+MONE_LOSS_MSE_SUM, MONE_LOSS_MSE_MEAN = 0, 1
+STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2")
+MONE_N_STAGES = len(STAGES)
+
+# every symbol include/mone_ttl.h declares
+EXPORTS = ("mone_ttl_workspace_bytes", "mone_ttl_init", "mone_ttl_segment", "mone_memory_kv",
+           "mone_ttl_loss", "mone_ttl_destroy", "mone_ttl_last_error",
+           "mone_ttl_set_stage_timing", "mone_ttl_stage_times")
+
+
+class MoneError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"[{code}] {message}")
+        self.code = code
+
+
+class mone_ttl_config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("d_hidden", ctypes.c_int32), ("d_kv", ctypes.c_int32),
+                ("seg_len", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
+                ("loss", ctypes.c_int32), ("lr", ctypes.c_float)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2608_17616_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32 = ctypes.c_void_p, ctypes.c_int32
+        cfgp = ctypes.POINTER(mone_ttl_config)
+        L.mone_ttl_workspace_bytes.argtypes = [cfgp]
+        L.mone_ttl_workspace_bytes.restype = ctypes.c_size_t
+        L.mone_ttl_init.argtypes = [ctypes.POINTER(vp), cfgp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        L.mone_ttl_segment.argtypes = [vp, vp, i32, vp]
+        L.mone_memory_kv.argtypes = [vp, vp, i32, vp, i32, vp]
+        L.mone_ttl_loss.argtypes = [vp, ctypes.POINTER(ctypes.c_float), vp]
+        L.mone_ttl_destroy.argtypes = [vp]
+        L.mone_ttl_last_error.argtypes = []
+        L.mone_ttl_last_error.restype = ctypes.c_char_p
+        L.mone_ttl_set_stage_timing.argtypes = [vp, i32]
+        L.mone_ttl_stage_times.argtypes = [vp, ctypes.POINTER(ctypes.c_double),
+                                           ctypes.POINTER(ctypes.c_int32)]
+        for name in EXPORTS:
+            if name not in ("mone_ttl_workspace_bytes", "mone_ttl_last_error"):
+                getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc: int) -> None:
+    if rc != MONE_OK:
+        raise MoneError(rc, mone_ttl_last_error())
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(s) -> int | None:
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def make_config(n_layers, d_model, d_hidden, d_kv, seg_len, act_dtype, loss, lr):
+    dt = {"f32": MONE_F32, "bf16": MONE_BF16}.get(act_dtype, act_dtype)
+    ls = {"mse_sum": MONE_LOSS_MSE_SUM, "mse_mean": MONE_LOSS_MSE_MEAN}.get(loss, loss)
+    return mone_ttl_config(int(n_layers), int(d_model), int(d_hidden), int(d_kv), int(seg_len),
+                           int(dt), int(ls), float(lr))
+
+
+def config_from(cfg) -> mone_ttl_config:
+    """C config of a configs.MoneConfig."""
+    return make_config(cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_kv, cfg.seg_len,
+                       cfg.act_dtype, cfg.loss, cfg.lr)
+
+
+def mone_ttl_last_error() -> str:
+    return lib().mone_ttl_last_error().decode()
+
+
+def mone_ttl_workspace_bytes(cfg: mone_ttl_config) -> int:
+    n = lib().mone_ttl_workspace_bytes(ctypes.byref(cfg))
+    if n == 0:
+        raise MoneError(MONE_EINVAL, mone_ttl_last_error())
+    return n
+
+
+def mone_ttl_init(cfg: mone_ttl_config, wkv, w1, w2, workspace, workspace_bytes: int,
+                  stream=None) -> int:
+    h = ctypes.c_void_p()
+    _check(lib().mone_ttl_init(ctypes.byref(h), ctypes.byref(cfg), _ptr(wkv), _ptr(w1), _ptr(w2),
+                               _ptr(workspace), int(workspace_bytes), _stream(stream)))
+    return h.value
+
+
+def mone_ttl_segment(handle: int, x, n_tokens: int, stream=None) -> None:
+    _check(lib().mone_ttl_segment(handle, _ptr(x), int(n_tokens), _stream(stream)))
+
+
+def mone_memory_kv(handle: int, xq, q: int, kv, kv_dtype: int, stream=None) -> None:
+    _check(lib().mone_memory_kv(handle, _ptr(xq), int(q), _ptr(kv), int(kv_dtype),
+                                _stream(stream)))
+
+
+def mone_ttl_loss(handle: int, n_layers: int, stream=None) -> list[float]:
+    out = (ctypes.c_float * n_layers)()
+    _check(lib().mone_ttl_loss(handle, out, _stream(stream)))
+    return list(out)
+
+
+def mone_ttl_destroy(handle: int) -> None:
+    _check(lib().mone_ttl_destroy(handle))
+
+
+def mone_ttl_set_stage_timing(handle: int, max_records: int) -> None:
+    _check(lib().mone_ttl_set_stage_timing(handle, int(max_records)))
+
+
+def mone_ttl_stage_times(handle: int) -> dict:
+    ms = (ctypes.c_double * MONE_N_STAGES)()
+    cnt = (ctypes.c_int32 * MONE_N_STAGES)()
+    _check(lib().mone_ttl_stage_times(handle, ms, cnt))
+    return {name: (ms[i], cnt[i]) for i, name in enumerate(STAGES)}
+
+
+class TtlSession:
+    """Device state of one TTL run: the caller-owned tensors the C ABI borrows, and a handle.
+
+    w1 [L, h, d] fp32, w2 [L, D, h] fp32 and wkv [L, D, d] (activation dtype) are torch tensors
+    on the GPU; the workspace is allocated here with torch (the library allocates nothing).
+    """
+
+    def __init__(self, cfg, wkv, w1, w2, stream=None):
+        import torch
+        self.cfg = cfg
+        self.ccfg = config_from(cfg)
+        self.wkv, self.w1, self.w2 = wkv, w1, w2
+        self.ws_bytes = mone_ttl_workspace_bytes(self.ccfg)
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=w1.device)
+        self.handle = mone_ttl_init(self.ccfg, wkv, w1, w2, self.workspace, self.ws_bytes, stream)
+
+    def segment(self, x, n_tokens=None, stream=None):
+        n = x.shape[1] if n_tokens is None else n_tokens
+        mone_ttl_segment(self.handle, x, n, stream)
+
+    def memory_kv(self, xq, kv, stream=None):
+        import torch
+        dt = MONE_BF16 if kv.dtype == torch.bfloat16 else MONE_F32
+        mone_memory_kv(self.handle, xq, xq.shape[1], kv, dt, stream)
+        return kv
+
+    def loss(self, stream=None):
+        return mone_ttl_loss(self.handle, self.cfg.n_layers, stream)
+
+    def close(self):
+        if self.handle:
+            mone_ttl_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

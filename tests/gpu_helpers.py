@@ -1,0 +1,67 @@
+"""Shared set-up of the GPU tests: device problems whose checked layers come from the keyed
+input generator (so the oracle sees the same numbers) and whose other layers are drawn on the
+device (only the GPU path reads them; layers are independent, so they cannot influence the
+checked ones)."""
+from __future__ import annotations
+
+import numpy as np
+
+from paper_2608_17616_amd import inputs
+
+
+def rel_l2(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    den = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / (den if den > 0 else 1.0))
+
+
+class DeviceProblem:
+    def __init__(self, cfg, checked, seed_dev=1234, device="cuda"):
+        import torch
+        self.torch = torch
+        self.cfg = cfg
+        self.checked = list(checked)
+        self.device = device
+        self.act = torch.bfloat16 if cfg.act_dtype == "bf16" else torch.float32
+        self.gen = torch.Generator(device=device)
+        self.gen.manual_seed(seed_dev)
+        L, d, h, D = cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out
+        self.w1 = torch.empty(L, h, d, dtype=torch.float32, device=device)
+        self.w2 = torch.empty(L, D, h, dtype=torch.float32, device=device)
+        self.wkv = torch.empty(L, D, d, dtype=self.act, device=device)
+        inputs.device_normal_(self.w1, 1 / np.sqrt(d), self.gen)
+        inputs.device_normal_(self.w2, 1 / np.sqrt(h), self.gen)
+        inputs.device_normal_(self.wkv, 1 / np.sqrt(d), self.gen)
+        self.host = {}
+        for l in self.checked:
+            w1, w2, wkv = inputs.layer_w1(cfg, l), inputs.layer_w2(cfg, l), inputs.layer_wkv(cfg, l)
+            self.host[l] = dict(w1=w1, w2=w2, wkv=wkv, x=[])
+            self.w1[l].copy_(torch.from_numpy(w1))
+            self.w2[l].copy_(torch.from_numpy(w2))
+            self.wkv[l].copy_(torch.from_numpy(wkv))
+
+    def segment(self, s, n_tokens=None):
+        """Device X [L, n, d] of segment s; records the checked layers' host copies."""
+        torch = self.torch
+        cfg = self.cfg
+        n = cfg.seg_len if n_tokens is None else n_tokens
+        x = torch.empty(cfg.n_layers, n, cfg.d_model, dtype=self.act, device=self.device)
+        inputs.device_normal_(x, 1.0, self.gen)
+        for l in self.checked:
+            xs = inputs.segment_x(cfg, l, s, n)
+            self.host[l]["x"].append(xs)
+            x[l].copy_(torch.from_numpy(xs))
+        return x
+
+    def query(self, q=None, index=0):
+        torch = self.torch
+        cfg = self.cfg
+        q = cfg.n_query if q is None else q
+        xq = torch.empty(cfg.n_layers, q, cfg.d_model, dtype=self.act, device=self.device)
+        inputs.device_normal_(xq, 1.0, self.gen)
+        hx = {}
+        for l in self.checked:
+            hx[l] = inputs.query_x(cfg, l, q, index)
+            xq[l].copy_(torch.from_numpy(hx[l]))
+        return xq, hx

@@ -1,0 +1,99 @@
+"""The C ABI on the CPU: the library loads, exports what the header declares, and rejects bad
+arguments on the host before any HIP call (no GPU is touched here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_17616_amd import configs, mone
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mone_ttl.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(mone.LIB_PATH),
+                                reason="libmone_ttl.so not built")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mone_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert header_functions() == sorted(mone.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = mone.lib()
+    for name in header_functions():
+        assert hasattr(L, name), name
+
+
+def _cfg(**kw):
+    base = dict(n_layers=2, d_model=128, d_hidden=192, d_kv=64, seg_len=100, act_dtype="bf16",
+                loss="mse_sum", lr=1e-3)
+    base.update(kw)
+    return mone.make_config(**base)
+
+
+def test_workspace_bytes_formula_and_independent_of_context_length():
+    c = _cfg()
+    n = mone.mone_ttl_workspace_bytes(c)
+    L, d, h, D, Tp, E = 2, 128, 192, 128, 256, 2
+    act = E * L * (h * d + D * h + h * D + 3 * Tp * h + 2 * Tp * D + h * Tp + d * Tp)
+    assert act <= n <= act + 64 * 1024
+    # the configs' context lengths never enter: N is not a parameter of any call
+    for cfg in configs.CONFIGS.values():
+        a = mone.mone_ttl_workspace_bytes(mone.config_from(cfg))
+        b = mone.mone_ttl_workspace_bytes(mone.config_from(cfg.with_(n_context=cfg.n_context * 8)))
+        assert a == b
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n_layers=0), mone.MONE_EINVAL),
+    (dict(seg_len=0), mone.MONE_EINVAL),
+    (dict(act_dtype=7), mone.MONE_EINVAL),
+    (dict(loss=3), mone.MONE_EINVAL),
+    (dict(lr=float("nan")), mone.MONE_EINVAL),
+    (dict(d_model=100), mone.MONE_EUNSUPPORTED),
+    (dict(d_kv=32), mone.MONE_EUNSUPPORTED),
+    (dict(seg_len=70000), mone.MONE_EUNSUPPORTED),
+])
+def test_invalid_configs_are_rejected(kw, code):
+    c = _cfg(**kw)
+    assert mone.lib().mone_ttl_workspace_bytes(ctypes.byref(c)) == 0
+    assert mone.mone_ttl_last_error()
+    h = ctypes.c_void_p(1234)
+    rc = mone.lib().mone_ttl_init(ctypes.byref(h), ctypes.byref(c), 16, 16, 16, 256, 1 << 30,
+                                  None)
+    assert rc == code and h.value is None
+
+
+def test_init_argument_checks_before_any_hip_call():
+    c = _cfg()
+    need = mone.mone_ttl_workspace_bytes(c)
+    L = mone.lib()
+    h = ctypes.c_void_p()
+    assert L.mone_ttl_init(None, ctypes.byref(c), 16, 16, 16, 256, need, None) == mone.MONE_EINVAL
+    assert L.mone_ttl_init(ctypes.byref(h), None, 16, 16, 16, 256, need, None) == mone.MONE_EINVAL
+    assert L.mone_ttl_init(ctypes.byref(h), ctypes.byref(c), None, 16, 16, 256, need,
+                           None) == mone.MONE_EINVAL
+    assert L.mone_ttl_init(ctypes.byref(h), ctypes.byref(c), 16, 16, 24, 256, need,
+                           None) == mone.MONE_EINVAL          # misaligned w2
+    assert L.mone_ttl_init(ctypes.byref(h), ctypes.byref(c), 16, 16, 16, 272, need,
+                           None) == mone.MONE_EINVAL          # workspace not 256-aligned
+    assert L.mone_ttl_init(ctypes.byref(h), ctypes.byref(c), 16, 16, 16, 256, need - 1,
+                           None) == mone.MONE_EINVAL          # workspace too small
+    assert "workspace" in mone.mone_ttl_last_error()
+
+
+def test_null_handle_calls_fail_cleanly():
+    L = mone.lib()
+    assert L.mone_ttl_segment(None, 16, 1, None) == mone.MONE_EINVAL
+    assert L.mone_memory_kv(None, 16, 1, 16, 0, None) == mone.MONE_EINVAL
+    out = (ctypes.c_float * 1)()
+    assert L.mone_ttl_loss(None, out, None) == mone.MONE_EINVAL
+    assert L.mone_ttl_destroy(None) == mone.MONE_OK
+    assert L.mone_ttl_set_stage_timing(None, 4) == mone.MONE_EINVAL
