@@ -74,7 +74,7 @@ struct Part {              // one K-range of the contraction: sum_k a(m, k) b(n,
 };
 
 struct Problem {
-  Part part[2];            // K-concatenated parts; the result is part0 - part1 when nparts == 2
+  Part part[2];            // K-concatenated parts: the result is their sum
   int nparts;
   int M, N;                // output rows/cols that are stored (bounds of the epilogue)
   int tiles_m, tiles_n;    // tiles per layer
@@ -91,28 +91,69 @@ struct GemmLaunch {
 // ------------------------------------------------------------------------------------------
 // The grouped GEMM kernel
 
-template <typename E, int BM, int BN, class Epi>
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer load of 4 bytes x size/4 per lane straight into LDS (no VGPR staging): lane l's data
+// lands at M0 + 16*l for 16-byte loads; offsets at or beyond the descriptor's byte count read 0.
+__device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t* lds,
+                                    int size, int voffset, int soffset, int offset,
+                                    int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+
+// Raw buffer descriptor over [p, p + bytes): stride 0, range-checked by byte offset.
+__device__ __forceinline__ i32x4 make_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  i32x4 r;
+  r[0] = (int32_t)(uint32_t)(a & 0xffffffffu);
+  r[1] = (int32_t)(uint32_t)((a >> 32) & 0xffffu);
+  r[2] = (int32_t)bytes;
+  r[3] = 0x00020000;
+  return r;
+}
+
+// Workgroup -> tile.  Workgroups are dispatched round-robin over the 8 XCDs (bid % 8), each
+// with its own L2: the bids of one XCD get one contiguous run of the problem's (layer, tile)
+// sequence, so a layer's tiles share an L2.  Within a layer, tiles go in groups of GM tile
+// rows, column-major inside a group, so concurrently running tiles reuse A and B panels.
+__device__ __forceinline__ void map_tile(int local, int total, int tiles_m, int tiles_n,
+                                         int* layer, int* tm, int* tn) {
+  constexpr int NXCD = 8, GM = 4;
+  const int full = total - total % NXCD;
+  int v = local;
+  if (local < full) v = (local % NXCD) * (full / NXCD) + local / NXCD;
+  const int per_layer = tiles_m * tiles_n;
+  *layer = v / per_layer;
+  const int t = v - *layer * per_layer;
+  const int group = t / (GM * tiles_n);
+  const int first = group * GM;
+  const int gm = tiles_m - first < GM ? tiles_m - first : GM;
+  const int r = t - group * GM * tiles_n;
+  *tm = first + r % gm;
+  *tn = r / gm;
+}
+
+template <typename E, int BM, int BN, int WAVES_M, class Epi>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
-  constexpr int VEC = 16 / (int)sizeof(E);  // elements per 16-byte vector
-  constexpr int BK = 8 * VEC;               // K per tile: 8 vectors = 128 bytes per row
-  constexpr int AV = BM / 32, BV = BN / 32; // 16-byte vectors per thread per tile
-  constexpr int WM = BM / 2, WN = BN / 2;   // wave tile
-  constexpr int FM = WM / 32, FN = WN / 32; // 32x32 MFMA blocks per wave
-  constexpr int STAGE = (BM + BN) * 128;    // bytes of one LDS buffer (A then B)
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * STAGE];
+  constexpr int VEC = 16 / (int)sizeof(E);   // elements per 16-byte vector
+  constexpr int BK = 8 * VEC;                // K per tile: 8 vectors = 128 bytes per row
+  constexpr int WAVES_N = 4 / WAVES_M;
+  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;  // wave tile
+  constexpr int FM = WM / 32, FN = WN / 32;  // 32x32 MFMA blocks per wave
+  constexpr int LA = BM / 32, LB = BN / 32;  // 1 KiB load instructions per wave per stage
+  constexpr int STAGE = (BM + BN) * 128;     // bytes of one LDS stage (A rows, then B rows)
+  static_assert(FM >= 1 && FN >= 1 && WAVES_M * WAVES_N == 4, "tile shape");
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE];
 
   const int bid = blockIdx.x;
   const int pi = (G.nprob > 1 && bid >= G.prob[1].tile_begin) ? 1 : 0;
   const Problem& P = G.prob[pi];
-  const int local = bid - P.tile_begin;
-  const int per_layer = P.tiles_m * P.tiles_n;
-  const int layer = local / per_layer;
-  const int t = local - layer * per_layer;
-  const int tm = t / P.tiles_n, tn = t - (t / P.tiles_n) * P.tiles_n;
+  const int total = G.nprob > 1 && pi == 0 ? G.prob[1].tile_begin : (int)gridDim.x - P.tile_begin;
+  int layer, tm, tn;
+  map_tile(bid - P.tile_begin, total, P.tiles_m, P.tiles_n, &layer, &tm, &tn);
+  const int t = tm * P.tiles_n + tn;
   const int m0 = tm * BM, n0 = tn * BN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -125,48 +166,49 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   const int nk0 = P.part[0].k_len / BK;
   const int nk = nk0 + (P.nparts > 1 ? P.part[1].k_len / BK : 0);
 
-  u32x4 ra[AV], rb[BV];
+  // Per part: buffer descriptors over this layer's operand slices and each lane's byte offset
+  // of its first load.  Lane l of load instruction i fills LDS row 8*(4*i + wave) + l/8, slot
+  // l%8, and fetches the 16-byte vector (slot ^ swizzle(row)) of that row.
+  i32x4 ra[2], rb[2];
+  int oa[2], ob[2];
+  const int lrow = lane >> 3, lslot = lane & 7;
+#pragma unroll
+  for (int pp = 0; pp < 2; ++pp) {
+    const Part& Pt = P.part[pp < P.nparts ? pp : 0];
+    const E* A = reinterpret_cast<const E*>(Pt.a.p) + (long long)layer * Pt.a.lstride;
+    const E* B = reinterpret_cast<const E*>(Pt.b.p) + (long long)layer * Pt.b.lstride;
+    ra[pp] = make_rsrc(A, (uint32_t)((long long)Pt.a.rows * Pt.a.ld * (int)sizeof(E)));
+    rb[pp] = make_rsrc(B, (uint32_t)((long long)Pt.b.rows * Pt.b.ld * (int)sizeof(E)));
+    const int r = 8 * wave + lrow;  // row of load 0; load i adds 32 rows (same swizzle)
+    const int v = lslot ^ ((r >> 1) & 7);
+    oa[pp] = ((m0 + r) * Pt.a.ld + v * VEC) * (int)sizeof(E);
+    ob[pp] = ((n0 + r) * Pt.b.ld + v * VEC) * (int)sizeof(E);
+  }
 
-  auto gload = [&](int kt) {
+  auto issue_loads = [&](int kt, int stage) {
     const int pp = kt < nk0 ? 0 : 1;
-    const int k0 = (kt - (pp ? nk0 : 0)) * BK;
-    const Opnd& oa = P.part[pp].a;
-    const Opnd& ob = P.part[pp].b;
-    const E* A = reinterpret_cast<const E*>(oa.p) + (long long)layer * oa.lstride;
-    const E* B = reinterpret_cast<const E*>(ob.p) + (long long)layer * ob.lstride;
-#pragma unroll
-    for (int i = 0; i < AV; ++i) {
-      const int vid = tid + 256 * i, r = vid >> 3, v = vid & 7, gr = m0 + r;
-      ra[i] = gr < oa.rows
-                  ? *reinterpret_cast<const u32x4*>(A + (long long)gr * oa.ld + k0 + v * VEC)
-                  : u32x4{0u, 0u, 0u, 0u};
-    }
-#pragma unroll
-    for (int i = 0; i < BV; ++i) {
-      const int vid = tid + 256 * i, r = vid >> 3, v = vid & 7, gr = n0 + r;
-      rb[i] = gr < ob.rows
-                  ? *reinterpret_cast<const u32x4*>(B + (long long)gr * ob.ld + k0 + v * VEC)
-                  : u32x4{0u, 0u, 0u, 0u};
-    }
-  };
-
-  auto lds_store = [&](int buf) {
-    unsigned char* sa = smem + buf * STAGE;
+    const int k0 = (kt - (pp ? nk0 : 0)) * BK * (int)sizeof(E);
+    const Part& Pt = P.part[pp];
+    unsigned char* sa = smem + stage * STAGE;
     unsigned char* sb = sa + BM * 128;
 #pragma unroll
-    for (int i = 0; i < AV; ++i) {
-      const int vid = tid + 256 * i, r = vid >> 3, v = vid & 7;
-      *reinterpret_cast<u32x4*>(sa + r * 128 + ((v ^ ((r >> 1) & 7)) << 4)) = ra[i];
+    for (int i = 0; i < LA; ++i) {
+      auto* dst = reinterpret_cast<__attribute__((address_space(3))) uint32_t*>(
+          reinterpret_cast<uintptr_t>(sa + (4 * i + wave) * 1024));
+      raw_buffer_load_lds(ra[pp], dst, 16, oa[pp] + 32 * i * Pt.a.ld * (int)sizeof(E) + k0, 0,
+                          0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < BV; ++i) {
-      const int vid = tid + 256 * i, r = vid >> 3, v = vid & 7;
-      *reinterpret_cast<u32x4*>(sb + r * 128 + ((v ^ ((r >> 1) & 7)) << 4)) = rb[i];
+    for (int i = 0; i < LB; ++i) {
+      auto* dst = reinterpret_cast<__attribute__((address_space(3))) uint32_t*>(
+          reinterpret_cast<uintptr_t>(sb + (4 * i + wave) * 1024));
+      raw_buffer_load_lds(rb[pp], dst, 16, ob[pp] + 32 * i * Pt.b.ld * (int)sizeof(E) + k0, 0,
+                          0, 0);
     }
   };
 
-  auto compute = [&](int buf) {
-    const unsigned char* sa = smem + buf * STAGE;
+  auto compute = [&](int stage) {
+    const unsigned char* sa = smem + stage * STAGE;
     const unsigned char* sb = sa + BM * 128;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
@@ -200,30 +242,15 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     }
   };
 
-  const bool two = P.nparts > 1 && nk > nk0;
   if (nk > 0) {
-    gload(0);
-    lds_store(0);
+    issue_loads(0, 0);
+    __builtin_amdgcn_s_waitcnt(0);  // all counters 0: this wave's loads have reached LDS
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
-      const bool more = kt + 1 < nk;
-      if (more) gload(kt + 1);
+      if (kt + 1 < nk) issue_loads(kt + 1, (kt + 1) & 1);
       compute(kt & 1);
-      if (two && kt + 1 == nk0) {
-        // switch to the subtracted part: acc = -(part0); ... ; result = -(acc) = part0 - part1
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j) acc[i][j] = -acc[i][j];
-      }
-      if (more) lds_store((kt + 1) & 1);
+      __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-    }
-    if (two) {
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = -acc[i][j];
     }
   }
 
@@ -286,8 +313,9 @@ struct EpiFwd1 : NoFinish {
   }
 };
 
-// Forward 2 and loss gradient: R = A W2^T - X W_kv^T  ->  G = c R in [Tp][D] and [D][Tp];
-// sum of R^2 per wave into loss partials.
+// Forward 2 and loss gradient.  The GEMM computes -R = A (-W2)^T + X W_kv^T (K-concatenated,
+// from the negated copy of W2), so R = Y - targets is the negated result.  Stores G = c R in
+// [Tp][D] and [D][Tp]; sums R^2 per wave into the loss partials.
 template <typename E>
 struct EpiFwd2 {
   E* g; E* gt;
@@ -298,7 +326,7 @@ struct EpiFwd2 {
   __device__ __forceinline__ float apply(int, int layer, int row, int col, int, int N, float r0,
                                          float r1, float r2, float r3) const {
     if (col >= N) return 0.0f;
-    float r[4] = {r0, r1, r2, r3};
+    float r[4] = {-r0, -r1, -r2, -r3};
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       if (row + i >= n) r[i] = 0.0f;
@@ -337,15 +365,16 @@ struct EpiBwd : NoFinish {
 
 // SGD update of both matrices in one launch.  Problem 0: G^T A = dL/dW2 tile of W2 [D][h];
 // problem 1: dZ^T X = dL/dW1 tile of W1 [h][d].  fp32 read-modify-write of the masters, then
-// the activation-dtype copies the next segment's forward and backward read (bf16 mode:
-// W1 and W2 rounded; both modes: W2^T).
+// the activation-dtype copies the next segment's GEMMs read: -W2 [D][h] (forward 2 and the
+// read) and W2^T [h][D] (backward) in both modes, W1 [h][d] in bf16 mode (fp32 mode reads the
+// master).
 template <typename E>
 struct EpiUpdate : NoFinish {
-  float* w2; E* w2s; E* w2t;
+  float* w2; E* w2n; E* w2t;
   float* w1; E* w1s;
   long long ls2, ls1;  // D*h, h*d
   int h, d, D;
-  int shadows;         // write w1s / w2s (bf16 mode)
+  int w1_copy;         // write w1s (bf16 mode)
   float lr;
   __device__ __forceinline__ float apply(int pi, int layer, int row, int col, int M, int N,
                                          float g0, float g1, float g2, float g3) const {
@@ -359,7 +388,7 @@ struct EpiUpdate : NoFinish {
         const long long idx = base + (long long)(row + i) * h + col;
         nw[i] = w2[idx] - lr * gv[i];
         w2[idx] = nw[i];
-        if (shadows) w2s[idx] = from_f32<E>(nw[i]);
+        w2n[idx] = from_f32<E>(-nw[i]);
       }
       store4(w2t + base + (long long)col * D + row, nw[0], nw[1], nw[2], nw[3]);
     } else {
@@ -369,7 +398,7 @@ struct EpiUpdate : NoFinish {
         const long long idx = base + (long long)(row + i) * d + col;
         const float w = w1[idx] - lr * gv[i];
         w1[idx] = w;
-        if (shadows) w1s[idx] = from_f32<E>(w);
+        if (w1_copy) w1s[idx] = from_f32<E>(w);
       }
     }
     return 0.0f;
@@ -394,7 +423,8 @@ struct EpiKv1 : NoFinish {
   }
 };
 
-// Read, second layer: KV = A_q W2^T into the caller's [L][q][D] output (fp32 or bf16).
+// Read, second layer: the GEMM computes A_q (-W2)^T = -KV; stores KV into the caller's
+// [L][q][D] output (fp32 or bf16).
 struct EpiKv2 : NoFinish {
   void* kv;
   long long ls;  // q*D
@@ -403,7 +433,7 @@ struct EpiKv2 : NoFinish {
   __device__ __forceinline__ float apply(int, int layer, int row, int col, int M, int N, float y0,
                                          float y1, float y2, float y3) const {
     if (col >= N) return 0.0f;
-    const float y[4] = {y0, y1, y2, y3};
+    const float y[4] = {-y0, -y1, -y2, -y3};
     const long long base = (long long)layer * ls + col;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -443,12 +473,13 @@ __global__ __launch_bounds__(256) void transpose_kernel(const Ein* __restrict__ 
   }
 }
 
-// dst[i] = activation-dtype copy of src[i] (fp32 -> bf16, nearest even).
-__global__ void convert_bf16_kernel(const float* __restrict__ src, bf16_t* __restrict__ dst,
-                                    long long n) {
+// dst[i] = sign * src[i] in the destination dtype (fp32 -> bf16: nearest even).
+template <typename Eout>
+__global__ void convert_kernel(const float* __restrict__ src, Eout* __restrict__ dst, long long n,
+                               float sign) {
   for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (long long)gridDim.x * blockDim.x)
-    dst[i] = from_f32<bf16_t>(src[i]);
+    dst[i] = from_f32<Eout>(sign * src[i]);
 }
 
 // out[l] = scale * sum of the loss partials of layer l (fixed order: deterministic).

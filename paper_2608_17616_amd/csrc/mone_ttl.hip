@@ -5,7 +5,8 @@
 // Data layout in HBM (row-major; "[L]" = the L layers back to back):
 //   caller state   W1 [L][h][d] fp32, W2 [L][D][h] fp32, W_kv [L][D][d] act
 //   workspace      W1c [L][h][d] act   (bf16 mode only: MFMA copy of W1; fp32 mode reads W1)
-//                  W2c [L][D][h] act   (bf16 mode only)
+//                  W2n [L][D][h] act   -W2 (forward 2 and the read: the residual Y - targets
+//                                      becomes one K-concatenated sum, negated in the epilogue)
 //                  W2t [L][h][D] act   W2 transposed (B operand of the backward GEMM)
 //                  A   [L][Tp][h], A^T [L][h][Tp], SiLU'(Z) [L][Tp][h]
 //                  G   [L][Tp][D], G^T [L][D][Tp]
@@ -17,7 +18,7 @@
 // A segment step is five launches on the caller's stream, each grouped over all L layers:
 //   XT   X -> X^T
 //   FWD1 Z = X W1^T                      epilogue: A, A^T, SiLU'(Z)
-//   FWD2 R = [A | X] [W2 | W_kv]^T-split epilogue: G = c R, G^T, sum R^2 partials
+//   FWD2 -R = [A | X] [-W2 | W_kv]^T     epilogue: G = c R, G^T, sum R^2 partials
 //   BWD  dA = G W2                       epilogue: dZ^T = (dA * SiLU'(Z))^T
 //   UPD  G^T A and dZ^T X (2 problems)   epilogue: fp32 SGD read-modify-write + copies
 #include <hip/hip_runtime.h>
@@ -78,9 +79,11 @@ int check_config(const mone_ttl_config* c) {
   const long long Tp = round_up(c->seg_len, 256);
   const long long d = c->d_model, h = c->d_hidden, D = 2LL * c->d_kv;
   const long long mx = d > h ? (d > D ? d : D) : (h > D ? h : D);
-  if (h * d >= (1LL << 31) || D * h >= (1LL << 31) || D * d >= (1LL << 31) ||
-      Tp * mx >= (1LL << 31))
-    return fail(MONE_EUNSUPPORTED, "a per-layer matrix exceeds 2^31 elements");
+  const long long E = c->act_dtype == MONE_BF16 ? 2 : 4;
+  // per-layer operand slices are addressed with 32-bit byte offsets; fp32 masters are 4 bytes
+  if (h * d * 4 >= (1LL << 31) || D * h * 4 >= (1LL << 31) || D * d * E >= (1LL << 31) ||
+      Tp * mx * E >= (1LL << 31))
+    return fail(MONE_EUNSUPPORTED, "a per-layer matrix exceeds 2^31 bytes");
   return MONE_OK;
 }
 
@@ -101,7 +104,7 @@ Layout make_layout(const mone_ttl_config* c) {
   };
   const bool bf = c->act_dtype == MONE_BF16;
   L.w1c = bf ? take(nl * h * d * E) : 0;
-  L.w2c = bf ? take(nl * D * h * E) : 0;
+  L.w2c = take(nl * D * h * E);
   L.w2t = take(nl * h * D * E);
   L.a = take(nl * Tp * h * E);
   L.at = take(nl * h * Tp * E);
@@ -118,13 +121,17 @@ Layout make_layout(const mone_ttl_config* c) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-enum TileShape { TILE_128x128 = 0, TILE_64x256 = 1 };
+enum TileShape { TILE_256x256 = 0, TILE_128x128 = 1, TILE_64x256 = 2 };
 
-// 64-row tiles for short token extents (short segments, query batches), 128 x 128 otherwise.
+constexpr int kNumCUs = 256;
+
+// 64-row tiles for short token extents (short segments, query batches); 256 x 256 when the
+// grouped problem still has at least one such tile per CU; 128 x 128 otherwise.
 TileShape pick_tile(int m, int n, int layers) {
-  (void)n;
-  (void)layers;
-  return m <= 64 ? TILE_64x256 : TILE_128x128;
+  if (m <= 64) return TILE_64x256;
+  const long long big = (long long)((m + 255) / 256) * ((n + 255) / 256) * layers;
+  if (m >= 256 && n >= 256 && big >= kNumCUs) return TILE_256x256;
+  return TILE_128x128;
 }
 
 // Host description of one grouped problem before the tile shape fixes its tiling.
@@ -145,7 +152,7 @@ Opnd opnd(const void* p, long long lstride, int ld, int rows) {
   return o;
 }
 
-template <typename E, int BM, int BN, class Epi>
+template <typename E, int BM, int BN, int WAVES_M, class Epi>
 hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi,
                         hipStream_t s, int* tiles_per_layer0) {
   GemmLaunch<Epi> G;
@@ -167,16 +174,21 @@ hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi
   G.epi = epi;
   if (tiles_per_layer0) *tiles_per_layer0 = G.prob[0].tiles_m * G.prob[0].tiles_n;
   if (begin == 0) return hipSuccess;
-  gemm_nt_kernel<E, BM, BN, Epi><<<dim3(begin), dim3(256), 0, s>>>(G);
+  gemm_nt_kernel<E, BM, BN, WAVES_M, Epi><<<dim3(begin), dim3(256), 0, s>>>(G);
   return hipGetLastError();
 }
 
 template <typename E, class Epi>
 hipError_t launch_gemm(TileShape t, const Spec* specs, int nspec, int layers, const Epi& epi,
                        hipStream_t s, int* tiles_per_layer0 = nullptr) {
-  if (t == TILE_64x256)
-    return launch_tiled<E, 64, 256>(specs, nspec, layers, epi, s, tiles_per_layer0);
-  return launch_tiled<E, 128, 128>(specs, nspec, layers, epi, s, tiles_per_layer0);
+  switch (t) {
+    case TILE_256x256:
+      return launch_tiled<E, 256, 256, 2>(specs, nspec, layers, epi, s, tiles_per_layer0);
+    case TILE_128x128:
+      return launch_tiled<E, 128, 128, 2>(specs, nspec, layers, epi, s, tiles_per_layer0);
+    default:
+      return launch_tiled<E, 64, 256, 1>(specs, nspec, layers, epi, s, tiles_per_layer0);
+  }
 }
 
 }  // namespace
@@ -227,7 +239,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
   constexpr int BK = 8 * (16 / (int)sizeof(E));
   const bool bf = sizeof(E) == 2;
   const E* w1op = bf ? H->at<E>(Ly.w1c) : reinterpret_cast<const E*>(H->w1);
-  const E* w2op = bf ? H->at<E>(Ly.w2c) : reinterpret_cast<const E*>(H->w2);
+  const E* w2neg = H->at<E>(Ly.w2c);
   E* w2t = H->at<E>(Ly.w2t);
   E* A = H->at<E>(Ly.a);
   E* At = H->at<E>(Ly.at);
@@ -265,11 +277,11 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
       return hip_fail(e, "launch FWD1");
     H->timing_end(MONE_STAGE_FWD1, s);
   }
-  // FWD2: R = A W2^T - X W_kv^T  ->  G = c R, G^T, loss partials
+  // FWD2: -R = A (-W2)^T + X W_kv^T  ->  G = c R, G^T, loss partials
   {
     Spec sp{};
     sp.part[0].a = opnd(A, lth, h, n);
-    sp.part[0].b = opnd(w2op, (long long)D * h, h, D);
+    sp.part[0].b = opnd(w2neg, (long long)D * h, h, D);
     sp.part[0].k_len = h;
     sp.part[1].a = opnd(x, lsx, d, n);
     sp.part[1].b = opnd(H->wkv, (long long)D * d, d, D);
@@ -325,10 +337,10 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     sp[1].n = d;
     sp[1].m_store = h;
     EpiUpdate<E> epi;
-    epi.w2 = H->w2; epi.w2s = bf ? H->at<E>(Ly.w2c) : nullptr; epi.w2t = w2t;
+    epi.w2 = H->w2; epi.w2n = H->at<E>(Ly.w2c); epi.w2t = w2t;
     epi.w1 = H->w1; epi.w1s = bf ? H->at<E>(Ly.w1c) : nullptr;
     epi.ls2 = (long long)D * h; epi.ls1 = (long long)h * d;
-    epi.h = h; epi.d = d; epi.D = D; epi.shadows = bf ? 1 : 0; epi.lr = c.lr;
+    epi.h = h; epi.d = d; epi.D = D; epi.w1_copy = bf ? 1 : 0; epi.lr = c.lr;
     H->timing_begin(MONE_STAGE_UPD, s);
     if ((e = launch_gemm<E>(pick_tile(D, h, Lc), sp, 2, Lc, epi, s)) != hipSuccess)
       return hip_fail(e, "launch UPD");
@@ -345,7 +357,7 @@ int run_kv(mone_ttl* H, const void* xq, int q, void* kv, int kv_bf16, hipStream_
   const int Lc = c.n_layers, d = c.d_model, h = c.d_hidden, D = 2 * c.d_kv, Tp = Ly.Tp;
   const bool bf = sizeof(E) == 2;
   const E* w1op = bf ? H->at<E>(Ly.w1c) : reinterpret_cast<const E*>(H->w1);
-  const E* w2op = bf ? H->at<E>(Ly.w2c) : reinterpret_cast<const E*>(H->w2);
+  const E* w2neg = H->at<E>(Ly.w2c);
   E* A = H->at<E>(Ly.a);  // scratch for A_q (the TTL intermediates are dead between calls)
   const long long lth = (long long)Tp * h;
   const size_t kvE = kv_bf16 ? 2 : 4;
@@ -373,7 +385,7 @@ int run_kv(mone_ttl* H, const void* xq, int q, void* kv, int kv_bf16, hipStream_
     {
       Spec sp{};
       sp.part[0].a = opnd(A, lth, h, qc);
-      sp.part[0].b = opnd(w2op, (long long)D * h, h, D);
+      sp.part[0].b = opnd(w2neg, (long long)D * h, h, D);
       sp.part[0].k_len = h;
       sp.nparts = 1;
       sp.m_extent = qc;
@@ -435,13 +447,14 @@ int mone_ttl_init(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, f
     delete H;
     return hip_fail(e, "clearing the workspace");
   }
+  const long long n1 = (long long)Lc * h * d, n2 = (long long)Lc * D * h;
   if (cfg->act_dtype == MONE_BF16) {
-    const long long n1 = (long long)Lc * h * d, n2 = (long long)Lc * D * h;
-    convert_bf16_kernel<<<dim3(2048), dim3(256), 0, s>>>(w1, H->at<bf16_t>(Ly.w1c), n1);
-    convert_bf16_kernel<<<dim3(2048), dim3(256), 0, s>>>(w2, H->at<bf16_t>(Ly.w2c), n2);
+    convert_kernel<bf16_t><<<dim3(2048), dim3(256), 0, s>>>(w1, H->at<bf16_t>(Ly.w1c), n1, 1.0f);
+    convert_kernel<bf16_t><<<dim3(2048), dim3(256), 0, s>>>(w2, H->at<bf16_t>(Ly.w2c), n2, -1.0f);
     transpose_kernel<float, bf16_t><<<dim3((h + 63) / 64, (D + 63) / 64, Lc), dim3(256), 0, s>>>(
         w2, (long long)D * h, h, D, h, H->at<bf16_t>(Ly.w2t), (long long)h * D, D, D);
   } else {
+    convert_kernel<float><<<dim3(2048), dim3(256), 0, s>>>(w2, H->at<float>(Ly.w2c), n2, -1.0f);
     transpose_kernel<float, float><<<dim3((h + 63) / 64, (D + 63) / 64, Lc), dim3(256), 0, s>>>(
         w2, (long long)D * h, h, D, h, H->at<float>(Ly.w2t), (long long)h * D, D, D);
   }
