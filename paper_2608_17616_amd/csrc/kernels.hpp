@@ -6,22 +6,30 @@
 // fused epilogue per stage that applies the elementwise part of the step (SiLU and its
 // derivative, the loss gradient and loss partials, the SiLU-gradient product, the SGD update).
 //
-// Every operand a GEMM reads is stored K-contiguous: the producers of intermediates write a
-// transposed copy next to the plain one where a later stage contracts over tokens, so every
-// tile load is a coalesced 16-byte-per-lane row load and every fragment read is one
-// ds_read_b128.
+// Every operand a GEMM reads is stored K-contiguous: where a later stage contracts over
+// tokens, the producing epilogue also writes a transposed copy, so every tile load is a
+// coalesced row load and every fragment read is one ds_read_b128.
 //
-// Tiles: BM x BN output per 256-thread workgroup (4 waves as 2 x 2), K step of 128 bytes per
-// row (64 bf16 or 32 fp32).  A and B tiles are staged in LDS in double buffers with an XOR
-// swizzle of the 16-byte column index by (row / 2) % 8, so both the row stores and the
-// 32-row fragment reads are free of bank conflicts.  Global loads for tile k+1 are issued
-// before the MFMAs of tile k.
+// Main loop.  BM x BN output per 256-thread workgroup (4 waves), K step of 128 bytes per row
+// (64 bf16 or 32 fp32).  Operand tiles go from memory straight into LDS (buffer_load ... lds,
+// no register staging) in two stages; the 16-byte column slot of row r is XOR-swizzled by
+// (r / 2) % 8, which each lane applies by choosing its source address, so fragment reads of 32
+// consecutive rows are free of bank conflicts.  Loads of K step k+1 are in flight while the
+// MFMAs of step k run.
 //
 // MFMA: bf16 uses v_mfma_f32_32x32x16_bf16 (one 16-byte fragment per lane = 8 k-values), fp32
 // uses four v_mfma_f32_32x32x2_f32 on the four floats of the same 16-byte fragment.  Within a
 // 32x32 block lane l supplies row (l % 32) of A and column (l % 32) of B; A and B take their
 // k-values from the same fragment positions, so the k order inside an instruction does not
 // matter.  Accumulator register r of lane l holds C[8*(r/4) + 4*(l/32) + r%4][l % 32].
+//
+// Epilogue.  The fp32 tile is staged through LDS in passes of up to 128 rows, then processed in
+// chunks of 8 consecutive elements: a row pass (8 columns of one row: 16- or 32-byte vector
+// accesses, a wave covering whole rows) and, where a transposed copy is stored, a column pass
+// (8 rows of one column; 16 lanes cover 128 consecutive rows of a column, so each wave writes
+// contiguous 256-byte runs).  The staging layout pads rows by 8 floats and XOR-swizzles the
+// column by 4 * ((row / 8) % 16), which keeps the MFMA-layout writes, the row reads and the
+// column reads free of bank conflicts.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -33,7 +41,7 @@ typedef uint16_t bf16_t;  // raw bf16 storage (same bits as torch.bfloat16)
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(bf16_t v) { return __uint_as_float((uint32_t)v << 16); }
@@ -45,15 +53,36 @@ template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) {
   return __builtin_bit_cast(bf16_t, (__bf16)v);
 }
 
-// Four consecutive elements (16 bytes of fp32 or 8 bytes of bf16), p aligned accordingly.
-__device__ __forceinline__ void store4(float* p, float a, float b, float c, float d) {
-  *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  return (uint32_t)from_f32<bf16_t>(a) | ((uint32_t)from_f32<bf16_t>(b) << 16);
 }
-__device__ __forceinline__ void store4(bf16_t* p, float a, float b, float c, float d) {
-  u32x2 v;
-  v[0] = (uint32_t)from_f32<bf16_t>(a) | ((uint32_t)from_f32<bf16_t>(b) << 16);
-  v[1] = (uint32_t)from_f32<bf16_t>(c) | ((uint32_t)from_f32<bf16_t>(d) << 16);
-  *reinterpret_cast<u32x2*>(p) = v;
+
+// Eight consecutive elements; p is 16-byte aligned.
+__device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
+  reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+  reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+__device__ __forceinline__ void store8(bf16_t* p, const float (&v)[8]) {
+  u32x4 w;
+  w[0] = pack_bf16(v[0], v[1]);
+  w[1] = pack_bf16(v[2], v[3]);
+  w[2] = pack_bf16(v[4], v[5]);
+  w[3] = pack_bf16(v[6], v[7]);
+  *reinterpret_cast<u32x4*>(p) = w;
+}
+__device__ __forceinline__ void load8(const float* p, float (&v)[8]) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0];
+  const float4 b = reinterpret_cast<const float4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void load8(const bf16_t* p, float (&v)[8]) {
+  const u32x4 w = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
 }
 
 __device__ __forceinline__ float sigmoidf_(float z) { return 1.0f / (1.0f + __expf(-z)); }
@@ -76,7 +105,7 @@ struct Part {              // one K-range of the contraction: sum_k a(m, k) b(n,
 struct Problem {
   Part part[2];            // K-concatenated parts: the result is their sum
   int nparts;
-  int M, N;                // output rows/cols that are stored (bounds of the epilogue)
+  int M, N;                // output rows/cols the epilogue may store
   int tiles_m, tiles_n;    // tiles per layer
   int tile_begin;          // first workgroup of this problem in the launch
 };
@@ -91,10 +120,8 @@ struct GemmLaunch {
 // ------------------------------------------------------------------------------------------
 // The grouped GEMM kernel
 
-typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-
-// Buffer load of 4 bytes x size/4 per lane straight into LDS (no VGPR staging): lane l's data
-// lands at M0 + 16*l for 16-byte loads; offsets at or beyond the descriptor's byte count read 0.
+// Buffer load of size bytes per lane straight into LDS (no VGPR staging): lane l's data lands
+// at M0 + 16*l for 16-byte loads; offsets at or beyond the descriptor's byte count read 0.
 __device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t* lds,
                                     int size, int voffset, int soffset, int offset,
                                     int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
@@ -131,17 +158,33 @@ __device__ __forceinline__ void map_tile(int local, int total, int tiles_m, int 
   *tn = r / gm;
 }
 
+template <int BM, int BN>
+struct TileCfg {
+  static constexpr int STAGE = (BM + BN) * 128;   // bytes of one main-loop LDS stage
+  static constexpr int PR = BM < 128 ? BM : 128;  // epilogue rows per pass
+  static constexpr int LDT = BN + 8;              // epilogue staging row stride (floats)
+  static constexpr int EPI_BYTES = PR * LDT * 4;
+  static constexpr int SMEM = 2 * STAGE > EPI_BYTES ? 2 * STAGE : EPI_BYTES;
+};
+
+// Staging position of tile element (r, c) within a pass.
+template <int LDT>
+__device__ __forceinline__ int stage_idx(int r, int c) {
+  return r * LDT + (c ^ (((r >> 3) & 15) << 2));
+}
+
 template <typename E, int BM, int BN, int WAVES_M, class Epi>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
+  using TC = TileCfg<BM, BN>;
   constexpr int VEC = 16 / (int)sizeof(E);   // elements per 16-byte vector
   constexpr int BK = 8 * VEC;                // K per tile: 8 vectors = 128 bytes per row
   constexpr int WAVES_N = 4 / WAVES_M;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;  // wave tile
   constexpr int FM = WM / 32, FN = WN / 32;  // 32x32 MFMA blocks per wave
   constexpr int LA = BM / 32, LB = BN / 32;  // 1 KiB load instructions per wave per stage
-  constexpr int STAGE = (BM + BN) * 128;     // bytes of one LDS stage (A rows, then B rows)
+  constexpr int STAGE = TC::STAGE;
   static_assert(FM >= 1 && FN >= 1 && WAVES_M * WAVES_N == 4, "tile shape");
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[TC::SMEM];
 
   const int bid = blockIdx.x;
   const int pi = (G.nprob > 1 && bid >= G.prob[1].tile_begin) ? 1 : 0;
@@ -254,87 +297,163 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     }
   }
 
+  // ---- epilogue: stage through LDS, then row and column passes
+  constexpr int PR = TC::PR, LDT = TC::LDT;
+  constexpr int RCH = PR * BN / 8 / 256;   // row chunks per thread per pass
+  constexpr int CCH = PR * BN / 8 / 256;   // column chunks per thread per pass
+  constexpr int NB = RCH < 8 ? RCH : 8;    // chunks whose memory reads are batched
+  static_assert(RCH >= 1 && RCH % NB == 0, "epilogue chunking");
+  float* st = reinterpret_cast<float*>(smem);
   float partial = 0.0f;
+#pragma unroll 1
+  for (int p = 0; p < BM / PR; ++p) {
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FM; ++i) {
+      const int r0 = wm * WM + i * 32 - p * PR;  // first pass-local row of block i
+      if (r0 < 0 || r0 >= PR) continue;          // uniform per wave
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int col = n0 + wn * WN + j * 32 + (lane & 31);
+      for (int j = 0; j < FN; ++j) {
+        const int c = wn * WN + j * 32 + (lane & 31);
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int row = m0 + wm * WM + i * 32 + g * 8 + (lane >> 5) * 4;
-        partial += G.epi.apply(pi, layer, row, col, P.M, P.N, acc[i][j][4 * g + 0],
-                               acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            st[stage_idx<LDT>(r0 + g * 8 + (lane >> 5) * 4 + e, c)] = acc[i][j][4 * g + e];
       }
     }
+    __syncthreads();
+    const int row0 = m0 + p * PR;
+#pragma unroll
+    for (int b0 = 0; b0 < RCH; b0 += NB) {
+      float aux[NB][8];
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int q = tid + 256 * (b0 + b);
+        const int r = q / (BN / 8), c = (q % (BN / 8)) * 8;
+        if (row0 + r < P.M && n0 + c < P.N)
+          G.epi.pre8(pi, layer, row0 + r, n0 + c, P.M, P.N, aux[b]);
+      }
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int q = tid + 256 * (b0 + b);
+        const int r = q / (BN / 8), c = (q % (BN / 8)) * 8;
+        float* s0 = st + stage_idx<LDT>(r, c);
+        float* s1 = st + stage_idx<LDT>(r, c + 4);
+        float v[8];
+        const float4 x0 = *reinterpret_cast<const float4*>(s0);
+        const float4 x1 = *reinterpret_cast<const float4*>(s1);
+        v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
+        v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
+        if (row0 + r >= P.M || n0 + c >= P.N) continue;
+        partial += G.epi.rows8(pi, layer, row0 + r, n0 + c, P.M, P.N, v, aux[b]);
+        if constexpr (Epi::kWriteback) {
+          *reinterpret_cast<float4*>(s0) = make_float4(v[0], v[1], v[2], v[3]);
+          *reinterpret_cast<float4*>(s1) = make_float4(v[4], v[5], v[6], v[7]);
+        }
+      }
+    }
+    if constexpr (Epi::kCols) {
+      if (G.epi.has_cols(pi)) {
+        if constexpr (Epi::kWriteback) __syncthreads();
+#pragma unroll
+        for (int b = 0; b < CCH; ++b) {
+          const int q = tid + 256 * b;
+          const int k = q % (PR / 8), c = q / (PR / 8);
+          if (row0 + 8 * k + 8 > P.M || n0 + c >= P.N) continue;
+          float v[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = st[stage_idx<LDT>(8 * k + e, c)];
+          G.epi.cols8(pi, layer, row0 + 8 * k, n0 + c, P.M, P.N, v);
+        }
+      }
+    }
+    __syncthreads();
+  }
   G.epi.finish(layer, t, wave, lane, partial);
 }
 
 // ------------------------------------------------------------------------------------------
-// Epilogues.  apply() receives four vertically adjacent results C[row..row+3][col] (row is a
-// multiple of 4) and returns a value summed per lane and handed to finish() (the loss
-// partials; 0 elsewhere).  Intermediate buffers have Tp >= every stored row (a multiple of
-// 256) rows, so tiles store whole 4-row groups; only caller-owned outputs check rows.
+// Epilogues.  pre8() may read memory for a row chunk (batched before the arithmetic); rows8()
+// handles 8 consecutive columns C[row][col..col+7] and returns a value summed per lane and
+// handed to finish() (the loss partials; 0 elsewhere); with kWriteback its updated values feed
+// the column pass; cols8() handles 8 consecutive rows C[row..row+7][col].  Intermediate
+// buffers have Tp rows (seg_len rounded up to 256), so tiles store whole chunks; bounds are
+// checked in the kernel: a chunk is handled only if its rows are below M and its columns below
+// N (M and N are multiples of 8 wherever a column pass runs).
 
-struct NoFinish {
+struct EpiBase {
+  static constexpr bool kCols = false;
+  static constexpr bool kWriteback = false;
+  __device__ __forceinline__ bool has_cols(int) const { return false; }
+  __device__ __forceinline__ void pre8(int, int, int, int, int, int, float (&)[8]) const {}
+  __device__ __forceinline__ void cols8(int, int, int, int, int, int, const float (&)[8]) const {}
   __device__ __forceinline__ void finish(int, int, int, int, float) const {}
 };
 
-// Forward 1: Z = X W1^T  ->  A = SiLU(Z) in [Tp][h] and [h][Tp], SiLU'(Z) in [Tp][h].
+// Forward 1: tile of Z = X W1^T [tokens][h].  Stores A = SiLU(Z) [Tp][h] (rows) and A^T,
+// SiLU'(Z)^T [h][Tp] (columns); token rows >= n are stored as 0.
 template <typename E>
-struct EpiFwd1 : NoFinish {
-  E* a; E* ds; E* at;
-  long long ls;  // layer stride of a, ds and at (Tp*h)
+struct EpiFwd1 : EpiBase {
+  static constexpr bool kCols = true;
+  E* a; E* at; E* dst;
+  long long ls;  // layer stride of a, at and dst (Tp*h)
   int h, Tp, n;
-  __device__ __forceinline__ float apply(int, int layer, int row, int col, int, int N, float z0,
-                                         float z1, float z2, float z3) const {
-    if (col >= N) return 0.0f;
-    const float z[4] = {z0, z1, z2, z3};
-    float av[4], dv[4];
+  __device__ __forceinline__ bool has_cols(int) const { return true; }
+  __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
+                                         float (&z)[8], const float (&)[8]) const {
+    float av[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if (row + i < n) {
-        const float s = sigmoidf_(z[i]);
-        av[i] = z[i] * s;
-        dv[i] = s * (1.0f + z[i] * (1.0f - s));
-      } else {
-        av[i] = 0.0f;
-        dv[i] = 0.0f;
-      }
-    }
-    const long long base = (long long)layer * ls;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      a[base + (long long)(row + i) * h + col] = from_f32<E>(av[i]);
-      ds[base + (long long)(row + i) * h + col] = from_f32<E>(dv[i]);
-    }
-    store4(at + base + (long long)col * Tp + row, av[0], av[1], av[2], av[3]);
+    for (int e = 0; e < 8; ++e) av[e] = row < n ? z[e] * sigmoidf_(z[e]) : 0.0f;
+    store8(a + (long long)layer * ls + (long long)row * h + col, av);
     return 0.0f;
+  }
+  __device__ __forceinline__ void cols8(int, int layer, int row, int col, int, int,
+                                        const float (&z)[8]) const {
+    float av[8], dv[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float s = sigmoidf_(z[e]);
+      const bool ok = row + e < n;
+      av[e] = ok ? z[e] * s : 0.0f;
+      dv[e] = ok ? s * (1.0f + z[e] * (1.0f - s)) : 0.0f;
+    }
+    const long long o = (long long)layer * ls + (long long)col * Tp + row;
+    store8(at + o, av);
+    store8(dst + o, dv);
   }
 };
 
-// Forward 2 and loss gradient.  The GEMM computes -R = A (-W2)^T + X W_kv^T (K-concatenated,
-// from the negated copy of W2), so R = Y - targets is the negated result.  Stores G = c R in
-// [Tp][D] and [D][Tp]; sums R^2 per wave into the loss partials.
+// Forward 2 and loss gradient: tile of -R [tokens][D], where the GEMM computes
+// A (-W2)^T + X W_kv^T (K-concatenated, from the negated copy of W2), so R = Y - targets.
+// Stores G = c R [Tp][D] (rows) and G^T [D][Tp] (columns); sums R^2 per wave into the loss
+// partials.
 template <typename E>
-struct EpiFwd2 {
+struct EpiFwd2 : EpiBase {
+  static constexpr bool kCols = true;
   E* g; E* gt;
   float* loss_part;       // [L][parts_per_layer]
   long long ls;           // Tp*D
   int D, Tp, n, parts_per_layer;
   float c;
-  __device__ __forceinline__ float apply(int, int layer, int row, int col, int, int N, float r0,
-                                         float r1, float r2, float r3) const {
-    if (col >= N) return 0.0f;
-    float r[4] = {-r0, -r1, -r2, -r3};
+  __device__ __forceinline__ bool has_cols(int) const { return true; }
+  __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
+                                         float (&v)[8], const float (&)[8]) const {
+    float gv[8], s = 0.0f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (row + i >= n) r[i] = 0.0f;
-    const long long base = (long long)layer * ls;
+    for (int e = 0; e < 8; ++e) {
+      const float r = row < n ? -v[e] : 0.0f;
+      s += r * r;
+      gv[e] = c * r;
+    }
+    store8(g + (long long)layer * ls + (long long)row * D + col, gv);
+    return s;
+  }
+  __device__ __forceinline__ void cols8(int, int layer, int row, int col, int, int,
+                                        const float (&v)[8]) const {
+    float gv[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) g[base + (long long)(row + i) * D + col] = from_f32<E>(c * r[i]);
-    store4(gt + base + (long long)col * Tp + row, c * r[0], c * r[1], c * r[2], c * r[3]);
-    return r[0] * r[0] + r[1] * r[1] + r[2] * r[2] + r[3] * r[3];
+    for (int e = 0; e < 8; ++e) gv[e] = row + e < n ? -c * v[e] : 0.0f;
+    store8(gt + (long long)layer * ls + (long long)col * Tp + row, gv);
   }
   __device__ __forceinline__ void finish(int layer, int tile, int wave, int lane, float s) const {
 #pragma unroll
@@ -343,107 +462,114 @@ struct EpiFwd2 {
   }
 };
 
-// Backward to the hidden layer: dA = G W2  ->  dZ = dA * SiLU'(Z), stored [h][Tp].
+// Backward to the hidden layer, transposed: tile of dA^T = W2^T G^T [h][tokens].  Stores
+// dZ^T = dA^T * SiLU'(Z)^T [h][Tp] (rows); token columns >= n are stored as 0.
 template <typename E>
-struct EpiBwd : NoFinish {
-  const E* ds; E* dzt;
+struct EpiBwd : EpiBase {
+  const E* dst; E* dzt;
   long long ls;  // Tp*h
-  int h, Tp, n;
-  __device__ __forceinline__ float apply(int, int layer, int row, int col, int, int N, float d0,
-                                         float d1, float d2, float d3) const {
-    if (col >= N) return 0.0f;
-    const float dv[4] = {d0, d1, d2, d3};
-    float dz[4];
-    const long long base = (long long)layer * ls;
+  int Tp, n;
+  __device__ __forceinline__ void pre8(int, int layer, int row, int col, int, int,
+                                       float (&ds)[8]) const {
+    load8(dst + (long long)layer * ls + (long long)row * Tp + col, ds);
+  }
+  __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
+                                         float (&v)[8], const float (&ds)[8]) const {
+    float dz[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      dz[i] = row + i < n ? dv[i] * to_f32(ds[base + (long long)(row + i) * h + col]) : 0.0f;
-    store4(dzt + base + (long long)col * Tp + row, dz[0], dz[1], dz[2], dz[3]);
+    for (int e = 0; e < 8; ++e) dz[e] = col + e < n ? v[e] * ds[e] : 0.0f;
+    store8(dzt + (long long)layer * ls + (long long)row * Tp + col, dz);
     return 0.0f;
   }
 };
 
 // SGD update of both matrices in one launch.  Problem 0: G^T A = dL/dW2 tile of W2 [D][h];
-// problem 1: dZ^T X = dL/dW1 tile of W1 [h][d].  fp32 read-modify-write of the masters, then
-// the activation-dtype copies the next segment's GEMMs read: -W2 [D][h] (forward 2 and the
-// read) and W2^T [h][D] (backward) in both modes, W1 [h][d] in bf16 mode (fp32 mode reads the
+// problem 1: dZ^T X = dL/dW1 tile of W1 [h][d].  fp32 read-modify-write of the masters
+// (rows), then the activation-dtype copies the next segment's GEMMs read: -W2 [D][h] (rows)
+// and W2^T [h][D] (columns) in both modes, W1 [h][d] (rows) in bf16 mode (fp32 mode reads the
 // master).
 template <typename E>
-struct EpiUpdate : NoFinish {
+struct EpiUpdate : EpiBase {
+  static constexpr bool kCols = true;
+  static constexpr bool kWriteback = true;
   float* w2; E* w2n; E* w2t;
   float* w1; E* w1s;
   long long ls2, ls1;  // D*h, h*d
   int h, d, D;
   int w1_copy;         // write w1s (bf16 mode)
   float lr;
-  __device__ __forceinline__ float apply(int pi, int layer, int row, int col, int M, int N,
-                                         float g0, float g1, float g2, float g3) const {
-    if (col >= N || row >= M) return 0.0f;
-    const float gv[4] = {g0, g1, g2, g3};
+  __device__ __forceinline__ bool has_cols(int pi) const { return pi == 0; }
+  __device__ __forceinline__ void pre8(int pi, int layer, int row, int col, int M, int N,
+                                       float (&w)[8]) const {
+    if (row >= M || col >= N) return;
+    if (pi == 0)
+      load8(w2 + (long long)layer * ls2 + (long long)row * h + col, w);
+    else
+      load8(w1 + (long long)layer * ls1 + (long long)row * d + col, w);
+  }
+  __device__ __forceinline__ float rows8(int pi, int layer, int row, int col, int M, int N,
+                                         float (&v)[8], const float (&w)[8]) const {
+    if (row >= M || col >= N) return 0.0f;
+    float nw[8], cp[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) nw[e] = w[e] - lr * v[e];
     if (pi == 0) {
-      const long long base = (long long)layer * ls2;
-      float nw[4];
+      const long long o = (long long)layer * ls2 + (long long)row * h + col;
+      store8(w2 + o, nw);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const long long idx = base + (long long)(row + i) * h + col;
-        nw[i] = w2[idx] - lr * gv[i];
-        w2[idx] = nw[i];
-        w2n[idx] = from_f32<E>(-nw[i]);
-      }
-      store4(w2t + base + (long long)col * D + row, nw[0], nw[1], nw[2], nw[3]);
+      for (int e = 0; e < 8; ++e) cp[e] = -nw[e];
+      store8(w2n + o, cp);
     } else {
-      const long long base = (long long)layer * ls1;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const long long idx = base + (long long)(row + i) * d + col;
-        const float w = w1[idx] - lr * gv[i];
-        w1[idx] = w;
-        if (w1_copy) w1s[idx] = from_f32<E>(w);
-      }
+      const long long o = (long long)layer * ls1 + (long long)row * d + col;
+      store8(w1 + o, nw);
+      if (w1_copy) store8(w1s + o, nw);
     }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = nw[e];
     return 0.0f;
+  }
+  __device__ __forceinline__ void cols8(int, int layer, int row, int col, int M, int N,
+                                        const float (&v)[8]) const {
+    if (row >= M || col >= N) return;
+    store8(w2t + (long long)layer * ls2 + (long long)col * D + row, v);
   }
 };
 
-// Read, first layer: A_q = SiLU(X_q W1^T), stored [Tp][h] (rows >= q hold SiLU(0) = 0).
+// Read, first layer: tile of X_q W1^T [q][h]; stores A_q = SiLU(.) [Tp][h] (rows >= q hold
+// SiLU(0) = 0).
 template <typename E>
-struct EpiKv1 : NoFinish {
+struct EpiKv1 : EpiBase {
   E* a;
   long long ls;
   int h;
-  __device__ __forceinline__ float apply(int, int layer, int row, int col, int, int N, float z0,
-                                         float z1, float z2, float z3) const {
-    if (col >= N) return 0.0f;
-    const float z[4] = {z0, z1, z2, z3};
-    const long long base = (long long)layer * ls;
+  __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
+                                         float (&z)[8], const float (&)[8]) const {
+    float av[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      a[base + (long long)(row + i) * h + col] = from_f32<E>(z[i] * sigmoidf_(z[i]));
+    for (int e = 0; e < 8; ++e) av[e] = z[e] * sigmoidf_(z[e]);
+    store8(a + (long long)layer * ls + (long long)row * h + col, av);
     return 0.0f;
   }
 };
 
-// Read, second layer: the GEMM computes A_q (-W2)^T = -KV; stores KV into the caller's
-// [L][q][D] output (fp32 or bf16).
-struct EpiKv2 : NoFinish {
+// Read, second layer: tile of A_q (-W2)^T = -KV [q][D]; stores KV into the caller's [L][q][D]
+// output (fp32 or bf16), rows < q only.
+struct EpiKv2 : EpiBase {
   void* kv;
   long long ls;  // q*D
   int D;
   int bf16_out;
-  __device__ __forceinline__ float apply(int, int layer, int row, int col, int M, int N, float y0,
-                                         float y1, float y2, float y3) const {
-    if (col >= N) return 0.0f;
-    const float y[4] = {-y0, -y1, -y2, -y3};
-    const long long base = (long long)layer * ls + col;
+  __device__ __forceinline__ float rows8(int, int layer, int row, int col, int M, int,
+                                         float (&v)[8], const float (&)[8]) const {
+    if (row >= M) return 0.0f;
+    float y[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if (row + i >= M) break;
-      const long long idx = base + (long long)(row + i) * D;
-      if (bf16_out)
-        reinterpret_cast<bf16_t*>(kv)[idx] = from_f32<bf16_t>(y[i]);
-      else
-        reinterpret_cast<float*>(kv)[idx] = y[i];
-    }
+    for (int e = 0; e < 8; ++e) y[e] = -v[e];
+    const long long o = (long long)layer * ls + (long long)row * D + col;
+    if (bf16_out)
+      store8(reinterpret_cast<bf16_t*>(kv) + o, y);
+    else
+      store8(reinterpret_cast<float*>(kv) + o, y);
     return 0.0f;
   }
 };

@@ -8,7 +8,7 @@
 //                  W2n [L][D][h] act   -W2 (forward 2 and the read: the residual Y - targets
 //                                      becomes one K-concatenated sum, negated in the epilogue)
 //                  W2t [L][h][D] act   W2 transposed (B operand of the backward GEMM)
-//                  A   [L][Tp][h], A^T [L][h][Tp], SiLU'(Z) [L][Tp][h]
+//                  A   [L][Tp][h], A^T [L][h][Tp], SiLU'(Z)^T [L][h][Tp]
 //                  G   [L][Tp][D], G^T [L][D][Tp]
 //                  dZ^T [L][h][Tp], X^T [L][d][Tp]
 //                  loss partials [L][P], loss [L] fp32
@@ -19,7 +19,7 @@
 //   XT   X -> X^T
 //   FWD1 Z = X W1^T                      epilogue: A, A^T, SiLU'(Z)
 //   FWD2 -R = [A | X] [-W2 | W_kv]^T     epilogue: G = c R, G^T, sum R^2 partials
-//   BWD  dA = G W2                       epilogue: dZ^T = (dA * SiLU'(Z))^T
+//   BWD  dA^T = W2^T G^T                 epilogue: dZ^T = dA^T * SiLU'(Z)^T
 //   UPD  G^T A and dZ^T X (2 problems)   epilogue: fp32 SGD read-modify-write + copies
 #include <hip/hip_runtime.h>
 
@@ -60,7 +60,7 @@ long long round_up(long long v, long long a) { return (v + a - 1) / a * a; }
 struct Layout {
   int Tp;
   int loss_per_layer;
-  size_t w1c, w2c, w2t, a, at, ds, g, gt, dzt, xt, loss_part, loss_out, total;
+  size_t w1c, w2c, w2t, a, at, dst, g, gt, dzt, xt, loss_part, loss_out, total;
 };
 
 int check_config(const mone_ttl_config* c) {
@@ -108,7 +108,7 @@ Layout make_layout(const mone_ttl_config* c) {
   L.w2t = take(nl * h * D * E);
   L.a = take(nl * Tp * h * E);
   L.at = take(nl * h * Tp * E);
-  L.ds = take(nl * Tp * h * E);
+  L.dst = take(nl * h * Tp * E);
   L.g = take(nl * Tp * D * E);
   L.gt = take(nl * D * Tp * E);
   L.dzt = take(nl * h * Tp * E);
@@ -121,14 +121,16 @@ Layout make_layout(const mone_ttl_config* c) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-enum TileShape { TILE_256x256 = 0, TILE_128x128 = 1, TILE_64x256 = 2 };
+enum TileShape { TILE_256x256 = 0, TILE_128x128 = 1, TILE_64x256 = 2, TILE_256x64 = 3 };
 
 constexpr int kNumCUs = 256;
 
-// 64-row tiles for short token extents (short segments, query batches); 256 x 256 when the
-// grouped problem still has at least one such tile per CU; 128 x 128 otherwise.
+// 64-row tiles for short row extents (short segments, query batches), 64-column tiles for
+// short column extents (the token axis of the transposed backward); 256 x 256 when the grouped
+// problem still has at least one such tile per CU; 128 x 128 otherwise.
 TileShape pick_tile(int m, int n, int layers) {
   if (m <= 64) return TILE_64x256;
+  if (n <= 64) return TILE_256x64;
   const long long big = (long long)((m + 255) / 256) * ((n + 255) / 256) * layers;
   if (m >= 256 && n >= 256 && big >= kNumCUs) return TILE_256x256;
   return TILE_128x128;
@@ -139,8 +141,9 @@ struct Spec {
   Part part[2];
   int nparts;
   int m_extent;   // rows that are computed (tiles cover them)
-  int n;          // columns
+  int n;          // columns that are computed
   int m_store;    // rows stored by the epilogue; -1 = every computed tile row
+  int n_store;    // columns stored by the epilogue; -1 = every computed tile column
 };
 
 Opnd opnd(const void* p, long long lstride, int ld, int rows) {
@@ -166,7 +169,7 @@ hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi
     P.tiles_m = (specs[i].m_extent + BM - 1) / BM;
     P.tiles_n = (specs[i].n + BN - 1) / BN;
     P.M = specs[i].m_store >= 0 ? specs[i].m_store : P.tiles_m * BM;
-    P.N = specs[i].n;
+    P.N = specs[i].n_store >= 0 ? specs[i].n_store : P.tiles_n * BN;
     P.tile_begin = begin;
     begin += P.tiles_m * P.tiles_n * layers;
   }
@@ -186,6 +189,8 @@ hipError_t launch_gemm(TileShape t, const Spec* specs, int nspec, int layers, co
       return launch_tiled<E, 256, 256, 2>(specs, nspec, layers, epi, s, tiles_per_layer0);
     case TILE_128x128:
       return launch_tiled<E, 128, 128, 2>(specs, nspec, layers, epi, s, tiles_per_layer0);
+    case TILE_256x64:
+      return launch_tiled<E, 256, 64, 4>(specs, nspec, layers, epi, s, tiles_per_layer0);
     default:
       return launch_tiled<E, 64, 256, 1>(specs, nspec, layers, epi, s, tiles_per_layer0);
   }
@@ -243,7 +248,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
   E* w2t = H->at<E>(Ly.w2t);
   E* A = H->at<E>(Ly.a);
   E* At = H->at<E>(Ly.at);
-  E* dS = H->at<E>(Ly.ds);
+  E* dSt = H->at<E>(Ly.dst);
   E* Gm = H->at<E>(Ly.g);
   E* Gt = H->at<E>(Ly.gt);
   E* dZt = H->at<E>(Ly.dzt);
@@ -260,7 +265,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
   if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch XT");
   H->timing_end(MONE_STAGE_XT, s);
 
-  // FWD1: Z = X W1^T  ->  A, A^T, SiLU'(Z)
+  // FWD1: Z = X W1^T  ->  A, A^T, SiLU'(Z)^T
   {
     Spec sp{};
     sp.part[0].a = opnd(x, lsx, d, n);
@@ -270,8 +275,9 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     sp.m_extent = n;
     sp.n = h;
     sp.m_store = -1;
+    sp.n_store = h;
     EpiFwd1<E> epi;
-    epi.a = A; epi.ds = dS; epi.at = At; epi.ls = lth; epi.h = h; epi.Tp = Tp; epi.n = n;
+    epi.a = A; epi.at = At; epi.dst = dSt; epi.ls = lth; epi.h = h; epi.Tp = Tp; epi.n = n;
     H->timing_begin(MONE_STAGE_FWD1, s);
     if ((e = launch_gemm<E>(pick_tile(n, h, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
       return hip_fail(e, "launch FWD1");
@@ -290,6 +296,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     sp.m_extent = n;
     sp.n = D;
     sp.m_store = -1;
+    sp.n_store = D;
     EpiFwd2<E> epi;
     epi.g = Gm; epi.gt = Gt; epi.loss_part = H->at<float>(Ly.loss_part); epi.ls = ltd;
     epi.D = D; epi.Tp = Tp; epi.n = n; epi.parts_per_layer = Ly.loss_per_layer;
@@ -301,20 +308,21 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     H->timing_end(MONE_STAGE_FWD2, s);
     H->last_loss_count = 4 * tiles;
   }
-  // BWD: dA = G W2 (B operand W2^T, K-contiguous)  ->  dZ^T
+  // BWD: dA^T = W2^T G^T (A operand W2^T [h][D], B operand G [tokens][D])  ->  dZ^T
   {
     Spec sp{};
-    sp.part[0].a = opnd(Gm, ltd, D, n);
-    sp.part[0].b = opnd(w2t, (long long)h * D, D, h);
+    sp.part[0].a = opnd(w2t, (long long)h * D, D, h);
+    sp.part[0].b = opnd(Gm, ltd, D, n);
     sp.part[0].k_len = D;
     sp.nparts = 1;
-    sp.m_extent = n;
-    sp.n = h;
-    sp.m_store = -1;
+    sp.m_extent = h;
+    sp.n = n;
+    sp.m_store = h;
+    sp.n_store = -1;
     EpiBwd<E> epi;
-    epi.ds = dS; epi.dzt = dZt; epi.ls = lth; epi.h = h; epi.Tp = Tp; epi.n = n;
+    epi.dst = dSt; epi.dzt = dZt; epi.ls = lth; epi.Tp = Tp; epi.n = n;
     H->timing_begin(MONE_STAGE_BWD, s);
-    if ((e = launch_gemm<E>(pick_tile(n, h, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
+    if ((e = launch_gemm<E>(pick_tile(h, n, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
       return hip_fail(e, "launch BWD");
     H->timing_end(MONE_STAGE_BWD, s);
   }
@@ -329,6 +337,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     sp[0].m_extent = D;
     sp[0].n = h;
     sp[0].m_store = D;
+    sp[0].n_store = h;
     sp[1].part[0].a = opnd(dZt, lth, Tp, h);
     sp[1].part[0].b = opnd(Xt, ltx, Tp, d);
     sp[1].part[0].k_len = kt;
@@ -336,6 +345,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     sp[1].m_extent = h;
     sp[1].n = d;
     sp[1].m_store = h;
+    sp[1].n_store = d;
     EpiUpdate<E> epi;
     epi.w2 = H->w2; epi.w2n = H->at<E>(Ly.w2c); epi.w2t = w2t;
     epi.w1 = H->w1; epi.w1s = bf ? H->at<E>(Ly.w1c) : nullptr;
@@ -375,6 +385,7 @@ int run_kv(mone_ttl* H, const void* xq, int q, void* kv, int kv_bf16, hipStream_
       sp.m_extent = qc;
       sp.n = h;
       sp.m_store = -1;
+      sp.n_store = h;
       EpiKv1<E> epi;
       epi.a = A; epi.ls = lth; epi.h = h;
       H->timing_begin(MONE_STAGE_KV1, s);
@@ -391,6 +402,7 @@ int run_kv(mone_ttl* H, const void* xq, int q, void* kv, int kv_bf16, hipStream_
       sp.m_extent = qc;
       sp.n = D;
       sp.m_store = qc;
+      sp.n_store = D;
       EpiKv2 epi;
       epi.kv = kvc; epi.ls = (long long)q * D; epi.D = D; epi.bf16_out = kv_bf16;
       H->timing_begin(MONE_STAGE_KV2, s);
