@@ -50,6 +50,26 @@ def stage_work(cfg, q):
     }
 
 
+def counted_traffic(stage):
+    """Per-launch HBM bytes of `stage` from the committed counter summary, or None when the
+    kernel sources have changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_8b.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        h = hashlib.sha256()
+        for src in rec["sources"]:
+            with open(os.path.join(ROOT, src), "rb") as f:
+                h.update(f.read())
+        if h.hexdigest() != rec["source_sha256"] or stage not in rec["per_launch"]:
+            return None
+        t = rec["per_launch"][stage]
+        return {"read_bytes": round(t["fetch_bytes"]), "write_bytes": round(t["write_bytes"])}
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(cfg, w1, w2, wkv, xs, budget_s):
     import numpy as np
 
@@ -186,6 +206,11 @@ def main():
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(dby / davg / 1e9, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(dby / davg / 1e9 / PEAK_HBM_GBS, 4), "traffic": None}
+    counted = counted_traffic(dom) if (args.config == "8b" and S >= 1) else None
+    if counted:
+        roof["traffic"] = counted["read_bytes"] + counted["write_bytes"]
+        roof["traffic_detail"] = dict(counted, algorithmic_bytes=dby,
+                                      source="profiles/hbm_traffic_8b.json")
 
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
