@@ -35,6 +35,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 namespace mone {
 
 typedef uint16_t bf16_t;  // raw bf16 storage (same bits as torch.bfloat16)
@@ -160,12 +162,37 @@ __device__ __forceinline__ void map_tile(int local, int total, int tiles_m, int 
 
 template <int BM, int BN>
 struct TileCfg {
-  static constexpr int STAGE = (BM + BN) * 128;   // bytes of one main-loop LDS stage
+  // Main loop: A and B panels of 128-byte rows in separate LDS rings.  The 256 x 256 and
+  // 128 x 128 tiles keep A two K steps ahead (3 slots) and B one step ahead (2 slots), which
+  // fills the 160 KiB of LDS for one 256 x 256 workgroup per CU or two 128 x 128 ones.
+  static constexpr int NA = BM == BN ? 3 : 2;
+  static constexpr int NB = 2;
+  static constexpr int ASLOT = BM * 128, BSLOT = BN * 128;
+  static constexpr int RING = NA * ASLOT + NB * BSLOT;
   static constexpr int PR = BM < 128 ? BM : 128;  // epilogue rows per pass
   static constexpr int LDT = BN + 8;              // epilogue staging row stride (floats)
   static constexpr int EPI_BYTES = PR * LDT * 4;
-  static constexpr int SMEM = 2 * STAGE > EPI_BYTES ? 2 * STAGE : EPI_BYTES;
+  static constexpr int SMEM = RING > EPI_BYTES ? RING : EPI_BYTES;
 };
+
+// Spread NR LDS reads and NV buffer loads evenly over NM MFMAs in the scheduler's order:
+// after MFMA i come the reads and loads whose share falls there.
+template <int NM, int NR, int NV, int I>
+__device__ __forceinline__ void interleave_step() {
+  constexpr int r = (NR * (I + 1)) / NM - (NR * I) / NM;
+  constexpr int v = (NV * (I + 1)) / NM - (NV * I) / NM;
+  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                   // MFMA
+  if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);  // DS read
+  if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);  // VMEM read
+}
+template <int NM, int NR, int NV, int... I>
+__device__ __forceinline__ void interleave_seq(std::integer_sequence<int, I...>) {
+  (interleave_step<NM, NR, NV, I>(), ...);
+}
+template <int NM, int NR, int NV>
+__device__ __forceinline__ void interleave() {
+  interleave_seq<NM, NR, NV>(std::make_integer_sequence<int, NM>{});
+}
 
 // Staging position of tile element (r, c) within a pass.
 template <int LDT>
@@ -177,12 +204,14 @@ template <typename E, int BM, int BN, int WAVES_M, class Epi>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   using TC = TileCfg<BM, BN>;
   constexpr int VEC = 16 / (int)sizeof(E);   // elements per 16-byte vector
-  constexpr int BK = 8 * VEC;                // K per tile: 8 vectors = 128 bytes per row
+  constexpr int BK = 8 * VEC;                // K per step: 8 vectors = 128 bytes per row
   constexpr int WAVES_N = 4 / WAVES_M;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;  // wave tile
   constexpr int FM = WM / 32, FN = WN / 32;  // 32x32 MFMA blocks per wave
-  constexpr int LA = BM / 32, LB = BN / 32;  // 1 KiB load instructions per wave per stage
-  constexpr int STAGE = TC::STAGE;
+  constexpr int LA = BM / 32, LB = BN / 32;  // 1 KiB load instructions per wave per panel
+  constexpr int NA = TC::NA, NB = TC::NB, ASLOT = TC::ASLOT, BSLOT = TC::BSLOT;
+  constexpr int MPF = sizeof(E) == 2 ? 1 : 4;  // MFMA instructions per fragment pair
+  constexpr int NM = FM * FN * MPF;            // MFMA instructions per sub-step
   static_assert(FM >= 1 && FN >= 1 && WAVES_M * WAVES_N == 4, "tile shape");
   __shared__ __attribute__((aligned(1024))) unsigned char smem[TC::SMEM];
 
@@ -213,7 +242,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   // of its first load.  Lane l of load instruction i fills LDS row 8*(4*i + wave) + l/8, slot
   // l%8, and fetches the 16-byte vector (slot ^ swizzle(row)) of that row.
   i32x4 ra[2], rb[2];
-  int oa[2], ob[2];
+  int oa[2], ob[2], lda[2], ldb[2];
   const int lrow = lane >> 3, lslot = lane & 7;
 #pragma unroll
   for (int pp = 0; pp < 2; ++pp) {
@@ -224,85 +253,139 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     rb[pp] = make_rsrc(B, (uint32_t)((long long)Pt.b.rows * Pt.b.ld * (int)sizeof(E)));
     const int r = 8 * wave + lrow;  // row of load 0; load i adds 32 rows (same swizzle)
     const int v = lslot ^ ((r >> 1) & 7);
-    oa[pp] = ((m0 + r) * Pt.a.ld + v * VEC) * (int)sizeof(E);
-    ob[pp] = ((n0 + r) * Pt.b.ld + v * VEC) * (int)sizeof(E);
+    lda[pp] = Pt.a.ld * (int)sizeof(E);
+    ldb[pp] = Pt.b.ld * (int)sizeof(E);
+    oa[pp] = (m0 + r) * lda[pp] + v * 16;
+    ob[pp] = (n0 + r) * ldb[pp] + v * 16;
   }
 
-  auto issue_loads = [&](int kt, int stage) {
-    const int pp = kt < nk0 ? 0 : 1;
-    const int k0 = (kt - (pp ? nk0 : 0)) * BK * (int)sizeof(E);
-    const Part& Pt = P.part[pp];
-    unsigned char* sa = smem + stage * STAGE;
-    unsigned char* sb = sa + BM * 128;
+  // Loads of K step kt into an LDS slot (operand part, offsets and strides chosen by selects,
+  // not branches).  Steps past the end use an offset beyond the descriptor's range: they move
+  // no data and fill an already consumed slot with zeros, so every step issues the same
+  // instructions and the loop body stays one scheduling region.
+  constexpr int KB = BK * (int)sizeof(E);  // bytes of one K step of one row
+  auto load_a = [&](int kt, int slot) {
+    const bool p1 = kt >= nk0;
+    const i32x4 rs = p1 ? ra[1] : ra[0];
+    const int ld = p1 ? lda[1] : lda[0];
+    const int off = p1 ? oa[1] + (kt - nk0) * KB : oa[0] + kt * KB;
+    const int base = kt < nk ? off : (int)0x80000000;
+    unsigned char* sa = smem + slot * ASLOT;
 #pragma unroll
     for (int i = 0; i < LA; ++i) {
       auto* dst = reinterpret_cast<__attribute__((address_space(3))) uint32_t*>(
           reinterpret_cast<uintptr_t>(sa + (4 * i + wave) * 1024));
-      raw_buffer_load_lds(ra[pp], dst, 16, oa[pp] + 32 * i * Pt.a.ld * (int)sizeof(E) + k0, 0,
-                          0, 0);
+      raw_buffer_load_lds(rs, dst, 16, base + 32 * i * ld, 0, 0, 0);
     }
+  };
+  auto load_b = [&](int kt, int slot) {
+    const bool p1 = kt >= nk0;
+    const i32x4 rs = p1 ? rb[1] : rb[0];
+    const int ld = p1 ? ldb[1] : ldb[0];
+    const int off = p1 ? ob[1] + (kt - nk0) * KB : ob[0] + kt * KB;
+    const int base = kt < nk ? off : (int)0x80000000;
+    unsigned char* sb = smem + NA * ASLOT + slot * BSLOT;
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
       auto* dst = reinterpret_cast<__attribute__((address_space(3))) uint32_t*>(
           reinterpret_cast<uintptr_t>(sb + (4 * i + wave) * 1024));
-      raw_buffer_load_lds(rb[pp], dst, 16, ob[pp] + 32 * i * Pt.b.ld * (int)sizeof(E) + k0, 0,
-                          0, 0);
+      raw_buffer_load_lds(rs, dst, 16, base + 32 * i * ld, 0, 0, 0);
     }
   };
 
-  auto compute = [&](int stage) {
-    const unsigned char* sa = smem + stage * STAGE;
-    const unsigned char* sb = sa + BM * 128;
+  // Fragments of one K sub-step (16 bf16 / 8 fp32 k-values per lane).
+  auto read_frags = [&](int sla, int slb, int kk, u32x4 (&fa)[FM], u32x4 (&fb)[FN]) {
+    const unsigned char* sa = smem + sla * ASLOT;
+    const unsigned char* sb = smem + NA * ASLOT + slb * BSLOT;
+    const int v = kk * 2 + (lane >> 5);
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int v = kk * 2 + (lane >> 5);
-      u32x4 fa[FM], fb[FN];
+    for (int i = 0; i < FM; ++i) {
+      const int r = wm * WM + i * 32 + (lane & 31);
+      fa[i] = *reinterpret_cast<const u32x4*>(sa + r * 128 + ((v ^ ((r >> 1) & 7)) << 4));
+    }
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int r = wm * WM + i * 32 + (lane & 31);
-        fa[i] = *reinterpret_cast<const u32x4*>(sa + r * 128 + ((v ^ ((r >> 1) & 7)) << 4));
-      }
+    for (int j = 0; j < FN; ++j) {
+      const int r = wn * WN + j * 32 + (lane & 31);
+      fb[j] = *reinterpret_cast<const u32x4*>(sb + r * 128 + ((v ^ ((r >> 1) & 7)) << 4));
+    }
+  };
+  auto mfmas = [&](const u32x4 (&fa)[FM], const u32x4 (&fb)[FN]) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
-        const int r = wn * WN + j * 32 + (lane & 31);
-        fb[j] = *reinterpret_cast<const u32x4*>(sb + r * 128 + ((v ^ ((r >> 1) & 7)) << 4));
-      }
+        if constexpr (sizeof(E) == 2) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8, fa[i]), __builtin_bit_cast(bf16x8, fb[j]), acc[i][j],
+              0, 0, 0);
+        } else {
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          if constexpr (sizeof(E) == 2) {
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                __builtin_bit_cast(bf16x8, fa[i]), __builtin_bit_cast(bf16x8, fb[j]),
-                acc[i][j], 0, 0, 0);
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                  __uint_as_float(fa[i][e]), __uint_as_float(fb[j][e]), acc[i][j], 0, 0, 0);
-          }
+          for (int e = 0; e < 4; ++e)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                __uint_as_float(fa[i][e]), __uint_as_float(fb[j][e]), acc[i][j], 0, 0, 0);
         }
-    }
+      }
   };
 
+  // Software pipeline.  K step kt reads A slot kt % NA and B slot kt % NB in four sub-steps;
+  // the fragments of sub-step kk+1 are read while the MFMAs of kk run, and the loads of B for
+  // step kt+1 and of A for step kt+NA-1 are spread over the MFMAs of sub-steps 0 and 1.
+  // Before the MFMAs of sub-step 3, each wave waits until its loads of step kt+1 have landed
+  // (A loads of later steps may stay in flight) and its LDS reads of step kt are done; the
+  // workgroup then synchronises, so step kt+1 is complete in LDS (its first fragments are read
+  // under the last MFMAs) and no wave reads the slots of step kt any more (the next step's
+  // loads may overwrite them).
+  constexpr int VMC = NA > 2 ? LA : 0;  // loads allowed in flight at the synchronisation
+  constexpr int WAIT_STEP = (VMC & 15) | ((VMC >> 4) << 14) | (7 << 4);
   if (nk > 0) {
-    issue_loads(0, 0);
-    __builtin_amdgcn_s_waitcnt(0);  // all counters 0: this wave's loads have reached LDS
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      if (kt + 1 < nk) issue_loads(kt + 1, (kt + 1) & 1);
-      compute(kt & 1);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
+    u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
+#pragma unroll
+    for (int k = 0; k < NA - 1; ++k) {
+      load_a(k, k);
+      if (k == 0) load_b(0, 0);
     }
+    __builtin_amdgcn_s_waitcnt(0);  // all counters 0: the prologue's loads have reached LDS
+    __syncthreads();
+    int sa = 0, sb = 0;
+    read_frags(sa, sb, 0, fa0, fb0);
+    for (int kt = 0; kt < nk; ++kt) {
+      const int sa_next = sa + 1 == NA ? 0 : sa + 1;
+      const int sa_load = sa == 0 ? NA - 1 : sa - 1;  // slot of step kt-1: free
+      const int sb_next = sb ^ 1;
+      read_frags(sa, sb, 1, fa1, fb1);
+      load_b(kt + 1, sb_next);
+      mfmas(fa0, fb0);
+      interleave<NM, FM + FN, LB>();
+      read_frags(sa, sb, 2, fa0, fb0);
+      load_a(kt + NA - 1, sa_load);
+      mfmas(fa1, fb1);
+      interleave<NM, FM + FN, LA>();
+      read_frags(sa, sb, 3, fa1, fb1);
+      mfmas(fa0, fb0);
+      interleave<NM, FM + FN, 0>();
+      // Explicit wait, then a bare barrier: a fenced barrier would also wait for the A loads
+      // that may stay in flight.  The empty asm statements keep the compiler from moving LDS
+      // accesses across the barrier.
+      __builtin_amdgcn_s_waitcnt(WAIT_STEP);
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      read_frags(sa_next, sb_next, 0, fa0, fb0);
+      mfmas(fa1, fb1);
+      interleave<NM, FM + FN, 0>();
+      sa = sa_next;
+      sb = sb_next;
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the last (out-of-range) loads have retired
+    __syncthreads();                // the epilogue reuses the LDS of the rings
   }
 
   // ---- epilogue: stage through LDS, then row and column passes
   constexpr int PR = TC::PR, LDT = TC::LDT;
   constexpr int RCH = PR * BN / 8 / 256;   // row chunks per thread per pass
   constexpr int CCH = PR * BN / 8 / 256;   // column chunks per thread per pass
-  constexpr int NB = RCH < 8 ? RCH : 8;    // chunks whose memory reads are batched
-  static_assert(RCH >= 1 && RCH % NB == 0, "epilogue chunking");
+  constexpr int EB = RCH < 8 ? RCH : 8;    // chunks whose memory reads are batched
+  static_assert(RCH >= 1 && RCH % EB == 0, "epilogue chunking");
   float* st = reinterpret_cast<float*>(smem);
   float partial = 0.0f;
 #pragma unroll 1
@@ -324,17 +407,17 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     __syncthreads();
     const int row0 = m0 + p * PR;
 #pragma unroll
-    for (int b0 = 0; b0 < RCH; b0 += NB) {
-      float aux[NB][8];
+    for (int b0 = 0; b0 < RCH; b0 += EB) {
+      float aux[EB][8];
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
+      for (int b = 0; b < EB; ++b) {
         const int q = tid + 256 * (b0 + b);
         const int r = q / (BN / 8), c = (q % (BN / 8)) * 8;
         if (row0 + r < P.M && n0 + c < P.N)
           G.epi.pre8(pi, layer, row0 + r, n0 + c, P.M, P.N, aux[b]);
       }
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
+      for (int b = 0; b < EB; ++b) {
         const int q = tid + 256 * (b0 + b);
         const int r = q / (BN / 8), c = (q % (BN / 8)) * 8;
         float* s0 = st + stage_idx<LDT>(r, c);
