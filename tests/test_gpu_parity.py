@@ -89,3 +89,69 @@ def test_ttl_and_read_match_oracle(torch_cuda, name):
         assert d1 <= bar and d2 <= bar, (d1, d2)
         assert ekv <= bar, ekv
         assert eloss <= bar, eloss
+
+
+# ------------------------------------------------------------------------------------------
+# Full-length runs, in the launch configuration the benchmark times (all layers, every segment
+# of the context).  The oracle cannot replay a whole 8B-class context, so it checks sampled
+# outputs it can compute one by one: the last segment's step from the GPU's own state after
+# all earlier segments, and the read of the GPU's final state.
+
+def _full_run_last_step(torch, cfg, checked):
+    prob = DeviceProblem(cfg, checked)
+    sess = mone.TtlSession(cfg, prob.wkv, prob.w1, prob.w2)
+    S = cfg.n_segments
+    for s in range(S - 1):
+        sess.segment(prob.segment(s))
+    torch.cuda.synchronize()
+    before = {l: (prob.w1[l].cpu().numpy(), prob.w2[l].cpu().numpy()) for l in checked}
+    sess.segment(prob.segment(S - 1))
+    loss = sess.loss()
+    xq, hxq = prob.query()
+    kv = torch.empty(cfg.n_layers, cfg.n_query, cfg.d_out, dtype=torch.float32, device="cuda")
+    sess.memory_kv(xq, kv)
+    torch.cuda.synchronize()
+    after = {l: (prob.w1[l].cpu().numpy(), prob.w2[l].cpu().numpy()) for l in checked}
+    assert bool(torch.isfinite(prob.w1).all()) and bool(torch.isfinite(prob.w2).all())
+    kvh = kv.cpu().numpy()
+    sess.close()
+    bar = tol(cfg)
+    for l in checked:
+        hs = prob.host[l]
+        w1p, w2p = before[l]
+        o1, o2, ls = orc.ttl_step(hs["x"][-1], w1p, w2p, hs["wkv"], cfg.lr, cfg.loss)
+        d1 = rel_l2(after[l][0] - w1p, o1 - w1p)
+        d2 = rel_l2(after[l][1] - w2p, o2 - w2p)
+        ekv = rel_l2(kvh[l], orc.memory_kv(hxq[l], after[l][0], after[l][1]))
+        eloss = abs(loss[l] - ls) / ls
+        drift = np.linalg.norm(after[l][0] - hs["w1"]) / np.linalg.norm(hs["w1"])
+        print(f"  layer {l}: last-step dW1 {d1:.2e} dW2 {d2:.2e} KV {ekv:.2e} loss {eloss:.2e} "
+              f"(|W1_S - W1_0|/|W1_0| {drift:.1e} after {S} segments)", flush=True)
+        assert d1 <= bar and d2 <= bar and ekv <= bar and eloss <= bar
+
+
+def test_full_context_8b_last_step_and_read(torch_cuda):
+    print("[parity] full 8B-class context: 64 segments, all 32 layers", flush=True)
+    _full_run_last_step(torch_cuda, configs.EIGHT_B, [0, 31])
+
+
+def test_full_context_1b_every_segment(torch_cuda):
+    # 1B-class: the oracle replays the whole 64-segment context for two layers.
+    torch = torch_cuda
+    cfg = configs.ONE_B
+    print("[parity] full 1B-class context: 64 segments, all 16 layers", flush=True)
+    prob = DeviceProblem(cfg, [0, 15])
+    sess = mone.TtlSession(cfg, prob.wkv, prob.w1, prob.w2)
+    for s in range(cfg.n_segments):
+        sess.segment(prob.segment(s))
+    torch.cuda.synchronize()
+    w1, w2 = prob.w1.cpu().numpy(), prob.w2.cpu().numpy()
+    sess.close()
+    for l in (0, 15):
+        hs = prob.host[l]
+        o1, o2, _ = orc.ttl_run(hs["x"], hs["w1"], hs["w2"], hs["wkv"], cfg.lr, cfg.loss)
+        errs = (rel_l2(w1[l], o1), rel_l2(w2[l], o2), rel_l2(w1[l] - hs["w1"], o1 - hs["w1"]),
+                rel_l2(w2[l] - hs["w2"], o2 - hs["w2"]))
+        print(f"  layer {l}: W1 {errs[0]:.2e} W2 {errs[1]:.2e} dW1 {errs[2]:.2e} "
+              f"dW2 {errs[3]:.2e}", flush=True)
+        assert max(errs) <= tol(cfg)
