@@ -42,9 +42,11 @@ def stage_work(cfg, q):
         "xt": (0, L * T * d * E * 2),
         "fwd1": (L * 2 * T * d * h, L * (T * d + h * d + T * h * 3) * E),
         "fwd2": (L * 2 * T * D * (h + d), L * (T * h + D * h + T * d + D * d + 2 * T * D) * E),
-        "bwd": (L * 2 * T * D * h, L * (T * D + h * D + 2 * T * h) * E),
-        "upd": (L * (2 * T * D * h + 2 * T * h * d),
-                L * ((D * T + h * T + h * T + d * T) * E + (D * h + h * d) * 8)),
+        # backward (G W2 -> dZ^T) and the W2 update (G^T A) share one launch
+        "bwd": (L * (2 * T * D * h + 2 * T * D * h),
+                L * ((T * D + h * D + 2 * T * h + D * T + h * T) * E + D * h * 8)),
+        # W1 update (dZ^T X)
+        "upd": (L * 2 * T * h * d, L * ((h * T + d * T) * E + h * d * 8)),
         "kv1": (L * 2 * q * d * h, L * (q * d + h * d + q * h) * E),
         "kv2": (L * 2 * q * h * D, L * (q * h + D * h) * E + L * q * D * 4),
     }

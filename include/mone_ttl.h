@@ -134,8 +134,8 @@ const char* mone_ttl_last_error(void);
 #define MONE_STAGE_XT 0    /* X -> X^T staging copy (operand of the W1 gradient) */
 #define MONE_STAGE_FWD1 1  /* Z = X W1^T; A = SiLU(Z) */
 #define MONE_STAGE_FWD2 2  /* R = A W2^T - X W_kv^T; G = c R; loss partials */
-#define MONE_STAGE_BWD 3   /* dZ = (G W2) * SiLU'(Z) */
-#define MONE_STAGE_UPD 4   /* W2 -= lr G^T A and W1 -= lr dZ^T X (one grouped launch) */
+#define MONE_STAGE_BWD 3   /* dZ = (G W2) * SiLU'(Z), and W2 -= lr G^T A (one grouped launch) */
+#define MONE_STAGE_UPD 4   /* W1 -= lr dZ^T X */
 #define MONE_STAGE_KV1 5   /* read: A_q = SiLU(X_q W1^T) */
 #define MONE_STAGE_KV2 6   /* read: KV = A_q W2^T */
 #define MONE_N_STAGES 7

@@ -215,12 +215,16 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   static_assert(FM >= 1 && FN >= 1 && WAVES_M * WAVES_N == 4, "tile shape");
   __shared__ __attribute__((aligned(1024))) unsigned char smem[TC::SMEM];
 
+  // Problem of this workgroup: problem 0's tiles come first.  (Alternating the two problems'
+  // tiles across the launch was measured slower: each XCD's L2 then serves both working sets.)
   const int bid = blockIdx.x;
-  const int pi = (G.nprob > 1 && bid >= G.prob[1].tile_begin) ? 1 : 0;
+  const int n0 = G.nprob > 1 ? G.prob[1].tile_begin : (int)gridDim.x;
+  const int pi = bid >= n0 ? 1 : 0;
+  const int local = bid - (pi ? n0 : 0);
+  const int total = pi ? (int)gridDim.x - n0 : n0;
   const Problem& P = G.prob[pi];
-  const int total = G.nprob > 1 && pi == 0 ? G.prob[1].tile_begin : (int)gridDim.x - P.tile_begin;
   int layer, tm, tn;
-  map_tile(bid - P.tile_begin, total, P.tiles_m, P.tiles_n, &layer, &tm, &tn);
+  map_tile(local, total, P.tiles_m, P.tiles_n, &layer, &tm, &tn);
   const int t = tm * P.tiles_n + tn;
   const int m0 = tm * BM, n0 = tn * BN;
 
@@ -545,76 +549,81 @@ struct EpiFwd2 : EpiBase {
   }
 };
 
-// Backward to the hidden layer, transposed: tile of dA^T = W2^T G^T [h][tokens].  Stores
-// dZ^T = dA^T * SiLU'(Z)^T [h][Tp] (rows); token columns >= n are stored as 0.
+// Backward and W2 update in one launch (both need only G, A and the previous W2).
+// Problem 0: tile of dA^T = W2^T G^T [h][tokens]; stores dZ^T = dA^T * SiLU'(Z)^T [h][Tp]
+// (rows; token columns >= n are stored as 0).  Problem 1: tile of G^T A = dL/dW2 of W2
+// [D][h]; fp32 read-modify-write of the master (rows), then the copies the next segment reads:
+// -W2 [D][h] (rows) and W2^T [h][D] (columns).  The backward reads the W2^T copy of the
+// weights the step started from; the update writes the other copy of a ping-pong pair.
 template <typename E>
-struct EpiBwd : EpiBase {
-  const E* dst; E* dzt;
-  long long ls;  // Tp*h
-  int Tp, n;
-  __device__ __forceinline__ void pre8(int, int layer, int row, int col, int, int,
-                                       float (&ds)[8]) const {
-    load8(dst + (long long)layer * ls + (long long)row * Tp + col, ds);
-  }
-  __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
-                                         float (&v)[8], const float (&ds)[8]) const {
-    float dz[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) dz[e] = col + e < n ? v[e] * ds[e] : 0.0f;
-    store8(dzt + (long long)layer * ls + (long long)row * Tp + col, dz);
-    return 0.0f;
-  }
-};
-
-// SGD update of both matrices in one launch.  Problem 0: G^T A = dL/dW2 tile of W2 [D][h];
-// problem 1: dZ^T X = dL/dW1 tile of W1 [h][d].  fp32 read-modify-write of the masters
-// (rows), then the activation-dtype copies the next segment's GEMMs read: -W2 [D][h] (rows)
-// and W2^T [h][D] (columns) in both modes, W1 [h][d] (rows) in bf16 mode (fp32 mode reads the
-// master).
-template <typename E>
-struct EpiUpdate : EpiBase {
+struct EpiBwdW2 : EpiBase {
   static constexpr bool kCols = true;
   static constexpr bool kWriteback = true;
+  const E* dst; E* dzt;
+  long long lst;       // Tp*h
+  int Tp, n;
   float* w2; E* w2n; E* w2t;
-  float* w1; E* w1s;
-  long long ls2, ls1;  // D*h, h*d
-  int h, d, D;
-  int w1_copy;         // write w1s (bf16 mode)
+  long long ls2;       // D*h
+  int h, D;
   float lr;
-  __device__ __forceinline__ bool has_cols(int pi) const { return pi == 0; }
-  __device__ __forceinline__ void pre8(int pi, int layer, int row, int col, int M, int N,
-                                       float (&w)[8]) const {
-    if (row >= M || col >= N) return;
+  __device__ __forceinline__ bool has_cols(int pi) const { return pi == 1; }
+  __device__ __forceinline__ void pre8(int pi, int layer, int row, int col, int, int,
+                                       float (&x)[8]) const {
     if (pi == 0)
-      load8(w2 + (long long)layer * ls2 + (long long)row * h + col, w);
+      load8(dst + (long long)layer * lst + (long long)row * Tp + col, x);
     else
-      load8(w1 + (long long)layer * ls1 + (long long)row * d + col, w);
+      load8(w2 + (long long)layer * ls2 + (long long)row * h + col, x);
   }
-  __device__ __forceinline__ float rows8(int pi, int layer, int row, int col, int M, int N,
-                                         float (&v)[8], const float (&w)[8]) const {
-    if (row >= M || col >= N) return 0.0f;
+  __device__ __forceinline__ float rows8(int pi, int layer, int row, int col, int, int,
+                                         float (&v)[8], const float (&x)[8]) const {
+    if (pi == 0) {
+      float dz[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dz[e] = col + e < n ? v[e] * x[e] : 0.0f;
+      store8(dzt + (long long)layer * lst + (long long)row * Tp + col, dz);
+      return 0.0f;
+    }
     float nw[8], cp[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) nw[e] = w[e] - lr * v[e];
-    if (pi == 0) {
-      const long long o = (long long)layer * ls2 + (long long)row * h + col;
-      store8(w2 + o, nw);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) cp[e] = -nw[e];
-      store8(w2n + o, cp);
-    } else {
-      const long long o = (long long)layer * ls1 + (long long)row * d + col;
-      store8(w1 + o, nw);
-      if (w1_copy) store8(w1s + o, nw);
+    for (int e = 0; e < 8; ++e) {
+      nw[e] = x[e] - lr * v[e];
+      cp[e] = -nw[e];
     }
+    const long long o = (long long)layer * ls2 + (long long)row * h + col;
+    store8(w2 + o, nw);
+    store8(w2n + o, cp);
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = nw[e];
     return 0.0f;
   }
-  __device__ __forceinline__ void cols8(int, int layer, int row, int col, int M, int N,
+  __device__ __forceinline__ void cols8(int, int layer, int row, int col, int, int,
                                         const float (&v)[8]) const {
-    if (row >= M || col >= N) return;
     store8(w2t + (long long)layer * ls2 + (long long)col * D + row, v);
+  }
+};
+
+// W1 update: tile of dZ^T X = dL/dW1 of W1 [h][d]; fp32 read-modify-write of the master, and
+// in bf16 mode the rounded copy the next segment's forward reads (fp32 mode reads the master).
+template <typename E>
+struct EpiW1 : EpiBase {
+  float* w1; E* w1s;
+  long long ls1;  // h*d
+  int d;
+  int w1_copy;
+  float lr;
+  __device__ __forceinline__ void pre8(int, int layer, int row, int col, int, int,
+                                       float (&w)[8]) const {
+    load8(w1 + (long long)layer * ls1 + (long long)row * d + col, w);
+  }
+  __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
+                                         float (&v)[8], const float (&w)[8]) const {
+    float nw[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) nw[e] = w[e] - lr * v[e];
+    const long long o = (long long)layer * ls1 + (long long)row * d + col;
+    store8(w1 + o, nw);
+    if (w1_copy) store8(w1s + o, nw);
+    return 0.0f;
   }
 };
 
@@ -679,6 +688,57 @@ __global__ __launch_bounds__(256) void transpose_kernel(const Ein* __restrict__ 
   for (int c = ty; c < 64; c += 4) {
     const int gc = c0 + c, gr = r0 + tx;
     if (gc < C && gr < Rz) o[(long long)gc * dst_ld + gr] = from_f32<Eout>(tile[tx][c]);
+  }
+}
+
+// X^T staging: dst[l][c][r] = src[l][r][c] for r < R, 0 for R <= r < Rz (Rz a multiple of 64).
+// 64 x 64 tiles through LDS with 16-byte vector loads (along c) and stores (along r).
+template <typename E>
+__global__ __launch_bounds__(256) void transpose_vec_kernel(const E* __restrict__ src,
+                                                            long long src_ls, int src_ld, int R,
+                                                            int C, E* __restrict__ dst,
+                                                            long long dst_ls, int dst_ld,
+                                                            int Rz) {
+  constexpr int VEC = 16 / (int)sizeof(E);
+  constexpr int VPR = 64 / VEC;          // vectors per 64-element row
+  constexpr int NV = 64 * VPR / 256;     // vectors per thread
+  __shared__ float tile[64][65];
+  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64, l = blockIdx.z;
+  const E* s = src + (long long)l * src_ls;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int idx = threadIdx.x + 256 * i, r = idx / VPR, cv = idx % VPR;
+    const int gr = r0 + r, gc = c0 + cv * VEC;
+    float v[8];
+    if (gr < R && gc < C) {
+      if constexpr (VEC == 8) {
+        load8(reinterpret_cast<const bf16_t*>(s) + (long long)gr * src_ld + gc, v);
+      } else {
+        const float4 x = *reinterpret_cast<const float4*>(s + (long long)gr * src_ld + gc);
+        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) v[e] = 0.0f;
+    }
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) tile[r][cv * VEC + e] = v[e];
+  }
+  __syncthreads();
+  E* o = dst + (long long)l * dst_ls;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int idx = threadIdx.x + 256 * i, c = idx / VPR, u = idx % VPR;
+    const int gc = c0 + c, gr = r0 + u * VEC;
+    if (gc >= C || gr >= Rz) continue;
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) v[e] = tile[u * VEC + e][c];
+    if constexpr (VEC == 8) {
+      store8(reinterpret_cast<bf16_t*>(o) + (long long)gc * dst_ld + gr, v);
+    } else {
+      *reinterpret_cast<float4*>(o + (long long)gc * dst_ld + gr) = make_float4(v[0], v[1], v[2], v[3]);
+    }
   }
 }
 

@@ -7,7 +7,9 @@
 //   workspace      W1c [L][h][d] act   (bf16 mode only: MFMA copy of W1; fp32 mode reads W1)
 //                  W2n [L][D][h] act   -W2 (forward 2 and the read: the residual Y - targets
 //                                      becomes one K-concatenated sum, negated in the epilogue)
-//                  W2t [L][h][D] act   W2 transposed (B operand of the backward GEMM)
+//                  W2t [2][L][h][D] act  W2 transposed (A operand of the backward GEMM), a
+//                                      ping-pong pair: the backward of a step reads one copy
+//                                      while the W2 update of the same launch writes the other
 //                  A   [L][Tp][h], A^T [L][h][Tp], SiLU'(Z)^T [L][h][Tp]
 //                  G   [L][Tp][D], G^T [L][D][Tp]
 //                  dZ^T [L][h][Tp], X^T [L][d][Tp]
@@ -17,10 +19,14 @@
 //
 // A segment step is five launches on the caller's stream, each grouped over all L layers:
 //   XT   X -> X^T
-//   FWD1 Z = X W1^T                      epilogue: A, A^T, SiLU'(Z)
+//   FWD1 Z = X W1^T                      epilogue: A, A^T, SiLU'(Z)^T
 //   FWD2 -R = [A | X] [-W2 | W_kv]^T     epilogue: G = c R, G^T, sum R^2 partials
-//   BWD  dA^T = W2^T G^T                 epilogue: dZ^T = dA^T * SiLU'(Z)^T
-//   UPD  G^T A and dZ^T X (2 problems)   epilogue: fp32 SGD read-modify-write + copies
+//   BWD  dA^T = W2^T G^T  and  G^T A     epilogues: dZ^T = dA^T * SiLU'(Z)^T; fp32 SGD
+//        (2 problems)                    read-modify-write of W2 + its copies
+//   UPD  dZ^T X                          epilogue: fp32 SGD read-modify-write of W1 + copy
+// The W2 update shares the backward's launch: it needs only G and A, and writes the W2^T copy
+// the backward does not read, so CUs in its memory-bound epilogue overlap CUs computing the
+// backward's MFMAs.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -105,7 +111,7 @@ Layout make_layout(const mone_ttl_config* c) {
   const bool bf = c->act_dtype == MONE_BF16;
   L.w1c = bf ? take(nl * h * d * E) : 0;
   L.w2c = take(nl * D * h * E);
-  L.w2t = take(nl * h * D * E);
+  L.w2t = take(2 * nl * h * D * E);
   L.a = take(nl * Tp * h * E);
   L.at = take(nl * h * Tp * E);
   L.dst = take(nl * h * Tp * E);
@@ -206,6 +212,7 @@ struct mone_ttl {
   float* w2;
   unsigned char* ws;
   int last_n;           // tokens of the last non-empty segment (0: none yet)
+  int w2t_cur;          // which copy of the W2^T ping-pong pair holds the current weights
   int last_loss_count;  // loss partials per layer written by that segment
   // stage timing
   std::vector<hipEvent_t> ev;
@@ -245,7 +252,9 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
   const bool bf = sizeof(E) == 2;
   const E* w1op = bf ? H->at<E>(Ly.w1c) : reinterpret_cast<const E*>(H->w1);
   const E* w2neg = H->at<E>(Ly.w2c);
-  E* w2t = H->at<E>(Ly.w2t);
+  const size_t w2t_bytes = (size_t)Lc * h * D * sizeof(E);
+  E* w2t_old = H->at<E>(Ly.w2t + (size_t)H->w2t_cur * w2t_bytes);
+  E* w2t_new = H->at<E>(Ly.w2t + (size_t)(H->w2t_cur ^ 1) * w2t_bytes);
   E* A = H->at<E>(Ly.a);
   E* At = H->at<E>(Ly.at);
   E* dSt = H->at<E>(Ly.dst);
@@ -260,7 +269,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
 
   // XT: X^T, the B operand of the W1 gradient (tokens become the contraction axis)
   H->timing_begin(MONE_STAGE_XT, s);
-  transpose_kernel<E, E><<<dim3((d + 63) / 64, (nz + 63) / 64, Lc), dim3(256), 0, s>>>(
+  transpose_vec_kernel<E><<<dim3((d + 63) / 64, nz / 64, Lc), dim3(256), 0, s>>>(
       reinterpret_cast<const E*>(x), lsx, d, n, d, Xt, ltx, Tp, nz);
   if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch XT");
   H->timing_end(MONE_STAGE_XT, s);
@@ -308,54 +317,57 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     H->timing_end(MONE_STAGE_FWD2, s);
     H->last_loss_count = 4 * tiles;
   }
-  // BWD: dA^T = W2^T G^T (A operand W2^T [h][D], B operand G [tokens][D])  ->  dZ^T
-  {
-    Spec sp{};
-    sp.part[0].a = opnd(w2t, (long long)h * D, D, h);
-    sp.part[0].b = opnd(Gm, ltd, D, n);
-    sp.part[0].k_len = D;
-    sp.nparts = 1;
-    sp.m_extent = h;
-    sp.n = n;
-    sp.m_store = h;
-    sp.n_store = -1;
-    EpiBwd<E> epi;
-    epi.dst = dSt; epi.dzt = dZt; epi.ls = lth; epi.Tp = Tp; epi.n = n;
-    H->timing_begin(MONE_STAGE_BWD, s);
-    if ((e = launch_gemm<E>(pick_tile(h, n, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
-      return hip_fail(e, "launch BWD");
-    H->timing_end(MONE_STAGE_BWD, s);
-  }
-  // UPD: W2 -= lr G^T A  and  W1 -= lr dZ^T X, one grouped launch
+  // BWD: dA^T = W2^T G^T (A operand W2^T [h][D], B operand G [tokens][D])  ->  dZ^T, and in
+  // the same launch W2 -= lr G^T A (A operand G^T [D][tokens], B operand A^T [h][tokens])
   {
     const int kt = (int)round_up(n, BK);
     Spec sp[2] = {};
-    sp[0].part[0].a = opnd(Gt, ltd, Tp, D);
-    sp[0].part[0].b = opnd(At, lth, Tp, h);
-    sp[0].part[0].k_len = kt;
+    sp[0].part[0].a = opnd(w2t_old, (long long)h * D, D, h);
+    sp[0].part[0].b = opnd(Gm, ltd, D, n);
+    sp[0].part[0].k_len = D;
     sp[0].nparts = 1;
-    sp[0].m_extent = D;
-    sp[0].n = h;
-    sp[0].m_store = D;
-    sp[0].n_store = h;
-    sp[1].part[0].a = opnd(dZt, lth, Tp, h);
-    sp[1].part[0].b = opnd(Xt, ltx, Tp, d);
+    sp[0].m_extent = h;
+    sp[0].n = n;
+    sp[0].m_store = h;
+    sp[0].n_store = -1;
+    sp[1].part[0].a = opnd(Gt, ltd, Tp, D);
+    sp[1].part[0].b = opnd(At, lth, Tp, h);
     sp[1].part[0].k_len = kt;
     sp[1].nparts = 1;
-    sp[1].m_extent = h;
-    sp[1].n = d;
-    sp[1].m_store = h;
-    sp[1].n_store = d;
-    EpiUpdate<E> epi;
-    epi.w2 = H->w2; epi.w2n = H->at<E>(Ly.w2c); epi.w2t = w2t;
+    sp[1].m_extent = D;
+    sp[1].n = h;
+    sp[1].m_store = D;
+    sp[1].n_store = h;
+    EpiBwdW2<E> epi;
+    epi.dst = dSt; epi.dzt = dZt; epi.lst = lth; epi.Tp = Tp; epi.n = n;
+    epi.w2 = H->w2; epi.w2n = H->at<E>(Ly.w2c); epi.w2t = w2t_new;
+    epi.ls2 = (long long)D * h; epi.h = h; epi.D = D; epi.lr = c.lr;
+    H->timing_begin(MONE_STAGE_BWD, s);
+    if ((e = launch_gemm<E>(pick_tile(h, n, Lc), sp, 2, Lc, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch BWD");
+    H->timing_end(MONE_STAGE_BWD, s);
+  }
+  // UPD: W1 -= lr dZ^T X (A operand dZ^T [h][tokens], B operand X^T [d][tokens])
+  {
+    const int kt = (int)round_up(n, BK);
+    Spec sp{};
+    sp.part[0].a = opnd(dZt, lth, Tp, h);
+    sp.part[0].b = opnd(Xt, ltx, Tp, d);
+    sp.part[0].k_len = kt;
+    sp.nparts = 1;
+    sp.m_extent = h;
+    sp.n = d;
+    sp.m_store = h;
+    sp.n_store = d;
+    EpiW1<E> epi;
     epi.w1 = H->w1; epi.w1s = bf ? H->at<E>(Ly.w1c) : nullptr;
-    epi.ls2 = (long long)D * h; epi.ls1 = (long long)h * d;
-    epi.h = h; epi.d = d; epi.D = D; epi.w1_copy = bf ? 1 : 0; epi.lr = c.lr;
+    epi.ls1 = (long long)h * d; epi.d = d; epi.w1_copy = bf ? 1 : 0; epi.lr = c.lr;
     H->timing_begin(MONE_STAGE_UPD, s);
-    if ((e = launch_gemm<E>(pick_tile(D, h, Lc), sp, 2, Lc, epi, s)) != hipSuccess)
+    if ((e = launch_gemm<E>(pick_tile(h, d, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
       return hip_fail(e, "launch UPD");
     H->timing_end(MONE_STAGE_UPD, s);
   }
+  H->w2t_cur ^= 1;
   H->last_n = n;
   return MONE_OK;
 }
@@ -451,6 +463,7 @@ int mone_ttl_init(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, f
   H->ws = reinterpret_cast<unsigned char*>(workspace);
   H->last_n = 0;
   H->last_loss_count = 0;
+  H->w2t_cur = 0;
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int Lc = cfg->n_layers, d = cfg->d_model, h = cfg->d_hidden, D = 2 * cfg->d_kv;

@@ -42,7 +42,7 @@ def test_workspace_bytes_formula_and_independent_of_context_length():
     c = _cfg()
     n = mone.mone_ttl_workspace_bytes(c)
     L, d, h, D, Tp, E = 2, 128, 192, 128, 256, 2
-    act = E * L * (h * d + D * h + h * D + 3 * Tp * h + 2 * Tp * D + h * Tp + d * Tp)
+    act = E * L * (h * d + D * h + 2 * h * D + 3 * Tp * h + 2 * Tp * D + h * Tp + d * Tp)
     assert act <= n <= act + 64 * 1024
     # the configs' context lengths never enter: N is not a parameter of any call
     for cfg in configs.CONFIGS.values():
