@@ -218,10 +218,10 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   // Problem of this workgroup: problem 0's tiles come first.  (Alternating the two problems'
   // tiles across the launch was measured slower: each XCD's L2 then serves both working sets.)
   const int bid = blockIdx.x;
-  const int n0 = G.nprob > 1 ? G.prob[1].tile_begin : (int)gridDim.x;
-  const int pi = bid >= n0 ? 1 : 0;
-  const int local = bid - (pi ? n0 : 0);
-  const int total = pi ? (int)gridDim.x - n0 : n0;
+  const int first1 = G.nprob > 1 ? G.prob[1].tile_begin : (int)gridDim.x;
+  const int pi = bid >= first1 ? 1 : 0;
+  const int local = bid - (pi ? first1 : 0);
+  const int total = pi ? (int)gridDim.x - first1 : first1;
   const Problem& P = G.prob[pi];
   int layer, tm, tn;
   map_tile(local, total, P.tiles_m, P.tiles_n, &layer, &tm, &tn);

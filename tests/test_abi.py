@@ -97,3 +97,11 @@ def test_null_handle_calls_fail_cleanly():
     assert L.mone_ttl_loss(None, out, None) == mone.MONE_EINVAL
     assert L.mone_ttl_destroy(None) == mone.MONE_OK
     assert L.mone_ttl_set_stage_timing(None, 4) == mone.MONE_EINVAL
+
+
+def test_library_is_built_from_the_current_sources():
+    # A stale libmone_ttl.so would make every other test exercise old kernels.
+    from paper_2608_17616_amd import build
+    lib_t = os.path.getmtime(mone.LIB_PATH)
+    stale = [p for p in build.DEPENDS if os.path.getmtime(p) > lib_t]
+    assert not stale, f"rebuild libmone_ttl.so (python -m paper_2608_17616_amd.build): {stale}"
