@@ -263,12 +263,12 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     ob[pp] = (n0 + r) * ldb[pp] + v * 16;
   }
 
-  // Loads of K step kt into an LDS slot (operand part, offsets and strides chosen by selects,
-  // not branches).  Steps past the end use an offset beyond the descriptor's range: they move
+  // Loads of K step kt into an LDS slot, instructions [i0, i1) of the panel (operand part,
+  // offsets and strides chosen by selects, not branches).  Steps past the end use an offset beyond the descriptor's range: they move
   // no data and fill an already consumed slot with zeros, so every step issues the same
   // instructions and the loop body stays one scheduling region.
   constexpr int KB = BK * (int)sizeof(E);  // bytes of one K step of one row
-  auto load_a = [&](int kt, int slot) {
+  auto load_a = [&](int kt, int slot, int i0, int i1) {
     const bool p1 = kt >= nk0;
     const i32x4 rs = p1 ? ra[1] : ra[0];
     const int ld = p1 ? lda[1] : lda[0];
@@ -277,12 +277,13 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     unsigned char* sa = smem + slot * ASLOT;
 #pragma unroll
     for (int i = 0; i < LA; ++i) {
+      if (i < i0 || i >= i1) continue;
       auto* dst = reinterpret_cast<__attribute__((address_space(3))) uint32_t*>(
           reinterpret_cast<uintptr_t>(sa + (4 * i + wave) * 1024));
       raw_buffer_load_lds(rs, dst, 16, base + 32 * i * ld, 0, 0, 0);
     }
   };
-  auto load_b = [&](int kt, int slot) {
+  auto load_b = [&](int kt, int slot, int i0, int i1) {
     const bool p1 = kt >= nk0;
     const i32x4 rs = p1 ? rb[1] : rb[0];
     const int ld = p1 ? ldb[1] : ldb[0];
@@ -291,6 +292,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     unsigned char* sb = smem + NA * ASLOT + slot * BSLOT;
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
+      if (i < i0 || i >= i1) continue;
       auto* dst = reinterpret_cast<__attribute__((address_space(3))) uint32_t*>(
           reinterpret_cast<uintptr_t>(sb + (4 * i + wave) * 1024));
       raw_buffer_load_lds(rs, dst, 16, base + 32 * i * ld, 0, 0, 0);
@@ -331,42 +333,63 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       }
   };
 
-  // Software pipeline.  K step kt reads A slot kt % NA and B slot kt % NB in four sub-steps;
-  // the fragments of sub-step kk+1 are read while the MFMAs of kk run, and the loads of B for
-  // step kt+1 and of A for step kt+NA-1 are spread over the MFMAs of sub-steps 0 and 1.
-  // Before the MFMAs of sub-step 3, each wave waits until its loads of step kt+1 have landed
-  // (A loads of later steps may stay in flight) and its LDS reads of step kt are done; the
-  // workgroup then synchronises, so step kt+1 is complete in LDS (its first fragments are read
-  // under the last MFMAs) and no wave reads the slots of step kt any more (the next step's
-  // loads may overwrite them).
+  // Pipeline.  K step kt reads A slot kt % NA and B slot kt % NB in four sub-steps, each
+  // reading its fragments and then issuing its MFMAs (keeping each fragment set live for one
+  // sub-step only schedules better than double-buffering them).  The loads of B for step kt+1
+  // and of A for step kt+NA-1 are spread over the MFMAs: with an A ring of 3, half of B's
+  // loads in each of sub-steps 0 and 1 and half of A's in each of sub-steps 2 and 3; with an A
+  // ring of 2, B's in sub-step 0 and A's in sub-step 1.  After the last sub-step, each wave
+  // waits until its loads of step kt+1 have landed (A loads of later steps may stay in flight)
+  // and its LDS reads of step kt are done; the workgroup then synchronises, so step kt+1 is
+  // complete in LDS and no wave reads the slots of step kt any more (the next step's loads may
+  // overwrite them).
   constexpr int VMC = NA > 2 ? LA : 0;  // loads allowed in flight at the synchronisation
   constexpr int WAIT_STEP = (VMC & 15) | ((VMC >> 4) << 14) | (7 << 4);
   if (nk > 0) {
     u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
 #pragma unroll
     for (int k = 0; k < NA - 1; ++k) {
-      load_a(k, k);
-      if (k == 0) load_b(0, 0);
+      load_a(k, k, 0, LA);
+      if (k == 0) load_b(0, 0, 0, LB);
     }
     __builtin_amdgcn_s_waitcnt(0);  // all counters 0: the prologue's loads have reached LDS
     __syncthreads();
     int sa = 0, sb = 0;
-    read_frags(sa, sb, 0, fa0, fb0);
     for (int kt = 0; kt < nk; ++kt) {
       const int sa_next = sa + 1 == NA ? 0 : sa + 1;
       const int sa_load = sa == 0 ? NA - 1 : sa - 1;  // slot of step kt-1: free
       const int sb_next = sb ^ 1;
+      if constexpr (NA > 2) {
+        read_frags(sa, sb, 0, fa0, fb0);
+        load_b(kt + 1, sb_next, 0, LB / 2);
+        mfmas(fa0, fb0);
+        interleave<NM, 0, LB / 2>();
+        read_frags(sa, sb, 1, fa1, fb1);
+        load_b(kt + 1, sb_next, LB / 2, LB);
+        mfmas(fa1, fb1);
+        interleave<NM, 0, LB - LB / 2>();
+        read_frags(sa, sb, 2, fa0, fb0);
+        load_a(kt + NA - 1, sa_load, 0, LA / 2);
+        mfmas(fa0, fb0);
+        interleave<NM, 0, LA / 2>();
+        read_frags(sa, sb, 3, fa1, fb1);
+        load_a(kt + NA - 1, sa_load, LA / 2, LA);
+        mfmas(fa1, fb1);
+        interleave<NM, 0, LA - LA / 2>();
+      } else {
+      read_frags(sa, sb, 0, fa0, fb0);
+      load_b(kt + 1, sb_next, 0, LB);
+      mfmas(fa0, fb0);
+      interleave<NM, 0, LB>();
       read_frags(sa, sb, 1, fa1, fb1);
-      load_b(kt + 1, sb_next);
-      mfmas(fa0, fb0);
-      interleave<NM, FM + FN, LB>();
-      read_frags(sa, sb, 2, fa0, fb0);
-      load_a(kt + NA - 1, sa_load);
+      load_a(kt + NA - 1, sa_load, 0, LA);
       mfmas(fa1, fb1);
-      interleave<NM, FM + FN, LA>();
-      read_frags(sa, sb, 3, fa1, fb1);
+      interleave<NM, 0, LA>();
+      read_frags(sa, sb, 2, fa0, fb0);
       mfmas(fa0, fb0);
-      interleave<NM, FM + FN, 0>();
+      read_frags(sa, sb, 3, fa1, fb1);
+      mfmas(fa1, fb1);
+      }
       // Explicit wait, then a bare barrier: a fenced barrier would also wait for the A loads
       // that may stay in flight.  The empty asm statements keep the compiler from moving LDS
       // accesses across the barrier.
@@ -374,9 +397,6 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       asm volatile("" ::: "memory");
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
-      read_frags(sa_next, sb_next, 0, fa0, fb0);
-      mfmas(fa1, fb1);
-      interleave<NM, FM + FN, 0>();
       sa = sa_next;
       sb = sb_next;
     }
