@@ -59,10 +59,16 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
   return (uint32_t)from_f32<bf16_t>(a) | ((uint32_t)from_f32<bf16_t>(b) << 16);
 }
 
-// Eight consecutive elements; p is 16-byte aligned.
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+// Eight consecutive elements; p is 16-byte aligned.  Stores and fp32 loads are non-temporal:
+// epilogue outputs are read by a later kernel, and the fp32 masters are read once per step, so
+// neither should displace the operand panels other tiles are streaming through L2.
 __device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
-  reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
-  reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+  f32x4v a, b;
+  a[0] = v[0]; a[1] = v[1]; a[2] = v[2]; a[3] = v[3];
+  b[0] = v[4]; b[1] = v[5]; b[2] = v[6]; b[3] = v[7];
+  __builtin_nontemporal_store(a, reinterpret_cast<f32x4v*>(p));
+  __builtin_nontemporal_store(b, reinterpret_cast<f32x4v*>(p) + 1);
 }
 __device__ __forceinline__ void store8(bf16_t* p, const float (&v)[8]) {
   u32x4 w;
@@ -70,13 +76,13 @@ __device__ __forceinline__ void store8(bf16_t* p, const float (&v)[8]) {
   w[1] = pack_bf16(v[2], v[3]);
   w[2] = pack_bf16(v[4], v[5]);
   w[3] = pack_bf16(v[6], v[7]);
-  *reinterpret_cast<u32x4*>(p) = w;
+  __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(p));
 }
 __device__ __forceinline__ void load8(const float* p, float (&v)[8]) {
-  const float4 a = reinterpret_cast<const float4*>(p)[0];
-  const float4 b = reinterpret_cast<const float4*>(p)[1];
-  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  const f32x4v a = __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(p));
+  const f32x4v b = __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(p) + 1);
+  v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
+  v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
 }
 __device__ __forceinline__ void load8(const bf16_t* p, float (&v)[8]) {
   const u32x4 w = *reinterpret_cast<const u32x4*>(p);
