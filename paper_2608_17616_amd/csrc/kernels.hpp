@@ -93,7 +93,11 @@ __device__ __forceinline__ void load8(const bf16_t* p, float (&v)[8]) {
   }
 }
 
-__device__ __forceinline__ float sigmoidf_(float z) { return 1.0f / (1.0f + __expf(-z)); }
+// Logistic function with the hardware exponential and reciprocal (about 1 ulp each; an IEEE
+// division would cost ten instructions per element in the epilogues).
+__device__ __forceinline__ float sigmoidf_(float z) {
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
+}
 
 // ------------------------------------------------------------------------------------------
 // Problem descriptors
@@ -199,6 +203,13 @@ template <int NM, int NR, int NV>
 __device__ __forceinline__ void interleave() {
   interleave_seq<NM, NR, NV>(std::make_integer_sequence<int, NM>{});
 }
+// The same after NRL leading LDS reads (the next sub-step's fragments, issued first so that
+// their latency hides behind this sub-step's MFMAs).
+template <int NRL, int NM, int NV>
+__device__ __forceinline__ void reads_then_interleave() {
+  __builtin_amdgcn_sched_group_barrier(0x100, NRL, 0);
+  interleave_seq<NM, 0, NV>(std::make_integer_sequence<int, NM>{});
+}
 
 // Staging position of tile element (r, c) within a pass.
 template <int LDT>
@@ -246,64 +257,70 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int nk0 = P.part[0].k_len / BK;
-  const int nk = nk0 + (P.nparts > 1 ? P.part[1].k_len / BK : 0);
+  constexpr int NP = Epi::kParts;
+  const int nk = nk0 + (NP > 1 && P.nparts > 1 ? P.part[1].k_len / BK : 0);
 
-  // Per part: buffer descriptors over this layer's operand slices and each lane's byte offset
-  // of its first load.  Lane l of load instruction i fills LDS row 8*(4*i + wave) + l/8, slot
-  // l%8, and fetches the 16-byte vector (slot ^ swizzle(row)) of that row.
-  i32x4 ra[2], rb[2];
-  int oa[2], ob[2], lda[2], ldb[2];
+  // Per part: buffer descriptors over this layer's operand slices, and each lane's byte offset
+  // for each of its load instructions.  Lane l of load instruction i fills LDS row
+  // 8*(4*i + wave) + l/8, 16-byte slot l%8, and fetches the vector (slot ^ swizzle(row)) of that
+  // row; the swizzle does not depend on i.  The K position of a step goes into the
+  // instruction's scalar offset, so the per-lane offsets stay fixed for the whole loop.
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);  // uniform: LDS addresses in SGPRs
+  i32x4 ra[NP], rb[NP];
+  int vofa[NP][LA], vofb[NP][LB];
   const int lrow = lane >> 3, lslot = lane & 7;
 #pragma unroll
-  for (int pp = 0; pp < 2; ++pp) {
+  for (int pp = 0; pp < NP; ++pp) {
     const Part& Pt = P.part[pp < P.nparts ? pp : 0];
     const E* A = reinterpret_cast<const E*>(Pt.a.p) + (long long)layer * Pt.a.lstride;
     const E* B = reinterpret_cast<const E*>(Pt.b.p) + (long long)layer * Pt.b.lstride;
     ra[pp] = make_rsrc(A, (uint32_t)((long long)Pt.a.rows * Pt.a.ld * (int)sizeof(E)));
     rb[pp] = make_rsrc(B, (uint32_t)((long long)Pt.b.rows * Pt.b.ld * (int)sizeof(E)));
-    const int r = 8 * wave + lrow;  // row of load 0; load i adds 32 rows (same swizzle)
-    const int v = lslot ^ ((r >> 1) & 7);
-    lda[pp] = Pt.a.ld * (int)sizeof(E);
-    ldb[pp] = Pt.b.ld * (int)sizeof(E);
-    oa[pp] = (m0 + r) * lda[pp] + v * 16;
-    ob[pp] = (n0 + r) * ldb[pp] + v * 16;
+    const unsigned r = 8u * wave + lrow;
+    const unsigned v = lslot ^ ((r >> 1) & 7u);
+    const unsigned lda = (unsigned)Pt.a.ld * sizeof(E), ldb = (unsigned)Pt.b.ld * sizeof(E);
+    // Rows past the operand's end give offsets at or beyond the descriptor's range (read as
+    // zero); the range is below 2^31, so the unsigned offsets cannot wrap.
+#pragma unroll
+    for (int i = 0; i < LA; ++i) vofa[pp][i] = (int)((m0 + r + 32u * i) * lda + v * 16u);
+#pragma unroll
+    for (int i = 0; i < LB; ++i) vofb[pp][i] = (int)((n0 + r + 32u * i) * ldb + v * 16u);
   }
+  const i32x4 rnone = make_rsrc(P.part[0].a.p, 0u);  // zero range: every load reads 0
 
-  // Loads of K step kt into an LDS slot, instructions [i0, i1) of the panel (operand part,
-  // offsets and strides chosen by selects, not branches).  Steps past the end use an offset beyond the descriptor's range: they move
+  // Loads of K step kt (of part PP, whose steps start at kbase) into an LDS slot, instructions
+  // [i0, i1) of the panel.  Steps at or past the end use the zero-range descriptor: they move
   // no data and fill an already consumed slot with zeros, so every step issues the same
-  // instructions and the loop body stays one scheduling region.
+  // instructions.
   constexpr int KB = BK * (int)sizeof(E);  // bytes of one K step of one row
-  auto load_a = [&](int kt, int slot, int i0, int i1) {
-    const bool p1 = kt >= nk0;
-    const i32x4 rs = p1 ? ra[1] : ra[0];
-    const int ld = p1 ? lda[1] : lda[0];
-    const int off = p1 ? oa[1] + (kt - nk0) * KB : oa[0] + kt * KB;
-    const int base = kt < nk ? off : (int)0x80000000;
+  auto load_a = [&](auto part, int kt, int slot, int i0, int i1) {
+    constexpr int PP = decltype(part)::value < NP ? decltype(part)::value : 0;
+    const i32x4 rs = kt < nk ? ra[PP] : rnone;
+    const int so = (kt - (PP ? nk0 : 0)) * KB;
     unsigned char* sa = smem + slot * ASLOT;
 #pragma unroll
     for (int i = 0; i < LA; ++i) {
       if (i < i0 || i >= i1) continue;
       auto* dst = reinterpret_cast<__attribute__((address_space(3))) uint32_t*>(
-          reinterpret_cast<uintptr_t>(sa + (4 * i + wave) * 1024));
-      raw_buffer_load_lds(rs, dst, 16, base + 32 * i * ld, 0, 0, 0);
+          reinterpret_cast<uintptr_t>(sa + (4 * i + wave_u) * 1024));
+      raw_buffer_load_lds(rs, dst, 16, vofa[PP][i], so, 0, 0);
     }
   };
-  auto load_b = [&](int kt, int slot, int i0, int i1) {
-    const bool p1 = kt >= nk0;
-    const i32x4 rs = p1 ? rb[1] : rb[0];
-    const int ld = p1 ? ldb[1] : ldb[0];
-    const int off = p1 ? ob[1] + (kt - nk0) * KB : ob[0] + kt * KB;
-    const int base = kt < nk ? off : (int)0x80000000;
+  auto load_b = [&](auto part, int kt, int slot, int i0, int i1) {
+    constexpr int PP = decltype(part)::value < NP ? decltype(part)::value : 0;
+    const i32x4 rs = kt < nk ? rb[PP] : rnone;
+    const int so = (kt - (PP ? nk0 : 0)) * KB;
     unsigned char* sb = smem + NA * ASLOT + slot * BSLOT;
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
       if (i < i0 || i >= i1) continue;
       auto* dst = reinterpret_cast<__attribute__((address_space(3))) uint32_t*>(
-          reinterpret_cast<uintptr_t>(sb + (4 * i + wave) * 1024));
-      raw_buffer_load_lds(rs, dst, 16, base + 32 * i * ld, 0, 0, 0);
+          reinterpret_cast<uintptr_t>(sb + (4 * i + wave_u) * 1024));
+      raw_buffer_load_lds(rs, dst, 16, vofb[PP][i], so, 0, 0);
     }
   };
+  using Part0 = std::integral_constant<int, 0>;
+  using Part1 = std::integral_constant<int, 1>;
 
   // Fragments of one K sub-step (16 bf16 / 8 fp32 k-values per lane).
   auto read_frags = [&](int sla, int slb, int kk, u32x4 (&fa)[FM], u32x4 (&fb)[FN]) {
@@ -339,62 +356,66 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       }
   };
 
-  // Pipeline.  K step kt reads A slot kt % NA and B slot kt % NB in four sub-steps, each
-  // reading its fragments and then issuing its MFMAs (keeping each fragment set live for one
-  // sub-step only schedules better than double-buffering them).  The loads of B for step kt+1
-  // and of A for step kt+NA-1 are spread over the MFMAs: with an A ring of 3, half of B's
-  // loads in each of sub-steps 0 and 1 and half of A's in each of sub-steps 2 and 3; with an A
-  // ring of 2, B's in sub-step 0 and A's in sub-step 1.  After the last sub-step, each wave
-  // waits until its loads of step kt+1 have landed (A loads of later steps may stay in flight)
-  // and its LDS reads of step kt are done; the workgroup then synchronises, so step kt+1 is
-  // complete in LDS and no wave reads the slots of step kt any more (the next step's loads may
-  // overwrite them).
+  // Pipeline.  K step kt reads A slot kt % NA and B slot kt % NB in four sub-steps.  The
+  // fragments of each sub-step are read while the MFMAs of the previous one run: sub-step 0 of
+  // step kt+1 is read right after the synchronisation that ends step kt, and sub-step 3 of
+  // step kt is multiplied after it.  With an A ring of 3 (A two steps ahead, B one), each of
+  // the four MFMA blocks between two synchronisations carries a quarter of the next loads:
+  // the second half of B's step kt+1, both halves of A's step kt+2, and (after the
+  // synchronisation, into the B slot step kt has just released) the first half of B's step
+  // kt+2.  With an A ring of 2, B's and A's step kt+1 go with sub-steps 0 and 1.  Before the
+  // synchronisation each wave waits until its loads of step kt+1 have landed (A loads of step
+  // kt+2 may stay in flight) and its LDS reads of step kt are done; the workgroup then
+  // synchronises, so step kt+1 is complete in LDS and no wave reads the slots of step kt any
+  // more (later loads may overwrite them).
   constexpr int VMC = NA > 2 ? LA : 0;  // loads allowed in flight at the synchronisation
   constexpr int WAIT_STEP = (VMC & 15) | ((VMC >> 4) << 14) | (7 << 4);
   if (nk > 0) {
     u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
 #pragma unroll
     for (int k = 0; k < NA - 1; ++k) {
-      load_a(k, k, 0, LA);
-      if (k == 0) load_b(0, 0, 0, LB);
+      if (k < nk0) load_a(Part0{}, k, k, 0, LA);
+      else load_a(Part1{}, k, k, 0, LA);
+    }
+    if (nk0 > 0) load_b(Part0{}, 0, 0, 0, LB);
+    else load_b(Part1{}, 0, 0, 0, LB);
+    if constexpr (NA > 2) {  // the first half of B's step 1 (the loop issues the rest)
+      if (nk0 > 1) load_b(Part0{}, 1, 1, 0, LB / 2);
+      else load_b(Part1{}, 1, 1, 0, LB / 2);
     }
     __builtin_amdgcn_s_waitcnt(0);  // all counters 0: the prologue's loads have reached LDS
     __syncthreads();
     int sa = 0, sb = 0;
-    for (int kt = 0; kt < nk; ++kt) {
+    read_frags(sa, sb, 0, fa0, fb0);
+    auto step = [&](int kt, auto pa, auto pb) {
       const int sa_next = sa + 1 == NA ? 0 : sa + 1;
       const int sa_load = sa == 0 ? NA - 1 : sa - 1;  // slot of step kt-1: free
       const int sb_next = sb ^ 1;
-      if constexpr (NA > 2) {
-        read_frags(sa, sb, 0, fa0, fb0);
-        load_b(kt + 1, sb_next, 0, LB / 2);
-        mfmas(fa0, fb0);
-        interleave<NM, 0, LB / 2>();
-        read_frags(sa, sb, 1, fa1, fb1);
-        load_b(kt + 1, sb_next, LB / 2, LB);
-        mfmas(fa1, fb1);
-        interleave<NM, 0, LB - LB / 2>();
-        read_frags(sa, sb, 2, fa0, fb0);
-        load_a(kt + NA - 1, sa_load, 0, LA / 2);
-        mfmas(fa0, fb0);
-        interleave<NM, 0, LA / 2>();
-        read_frags(sa, sb, 3, fa1, fb1);
-        load_a(kt + NA - 1, sa_load, LA / 2, LA);
-        mfmas(fa1, fb1);
-        interleave<NM, 0, LA - LA / 2>();
-      } else {
-      read_frags(sa, sb, 0, fa0, fb0);
-      load_b(kt + 1, sb_next, 0, LB);
-      mfmas(fa0, fb0);
-      interleave<NM, 0, LB>();
+      constexpr int NF = FM + FN;  // LDS reads per sub-step
       read_frags(sa, sb, 1, fa1, fb1);
-      load_a(kt + NA - 1, sa_load, 0, LA);
-      mfmas(fa1, fb1);
-      interleave<NM, 0, LA>();
-      read_frags(sa, sb, 2, fa0, fb0);
-      mfmas(fa0, fb0);
-      read_frags(sa, sb, 3, fa1, fb1);
-      mfmas(fa1, fb1);
+      if constexpr (NA > 2) {
+        load_b(pb, kt + 1, sb_next, LB / 2, LB);
+        mfmas(fa0, fb0);
+        reads_then_interleave<NF, NM, LB - LB / 2>();
+        read_frags(sa, sb, 2, fa0, fb0);
+        load_a(pa, kt + NA - 1, sa_load, 0, LA / 2);
+        mfmas(fa1, fb1);
+        reads_then_interleave<NF, NM, LA / 2>();
+        read_frags(sa, sb, 3, fa1, fb1);
+        load_a(pa, kt + NA - 1, sa_load, LA / 2, LA);
+        mfmas(fa0, fb0);
+        reads_then_interleave<NF, NM, LA - LA / 2>();
+      } else {
+        load_b(pb, kt + 1, sb_next, 0, LB);
+        mfmas(fa0, fb0);
+        reads_then_interleave<NF, NM, LB>();
+        read_frags(sa, sb, 2, fa0, fb0);
+        load_a(pa, kt + NA - 1, sa_load, 0, LA);
+        mfmas(fa1, fb1);
+        reads_then_interleave<NF, NM, LA>();
+        read_frags(sa, sb, 3, fa1, fb1);
+        mfmas(fa0, fb0);
+        reads_then_interleave<NF, NM, 0>();
       }
       // Explicit wait, then a bare barrier: a fenced barrier would also wait for the A loads
       // that may stay in flight.  The empty asm statements keep the compiler from moving LDS
@@ -403,23 +424,64 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       asm volatile("" ::: "memory");
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
+      const int sb_free = sb;  // B slot of step kt: read completely, free for step kt+2
       sa = sa_next;
       sb = sb_next;
+      read_frags(sa, sb, 0, fa0, fb0);  // after the last step: a consumed slot, never used
+      if constexpr (NA > 2) load_b(pa, kt + 2, sb_free, 0, LB / 2);  // step kt+2: A's part
+      mfmas(fa1, fb1);
+      reads_then_interleave<FM + FN, NM, (NA > 2 ? LB / 2 : 0)>();
+    };
+    if constexpr (NP == 1) {
+      for (int kt = 0; kt < nk; ++kt) step(kt, Part0{}, Part0{});
+    } else {
+      // The loads' operand part changes at step nk0; running the steps in three ranges keeps
+      // the part a compile-time choice (no per-step selects of offsets).
+      const int e1 = nk0 - (NA - 1) < 0 ? 0 : (nk0 - (NA - 1) > nk ? nk : nk0 - (NA - 1));
+      const int e2 = nk0 - 1 < e1 ? e1 : (nk0 - 1 > nk ? nk : nk0 - 1);
+      int kt = 0;
+      for (; kt < e1; ++kt) step(kt, Part0{}, Part0{});  // A and B loads in part 0
+      for (; kt < e2; ++kt) step(kt, Part1{}, Part0{});  // A loads reach part 1 first
+      for (; kt < nk; ++kt) step(kt, Part1{}, Part1{});
     }
     __builtin_amdgcn_s_waitcnt(0);  // the last (out-of-range) loads have retired
     __syncthreads();                // the epilogue reuses the LDS of the rings
   }
 
   // ---- epilogue: stage through LDS, then row and column passes
+  // The tile goes through LDS in passes of PR rows.  Each pass: the waves holding those rows
+  // stage their accumulators, then every thread takes row chunks (8 consecutive columns of one
+  // row) for the row pass and, if the epilogue has one, column chunks (8 consecutive rows of
+  // one column) for the column pass.  Row chunks go in batches of EB; the memory reads an
+  // epilogue needs per chunk (pre8: the fp32 master, SiLU') are issued one batch ahead, the
+  // first batch before the first staging, so their latency overlaps staging and the previous
+  // batch's work.
   constexpr int PR = TC::PR, LDT = TC::LDT;
+  constexpr int NPASS = BM / PR;
   constexpr int RCH = PR * BN / 8 / 256;   // row chunks per thread per pass
   constexpr int CCH = PR * BN / 8 / 256;   // column chunks per thread per pass
-  constexpr int EB = RCH < 8 ? RCH : 8;    // chunks whose memory reads are batched
+  constexpr int EB = RCH < 8 ? RCH : 8;    // chunks per batch
+  constexpr int NBP = RCH / EB;            // batches per pass
+  constexpr int NBT = NPASS * NBP;         // batches per tile
   static_assert(RCH >= 1 && RCH % EB == 0, "epilogue chunking");
   float* st = reinterpret_cast<float*>(smem);
   float partial = 0.0f;
-#pragma unroll 1
-  for (int p = 0; p < BM / PR; ++p) {
+  float aux[2][EB][8];
+  auto issue_pre = [&](int bi, float (&ax)[EB][8]) {
+    const int row0 = m0 + (bi / NBP) * PR;
+#pragma unroll
+    for (int b = 0; b < EB; ++b) {
+      const int q = tid + 256 * ((bi % NBP) * EB + b);
+      const int r = q / (BN / 8), c = (q % (BN / 8)) * 8;
+      if (row0 + r < P.M && n0 + c < P.N)
+        G.epi.pre8(pi, layer, row0 + r, n0 + c, P.M, P.N, ax[b]);
+    }
+  };
+  if constexpr (Epi::kPre) issue_pre(0, aux[0]);
+  // unrolled only where the batch buffers alternate across passes
+  constexpr int PASS_UNROLL = Epi::kPre ? NPASS : 1;
+#pragma unroll PASS_UNROLL
+  for (int p = 0; p < NPASS; ++p) {
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int r0 = wm * WM + i * 32 - p * PR;  // first pass-local row of block i
@@ -437,18 +499,14 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     __syncthreads();
     const int row0 = m0 + p * PR;
 #pragma unroll
-    for (int b0 = 0; b0 < RCH; b0 += EB) {
-      float aux[EB][8];
-#pragma unroll
-      for (int b = 0; b < EB; ++b) {
-        const int q = tid + 256 * (b0 + b);
-        const int r = q / (BN / 8), c = (q % (BN / 8)) * 8;
-        if (row0 + r < P.M && n0 + c < P.N)
-          G.epi.pre8(pi, layer, row0 + r, n0 + c, P.M, P.N, aux[b]);
+    for (int bb = 0; bb < NBP; ++bb) {
+      const int bi = p * NBP + bb;
+      if constexpr (Epi::kPre) {
+        if (bi + 1 < NBT) issue_pre(bi + 1, aux[(bi + 1) & 1]);
       }
 #pragma unroll
       for (int b = 0; b < EB; ++b) {
-        const int q = tid + 256 * (b0 + b);
+        const int q = tid + 256 * (bb * EB + b);
         const int r = q / (BN / 8), c = (q % (BN / 8)) * 8;
         float* s0 = st + stage_idx<LDT>(r, c);
         float* s1 = st + stage_idx<LDT>(r, c + 4);
@@ -458,7 +516,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
         v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
         v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
         if (row0 + r >= P.M || n0 + c >= P.N) continue;
-        partial += G.epi.rows8(pi, layer, row0 + r, n0 + c, P.M, P.N, v, aux[b]);
+        partial += G.epi.rows8(pi, layer, row0 + r, n0 + c, P.M, P.N, v, aux[bi & 1][b]);
         if constexpr (Epi::kWriteback) {
           *reinterpret_cast<float4*>(s0) = make_float4(v[0], v[1], v[2], v[3]);
           *reinterpret_cast<float4*>(s1) = make_float4(v[4], v[5], v[6], v[7]);
@@ -495,6 +553,8 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
 // N (M and N are multiples of 8 wherever a column pass runs).
 
 struct EpiBase {
+  static constexpr int kParts = 1;  // K-concatenated operand parts the problems may have
+  static constexpr bool kPre = false;  // pre8 reads memory (loads are issued a batch ahead)
   static constexpr bool kCols = false;
   static constexpr bool kWriteback = false;
   __device__ __forceinline__ bool has_cols(int) const { return false; }
@@ -504,20 +564,31 @@ struct EpiBase {
 };
 
 // Forward 1: tile of Z = X W1^T [tokens][h].  Stores A = SiLU(Z) [Tp][h] (rows) and A^T,
-// SiLU'(Z)^T [h][Tp] (columns); token rows >= n are stored as 0.
+// SiLU'(Z)^T [h][Tp] (columns); token rows >= n are stored as 0.  With bf16 outputs the row
+// pass evaluates the logistic once per element and leaves (A, SiLU') packed as two bf16 in the
+// staging slot for the column pass; with fp32 outputs the column pass recomputes them.
 template <typename E>
 struct EpiFwd1 : EpiBase {
   static constexpr bool kCols = true;
+  static constexpr bool kWriteback = sizeof(E) == 2;
   E* a; E* at; E* dst;
   long long ls;  // layer stride of a, at and dst (Tp*h)
   int h, Tp, n;
   __device__ __forceinline__ bool has_cols(int) const { return true; }
   __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
                                          float (&z)[8], const float (&)[8]) const {
-    float av[8];
+    float av[8], dv[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) av[e] = row < n ? z[e] * sigmoidf_(z[e]) : 0.0f;
+    for (int e = 0; e < 8; ++e) {
+      const float s = sigmoidf_(z[e]);
+      av[e] = row < n ? z[e] * s : 0.0f;
+      dv[e] = row < n ? s * (1.0f + z[e] * (1.0f - s)) : 0.0f;
+    }
     store8(a + (long long)layer * ls + (long long)row * h + col, av);
+    if constexpr (kWriteback) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) z[e] = __uint_as_float(pack_bf16(av[e], dv[e]));
+    }
     return 0.0f;
   }
   __device__ __forceinline__ void cols8(int, int layer, int row, int col, int, int,
@@ -525,10 +596,16 @@ struct EpiFwd1 : EpiBase {
     float av[8], dv[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float s = sigmoidf_(z[e]);
-      const bool ok = row + e < n;
-      av[e] = ok ? z[e] * s : 0.0f;
-      dv[e] = ok ? s * (1.0f + z[e] * (1.0f - s)) : 0.0f;
+      if constexpr (kWriteback) {
+        const uint32_t w = __float_as_uint(z[e]);
+        av[e] = __uint_as_float(w << 16);
+        dv[e] = __uint_as_float(w & 0xffff0000u);
+      } else {
+        const float s = sigmoidf_(z[e]);
+        const bool ok = row + e < n;
+        av[e] = ok ? z[e] * s : 0.0f;
+        dv[e] = ok ? s * (1.0f + z[e] * (1.0f - s)) : 0.0f;
+      }
     }
     const long long o = (long long)layer * ls + (long long)col * Tp + row;
     store8(at + o, av);
@@ -542,6 +619,7 @@ struct EpiFwd1 : EpiBase {
 // partials.
 template <typename E>
 struct EpiFwd2 : EpiBase {
+  static constexpr int kParts = 2;
   static constexpr bool kCols = true;
   E* g; E* gt;
   float* loss_part;       // [L][parts_per_layer]
@@ -583,6 +661,7 @@ struct EpiFwd2 : EpiBase {
 // weights the step started from; the update writes the other copy of a ping-pong pair.
 template <typename E>
 struct EpiBwdW2 : EpiBase {
+  static constexpr bool kPre = true;
   static constexpr bool kCols = true;
   static constexpr bool kWriteback = true;
   const E* dst; E* dzt;
@@ -632,6 +711,7 @@ struct EpiBwdW2 : EpiBase {
 // in bf16 mode the rounded copy the next segment's forward reads (fp32 mode reads the master).
 template <typename E>
 struct EpiW1 : EpiBase {
+  static constexpr bool kPre = true;
   float* w1; E* w1s;
   long long ls1;  // h*d
   int d;

@@ -168,6 +168,8 @@ hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi
   std::memset(&G, 0, sizeof G);
   int begin = 0;
   for (int i = 0; i < nspec; ++i) {
+    // the kernel reads as many operand parts as the epilogue type declares
+    if (specs[i].nparts < 1 || specs[i].nparts > Epi::kParts) return hipErrorInvalidValue;
     Problem& P = G.prob[i];
     P.part[0] = specs[i].part[0];
     P.part[1] = specs[i].part[1];
