@@ -179,9 +179,7 @@ struct TileCfg {
   static constexpr int NB = 2;
   static constexpr int ASLOT = BM * 128, BSLOT = BN * 128;
   static constexpr int RING = NA * ASLOT + NB * BSLOT;
-  static constexpr int PR = BM < 128 ? BM : 128;  // epilogue rows per pass
-  static constexpr int LDT = BN + 8;              // epilogue staging row stride (floats)
-  static constexpr int EPI_BYTES = PR * LDT * 4;
+  static constexpr int EPI_BYTES = 4 * 64 * 64 * 4;  // per-wave 64 x 64 fp32 staging
   static constexpr int SMEM = RING > EPI_BYTES ? RING : EPI_BYTES;
 };
 
@@ -203,18 +201,26 @@ template <int NM, int NR, int NV>
 __device__ __forceinline__ void interleave() {
   interleave_seq<NM, NR, NV>(std::make_integer_sequence<int, NM>{});
 }
-// The same after NRL leading LDS reads (the next sub-step's fragments, issued first so that
-// their latency hides behind this sub-step's MFMAs).
+// The LDS reads of the next sub-step's fragments (NRL of them) go first: four before the
+// first MFMA, then one after each MFMA until none is left (measured better than issuing all
+// of them at once or spreading them evenly); the NV buffer loads are spread evenly.
+template <int NM, int NR, int NV, int I>
+__device__ __forceinline__ void front_step() {
+  constexpr int r = I < NR ? 1 : 0;
+  constexpr int v = (NV * (I + 1)) / NM - (NV * I) / NM;
+  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                   // MFMA
+  if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);  // DS read
+  if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);  // VMEM read
+}
+template <int NM, int NR, int NV, int... I>
+__device__ __forceinline__ void front_seq(std::integer_sequence<int, I...>) {
+  (front_step<NM, NR, NV, I>(), ...);
+}
 template <int NRL, int NM, int NV>
 __device__ __forceinline__ void reads_then_interleave() {
-  __builtin_amdgcn_sched_group_barrier(0x100, NRL, 0);
-  interleave_seq<NM, 0, NV>(std::make_integer_sequence<int, NM>{});
-}
-
-// Staging position of tile element (r, c) within a pass.
-template <int LDT>
-__device__ __forceinline__ int stage_idx(int r, int c) {
-  return r * LDT + (c ^ (((r >> 3) & 15) << 2));
+  constexpr int lead = NRL < 4 ? NRL : 4;
+  __builtin_amdgcn_sched_group_barrier(0x100, lead, 0);
+  front_seq<NM, NRL - lead, NV>(std::make_integer_sequence<int, NM>{});
 }
 
 template <typename E, int BM, int BN, int WAVES_M, class Epi>
@@ -448,97 +454,92 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     __syncthreads();                // the epilogue reuses the LDS of the rings
   }
 
-  // ---- epilogue: stage through LDS, then row and column passes
-  // The tile goes through LDS in passes of PR rows.  Each pass: the waves holding those rows
-  // stage their accumulators, then every thread takes row chunks (8 consecutive columns of one
-  // row) for the row pass and, if the epilogue has one, column chunks (8 consecutive rows of
-  // one column) for the column pass.  Row chunks go in batches of EB; the memory reads an
-  // epilogue needs per chunk (pre8: the fp32 master, SiLU') are issued one batch ahead, the
-  // first batch before the first staging, so their latency overlaps staging and the previous
-  // batch's work.
-  constexpr int PR = TC::PR, LDT = TC::LDT;
-  constexpr int NPASS = BM / PR;
-  constexpr int RCH = PR * BN / 8 / 256;   // row chunks per thread per pass
-  constexpr int CCH = PR * BN / 8 / 256;   // column chunks per thread per pass
-  constexpr int EB = RCH < 8 ? RCH : 8;    // chunks per batch
-  constexpr int NBP = RCH / EB;            // batches per pass
-  constexpr int NBT = NPASS * NBP;         // batches per tile
-  static_assert(RCH >= 1 && RCH % EB == 0, "epilogue chunking");
-  float* st = reinterpret_cast<float*>(smem);
+  // ---- epilogue: each wave stages its own accumulators through LDS, 64 x 64 at a time
+  // A wave's tile is processed in 64 x 64 sub-blocks (2 x 2 MFMA blocks) in a private 16 KiB
+  // LDS region, so the epilogue needs no workgroup synchronisation.  Per sub-block: stage the
+  // accumulators; row pass: each lane takes row chunks (8 consecutive columns of one row;
+  // 8 lanes cover a 64-column row segment); column pass, if the epilogue has one: column
+  // chunks (8 consecutive rows of one column; 8 lanes cover the 64 rows of a column).  The
+  // memory reads an epilogue needs per row chunk (pre8: the fp32 master, SiLU') are issued one
+  // sub-block ahead, the first before the first staging.  Staging layout: row r, column c at
+  // r*64 + (c ^ sw(r)) with sw(r) = ((r ^ r/8) & 7) * 4, which keeps 4-column groups intact
+  // (16-byte reads) and spreads the 8 rows of a column chunk over distinct banks.
+  constexpr int SB = 64;                        // sub-block edge
+  constexpr int NSM = WM / SB, NSN = WN / SB;   // sub-blocks per wave
+  constexpr int NSB = NSM * NSN;
+  constexpr int CPL = SB * SB / 8 / 64;         // row (and column) chunks per lane: 8
+  static_assert(WM % SB == 0 && WN % SB == 0, "wave tile");
+  float* stw = reinterpret_cast<float*>(smem) + wave * (SB * SB);
+  auto sidx = [](int r, int c) { return r * SB + (c ^ (((r ^ (r >> 3)) & 7) << 2)); };
+  auto wave_sync = [] {  // this wave's LDS writes are visible to all its lanes
+    __builtin_amdgcn_s_waitcnt((63 & 15) | ((63 >> 4) << 14) | (7 << 4));  // lgkmcnt(0)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
   float partial = 0.0f;
-  float aux[2][EB][8];
-  auto issue_pre = [&](int bi, float (&ax)[EB][8]) {
-    const int row0 = m0 + (bi / NBP) * PR;
+  float aux[2][CPL][8];
+  const int rl = lane >> 3, ql = lane & 7;      // row-chunk lane coordinates
+  auto issue_pre = [&](int sb, float (&ax)[CPL][8]) {
+    const int grow = m0 + wm * WM + (sb / NSN) * SB, gcol = n0 + wn * WN + (sb % NSN) * SB;
 #pragma unroll
-    for (int b = 0; b < EB; ++b) {
-      const int q = tid + 256 * ((bi % NBP) * EB + b);
-      const int r = q / (BN / 8), c = (q % (BN / 8)) * 8;
-      if (row0 + r < P.M && n0 + c < P.N)
-        G.epi.pre8(pi, layer, row0 + r, n0 + c, P.M, P.N, ax[b]);
+    for (int b = 0; b < CPL; ++b) {
+      const int row = grow + rl + 8 * b, col = gcol + 8 * ql;
+      if (row < P.M && col < P.N) G.epi.pre8(pi, layer, row, col, P.M, P.N, ax[b]);
     }
   };
   if constexpr (Epi::kPre) issue_pre(0, aux[0]);
-  // unrolled only where the batch buffers alternate across passes
-  constexpr int PASS_UNROLL = Epi::kPre ? NPASS : 1;
-#pragma unroll PASS_UNROLL
-  for (int p = 0; p < NPASS; ++p) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const int r0 = wm * WM + i * 32 - p * PR;  // first pass-local row of block i
-      if (r0 < 0 || r0 >= PR) continue;          // uniform per wave
+  for (int sb = 0; sb < NSB; ++sb) {
+    const int sm = sb / NSN, sn = sb % NSN;
+    const int grow = m0 + wm * WM + sm * SB, gcol = n0 + wn * WN + sn * SB;
+    if (sb > 0) wave_sync();  // the previous sub-block's reads are done
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int c = wn * WN + j * 32 + (lane & 31);
+    for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
         for (int g = 0; g < 4; ++g)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            st[stage_idx<LDT>(r0 + g * 8 + (lane >> 5) * 4 + e, c)] = acc[i][j][4 * g + e];
-      }
+            stw[sidx(ii * 32 + g * 8 + (lane >> 5) * 4 + e, jj * 32 + (lane & 31))] =
+                acc[2 * sm + ii][2 * sn + jj][4 * g + e];
+    wave_sync();
+    if constexpr (Epi::kPre) {
+      if (sb + 1 < NSB) issue_pre(sb + 1, aux[(sb + 1) & 1]);
     }
-    __syncthreads();
-    const int row0 = m0 + p * PR;
 #pragma unroll
-    for (int bb = 0; bb < NBP; ++bb) {
-      const int bi = p * NBP + bb;
-      if constexpr (Epi::kPre) {
-        if (bi + 1 < NBT) issue_pre(bi + 1, aux[(bi + 1) & 1]);
-      }
-#pragma unroll
-      for (int b = 0; b < EB; ++b) {
-        const int q = tid + 256 * (bb * EB + b);
-        const int r = q / (BN / 8), c = (q % (BN / 8)) * 8;
-        float* s0 = st + stage_idx<LDT>(r, c);
-        float* s1 = st + stage_idx<LDT>(r, c + 4);
-        float v[8];
-        const float4 x0 = *reinterpret_cast<const float4*>(s0);
-        const float4 x1 = *reinterpret_cast<const float4*>(s1);
-        v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
-        v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
-        if (row0 + r >= P.M || n0 + c >= P.N) continue;
-        partial += G.epi.rows8(pi, layer, row0 + r, n0 + c, P.M, P.N, v, aux[bi & 1][b]);
-        if constexpr (Epi::kWriteback) {
-          *reinterpret_cast<float4*>(s0) = make_float4(v[0], v[1], v[2], v[3]);
-          *reinterpret_cast<float4*>(s1) = make_float4(v[4], v[5], v[6], v[7]);
-        }
+    for (int b = 0; b < CPL; ++b) {
+      const int r = rl + 8 * b, c = 8 * ql;
+      float* s0 = stw + sidx(r, c);
+      float* s1 = stw + sidx(r, c + 4);
+      float v[8];
+      const float4 x0 = *reinterpret_cast<const float4*>(s0);
+      const float4 x1 = *reinterpret_cast<const float4*>(s1);
+      v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
+      v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
+      if (grow + r >= P.M || gcol + c >= P.N) continue;
+      partial += G.epi.rows8(pi, layer, grow + r, gcol + c, P.M, P.N, v, aux[sb & 1][b]);
+      if constexpr (Epi::kWriteback) {
+        *reinterpret_cast<float4*>(s0) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(s1) = make_float4(v[4], v[5], v[6], v[7]);
       }
     }
     if constexpr (Epi::kCols) {
       if (G.epi.has_cols(pi)) {
-        if constexpr (Epi::kWriteback) __syncthreads();
+        if constexpr (Epi::kWriteback) wave_sync();
+        const int kc = lane & 7;  // row group of this lane's column chunks
 #pragma unroll
-        for (int b = 0; b < CCH; ++b) {
-          const int q = tid + 256 * b;
-          const int k = q % (PR / 8), c = q / (PR / 8);
-          if (row0 + 8 * k + 8 > P.M || n0 + c >= P.N) continue;
+        for (int b = 0; b < CPL; ++b) {
+          const int c = (lane >> 3) + 8 * b;
+          if (grow + 8 * kc + 8 > P.M || gcol + c >= P.N) continue;
           float v[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = st[stage_idx<LDT>(8 * k + e, c)];
-          G.epi.cols8(pi, layer, row0 + 8 * k, n0 + c, P.M, P.N, v);
+          for (int e = 0; e < 8; ++e) v[e] = stw[sidx(8 * kc + e, c)];
+          G.epi.cols8(pi, layer, grow + 8 * kc, gcol + c, P.M, P.N, v);
         }
       }
     }
-    __syncthreads();
   }
   G.epi.finish(layer, t, wave, lane, partial);
 }
