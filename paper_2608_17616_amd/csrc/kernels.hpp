@@ -378,19 +378,19 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   constexpr int WAIT_STEP = (VMC & 15) | ((VMC >> 4) << 14) | (7 << 4);
   if (nk > 0) {
     u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
-#pragma unroll
-    for (int k = 0; k < NA - 1; ++k) {
-      if (k < nk0) load_a(Part0{}, k, k, 0, LA);
-      else load_a(Part1{}, k, k, 0, LA);
+    // Prologue: step 0 first, then (ring of 3) A's step 1 and the first half of B's step 1,
+    // which may still be in flight when step 0 starts.
+    if (nk0 > 0) { load_a(Part0{}, 0, 0, 0, LA); load_b(Part0{}, 0, 0, 0, LB); }
+    else { load_a(Part1{}, 0, 0, 0, LA); load_b(Part1{}, 0, 0, 0, LB); }
+    if constexpr (NA > 2) {
+      if (nk0 > 1) { load_a(Part0{}, 1, 1, 0, LA); load_b(Part0{}, 1, 1, 0, LB / 2); }
+      else { load_a(Part1{}, 1, 1, 0, LA); load_b(Part1{}, 1, 1, 0, LB / 2); }
     }
-    if (nk0 > 0) load_b(Part0{}, 0, 0, 0, LB);
-    else load_b(Part1{}, 0, 0, 0, LB);
-    if constexpr (NA > 2) {  // the first half of B's step 1 (the loop issues the rest)
-      if (nk0 > 1) load_b(Part0{}, 1, 1, 0, LB / 2);
-      else load_b(Part1{}, 1, 1, 0, LB / 2);
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // all counters 0: the prologue's loads have reached LDS
-    __syncthreads();
+    constexpr int VPRO = NA > 2 ? LA + LB / 2 : 0;  // prologue loads allowed in flight
+    __builtin_amdgcn_s_waitcnt((VPRO & 15) | ((VPRO >> 4) << 14) | (7 << 4));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
     int sa = 0, sb = 0;
     read_frags(sa, sb, 0, fa0, fb0);
     auto step = [&](int kt, auto pa, auto pb) {
