@@ -15,12 +15,18 @@ Distributions (the workloads' stated defaults):
   W_k, W_v ~ N(0, 1/d)   stacked as W_kv = [W_k; W_v], shape [2*d_kv, d]
   W1 ~ N(0, 1/d)         shape [h, d]      (variance 1/fan_in)
   W2 ~ N(0, 1/h)         shape [2*d_kv, h] (variance 1/fan_in)
+Meta-parameters of the paper's optimiser (trained offline in the paper; synthetic here):
+  u, v ~ N(0, 1/d)       rate and decay projections, shape [d] each
+  b_u = log(e - 1)       so that softplus(b_u) = 1: rates average about lr
+  b_v = 0                decays average about 1/2
 """
 from __future__ import annotations
 
 import numpy as np
 
-KIND_WK, KIND_WV, KIND_W1, KIND_W2, KIND_X, KIND_XQ = range(6)
+KIND_WK, KIND_WV, KIND_W1, KIND_W2, KIND_X, KIND_XQ, KIND_U, KIND_V = range(8)
+B_U = float(np.log(np.e - 1.0))
+B_V = 0.0
 
 
 def normal(seed: int, kind: int, layer: int, index: int, shape, std: float) -> np.ndarray:
@@ -70,6 +76,14 @@ def layer_w2(cfg, layer: int) -> np.ndarray:
     """Initial fast weight W2 (W_out) of one layer, [2*d_kv, h], float32."""
     return normal(cfg.seed, KIND_W2, layer, 0, (cfg.d_out, cfg.d_hidden),
                   1.0 / np.sqrt(cfg.d_hidden))
+
+
+def layer_meta(cfg, layer: int):
+    """Optimiser meta-parameters of one layer: (u [d], b_u, v [d], b_v), float32 vectors."""
+    d = cfg.d_model
+    u = normal(cfg.seed, KIND_U, layer, 0, (d,), 1.0 / np.sqrt(d))
+    v = normal(cfg.seed, KIND_V, layer, 0, (d,), 1.0 / np.sqrt(d))
+    return u, np.float32(B_U), v, np.float32(B_V)
 
 
 def segment_x(cfg, layer: int, s: int, n_tokens: int | None = None) -> np.ndarray:
