@@ -38,6 +38,22 @@ def stage_work(cfg, q):
     """Algorithmic FLOPs and bytes of one launch of each stage (all layers)."""
     L, d, h, D, T = cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out, cfg.seg_len
     E = 2 if cfg.act_dtype == "bf16" else 4
+    if cfg.optimizer == "paper":
+        # momentum read-modify-write in the update epilogues; the copies move to RENORM
+        cp1 = E if cfg.act_dtype == "bf16" else 0
+        return {
+            "xt": (0, L * T * d * E * 2),
+            "rate": (L * 4 * T * d, L * (T * d * E + 2 * d * 4 + T * 4)),
+            "fwd1": (L * 2 * T * d * h, L * (T * d + h * d + T * h * 3) * E),
+            "fwd2": (L * 2 * T * D * (h + d), L * ((T * h + D * h + T * d + D * d + 2 * T * D) * E
+                                                   + T * 4)),
+            "bwd": (L * (2 * T * D * h + 2 * T * D * h),
+                    L * ((T * D + h * D + 2 * T * h + D * T + h * T) * E + D * h * 16)),
+            "upd": (L * 2 * T * h * d, L * ((h * T + d * T) * E + h * d * 16)),
+            "renorm": (0, L * (h * d * (8 + cp1) + D * h * (8 + 2 * E))),
+            "kv1": (L * 2 * q * d * h, L * (q * d + h * d + q * h) * E),
+            "kv2": (L * 2 * q * h * D, L * (q * h + D * h) * E + L * q * D * 4),
+        }
     return {
         "xt": (0, L * T * d * E * 2),
         "fwd1": (L * 2 * T * d * h, L * (T * d + h * d + T * h * 3) * E),
@@ -72,7 +88,7 @@ def counted_traffic(stage):
         return None
 
 
-def cpu_baseline(cfg, w1, w2, wkv, xs, budget_s):
+def cpu_baseline(cfg, w1, w2, wkv, xs, budget_s, meta=None):
     import numpy as np
 
     import oracle as orc
@@ -84,9 +100,17 @@ def cpu_baseline(cfg, w1, w2, wkv, xs, budget_s):
         cores = os.cpu_count() or 1
     w1 = np.asarray(w1, np.float64)
     w2 = np.asarray(w2, np.float64)
+    if meta is not None:
+        norms0 = (orc.row_norms(w1), orc.row_norms(w2))
+        m1, m2 = np.zeros_like(w1), np.zeros_like(w2)
     done, t0 = 0, time.perf_counter()
     while True:
-        w1, w2, _ = orc.ttl_step(xs[done % len(xs)], w1, w2, wkv, cfg.lr, cfg.loss)
+        x = xs[done % len(xs)]
+        if meta is None:
+            w1, w2, _ = orc.ttl_step(x, w1, w2, wkv, cfg.lr, cfg.loss)
+        else:
+            w1, w2, m1, m2, _, _ = orc.paper_step(x, w1, w2, m1, m2, wkv, meta, norms0, cfg.lr,
+                                                  cfg.loss)
         done += 1
         if time.perf_counter() - t0 >= budget_s or done >= 64:
             break
@@ -109,6 +133,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this size (HBM counter calibration)")
+    ap.add_argument("--optimizer", default="sgd", choices=("sgd", "paper"),
+                    help="the configuration's SGD, or the paper's optimiser (per-token rates, "
+                         "momentum, row renormalisation)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: this build measures one GPU "
@@ -121,7 +148,7 @@ def main():
 
     from paper_2608_17616_amd import configs, inputs, mone
 
-    cfg = configs.CONFIGS[args.config]
+    cfg = configs.CONFIGS[args.config].with_(optimizer=args.optimizer)
     L, d, h, D, T, Q = (cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out, cfg.seg_len,
                         cfg.n_query)
     S = args.segments or cfg.n_segments
@@ -149,8 +176,18 @@ def main():
                   wkv[0].double().cpu().numpy(),
                   [ctx[s, 0].double().cpu().numpy() for s in range(n_cpu)])
 
+    opt = None
+    if cfg.optimizer == "paper":
+        opt = (inputs.device_normal_(torch.empty(L, d, dtype=torch.float32, device=dev),
+                                     1 / np.sqrt(d), gen),
+               torch.full((L,), inputs.B_U, dtype=torch.float32, device=dev),
+               inputs.device_normal_(torch.empty(L, d, dtype=torch.float32, device=dev),
+                                     1 / np.sqrt(d), gen),
+               torch.full((L,), inputs.B_V, dtype=torch.float32, device=dev),
+               torch.zeros(L, h, d, dtype=torch.float32, device=dev),
+               torch.zeros(L, D, h, dtype=torch.float32, device=dev))
     stream = torch.cuda.current_stream(dev)
-    sess = mone.TtlSession(cfg, wkv, w1, w2, stream)
+    sess = mone.TtlSession(cfg, wkv, w1, w2, stream, opt=opt)
     H = sess.handle
     sptr = stream.cuda_stream
 
@@ -170,7 +207,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    mone.mone_ttl_set_stage_timing(H, args.steps * (S * 5 + 2))
+    mone.mone_ttl_set_stage_timing(H, args.steps * (S * 7 + 2))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -208,7 +245,8 @@ def main():
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(dby / davg / 1e9, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(dby / davg / 1e9 / PEAK_HBM_GBS, 4), "traffic": None}
-    counted = counted_traffic(dom) if (args.config == "8b" and S >= 1) else None
+    counted = (counted_traffic(dom) if (args.config == "8b" and cfg.optimizer == "sgd" and S >= 1)
+               else None)
     if counted:
         roof["traffic"] = counted["read_bytes"] + counted["write_bytes"]
         roof["traffic_detail"] = dict(counted, algorithmic_bytes=dby,
@@ -220,9 +258,10 @@ def main():
         "ms_per_step": round(elapsed / args.steps * 1e3, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": cfg.act_dtype, "data": "synthetic",
         "config": {"workload": f"{cfg.name}-class TTL: L={L} d={d} h={h} D={D} T={T} "
-                               f"N={S * T} ({S} segments) + read Q={Q}",
+                               f"N={S * T} ({S} segments) + read Q={Q}"
+                               + (", paper optimiser" if cfg.optimizer == "paper" else ""),
                    "n_layers": L, "d_model": d, "d_hidden": h, "d_out": D, "seg_len": T,
-                   "n_context": S * T, "n_query": Q, "lr": cfg.lr},
+                   "n_context": S * T, "n_query": Q, "lr": cfg.lr, "optimizer": cfg.optimizer},
         "mfma_pct": round(mfma_pct, 2),
         "flop_per_token": flop_tok,
         "roofline": roof,
@@ -230,7 +269,11 @@ def main():
         "finite": finite,
     }
     if cpu_in is not None:
-        out["cpu_baseline"] = cpu_baseline(cfg, *cpu_in, args.cpu_seconds)
+        meta = None
+        if opt is not None:
+            meta = (opt[0][0].double().cpu().numpy(), float(opt[1][0]),
+                    opt[2][0].double().cpu().numpy(), float(opt[3][0]))
+        out["cpu_baseline"] = cpu_baseline(cfg, *cpu_in, args.cpu_seconds, meta)
     print(json.dumps(out), flush=True)
 
 

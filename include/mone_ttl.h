@@ -14,7 +14,11 @@
  *   loss     L_s = (1/n) sum_j ||M(x_j) - t_j||^2 over the n tokens of the segment
  *            (segment-level average of Sec. 3.3; MONE_LOSS_MSE_MEAN also divides by D);
  *   update   W <- W - lr * dL_s/dW for W1 and W2, both gradients taken at W_{s-1}
- *            (Eq. update with a plain SGD step).
+ *            (Eq. update with a plain SGD step),
+ *            or, with MONE_OPT_PAPER (mone_ttl_init_paper), the paper's own optimiser: a
+ *            softplus per-token learning rate, momentum with a sigmoid decay predicted from
+ *            the segment, and a channel-wise L2 renormalisation after each update (the
+ *            exact form is stated at mone_ttl_init_paper).
  *
  * Conventions for every call:
  *   - Matrices are row-major.  W1 is [h][d] (acts on column vectors: z = W1 x), W2 is [D][h],
@@ -56,6 +60,11 @@ typedef enum {
   MONE_LOSS_MSE_MEAN = 1  /* l_j = ||y_j - t_j||^2 / D; dL_s/dY = (2/(n D))(Y - T) */
 } mone_loss;
 
+typedef enum {
+  MONE_OPT_SGD = 0,   /* W -= lr * grad (mone_ttl_init) */
+  MONE_OPT_PAPER = 1  /* per-token rates, momentum, renormalisation (mone_ttl_init_paper) */
+} mone_optimizer;
+
 typedef struct {
   int32_t n_layers;  /* L >= 1: layers with a memory */
   int32_t d_model;   /* d: width of the hidden states x (memory input) */
@@ -65,15 +74,17 @@ typedef struct {
   int32_t act_dtype; /* mone_dtype of x, x_q, W_kv and stored intermediates; the fast weights
                         are always fp32 */
   int32_t loss;      /* mone_loss */
-  float lr;          /* SGD learning rate (finite, may be 0) */
+  float lr;          /* learning rate (finite, may be 0); with MONE_OPT_PAPER it scales the
+                        per-token rates */
+  int32_t optimizer; /* mone_optimizer */
 } mone_ttl_config;
 
 typedef struct mone_ttl mone_ttl; /* opaque host object */
 
-/* Number of workspace bytes a handle for `cfg` needs.  It depends on L, d, h, d_kv, T and the
- * activation dtype only -- never on the context length N, which is not an argument anywhere:
- * the memory's footprint is constant in N (Sec. 4.3).  Returns 0 if `cfg` is invalid or
- * unsupported (mone_ttl_last_error() says why). */
+/* Number of workspace bytes a handle for `cfg` needs.  It depends on L, d, h, d_kv, T, the
+ * activation dtype and the optimiser only -- never on the context length N, which is not an
+ * argument anywhere: the memory's footprint is constant in N (Sec. 4.3).  Returns 0 if `cfg` is
+ * invalid or unsupported (mone_ttl_last_error() says why). */
 size_t mone_ttl_workspace_bytes(const mone_ttl_config* cfg);
 
 /* Create a handle over caller-owned state (the initial state W_0, s = 0 in Sec. 3.1).
@@ -91,6 +102,34 @@ size_t mone_ttl_workspace_bytes(const mone_ttl_config* cfg);
  * On success *out receives the handle; on failure *out is left NULL. */
 int mone_ttl_init(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, float* w1,
                   float* w2, void* workspace, size_t workspace_bytes, void* stream);
+
+/* The paper's optimiser (Sec. 3.3, Eq. update; implementation details, App. A.2), whose
+ * exact form the paper leaves open; the reading implemented, per layer and segment of n tokens:
+ *   eta_j  = lr * softplus(u . x_j + b_u)            per-token learning rate
+ *   beta   = sigmoid(v . mean_j(x_j) + b_v)          momentum decay, one per layer and segment
+ *   g      = gradient of (1/n) sum_j eta_j l_j at W_{s-1}
+ *   mu     = beta * mu + g;   W = W - mu             (for W1 and W2; mu starts as given)
+ *   W      = W with each row (output channel) rescaled to the L2 norm it had in the weights
+ *            the handle was created from (a row of norm 0 stays as it is).
+ * Since the rescaling keeps every row norm, resuming from a checkpoint (a copy of w1, w2, mom1,
+ * mom2) restores the same targets.  Pointers (device, fp32, 16-byte aligned, borrowed for the
+ * handle's lifetime; u and v are read, mom1 and mom2 are state updated in place): */
+typedef struct {
+  const float* rate_w;   /* u   [L][d] */
+  const float* rate_b;   /* b_u [L] */
+  const float* decay_w;  /* v   [L][d] */
+  const float* decay_b;  /* b_v [L] */
+  float* mom1;           /* mu of W1 [L][h][d]; zero for a fresh state */
+  float* mom2;           /* mu of W2 [L][D][h]; zero for a fresh state */
+} mone_paper_optimizer;
+
+/* mone_ttl_init for cfg->optimizer == MONE_OPT_PAPER (mone_ttl_init rejects that value, this
+ * call rejects any other).  Also enqueues the computation of the row norms of w1 and w2 (the
+ * renormalisation targets).  Errors as mone_ttl_init; opt and every pointer in it must be
+ * non-NULL. */
+int mone_ttl_init_paper(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, float* w1,
+                        float* w2, const mone_paper_optimizer* opt, void* workspace,
+                        size_t workspace_bytes, void* stream);
 
 /* One test-time-learning step of every layer on one segment (Eq. update; Sec. 3.4).
  *   x         [L][n_tokens][d] act_dtype: the segment's hidden states at each layer.
@@ -133,12 +172,14 @@ const char* mone_ttl_last_error(void);
 /* Stages of one segment and of one read, in launch order. */
 #define MONE_STAGE_XT 0    /* X -> X^T staging copy (operand of the W1 gradient) */
 #define MONE_STAGE_FWD1 1  /* Z = X W1^T; A = SiLU(Z) */
-#define MONE_STAGE_FWD2 2  /* R = A W2^T - X W_kv^T; G = c R; loss partials */
-#define MONE_STAGE_BWD 3   /* dZ = (G W2) * SiLU'(Z), and W2 -= lr G^T A (one grouped launch) */
-#define MONE_STAGE_UPD 4   /* W1 -= lr dZ^T X */
+#define MONE_STAGE_FWD2 2  /* R = A W2^T - X W_kv^T; G = c R (times the rates); loss partials */
+#define MONE_STAGE_BWD 3   /* dZ = (G W2) * SiLU'(Z), and the W2 update (one grouped launch) */
+#define MONE_STAGE_UPD 4   /* the W1 update (dZ^T X) */
 #define MONE_STAGE_KV1 5   /* read: A_q = SiLU(X_q W1^T) */
 #define MONE_STAGE_KV2 6   /* read: KV = A_q W2^T */
-#define MONE_N_STAGES 7
+#define MONE_STAGE_RATE 7  /* MONE_OPT_PAPER: per-token rates and the momentum decay */
+#define MONE_STAGE_RENORM 8 /* MONE_OPT_PAPER: row renormalisation of W1, W2 and their copies */
+#define MONE_N_STAGES 9
 
 /* Enable (max_records > 0) or disable (0) per-stage timing: each subsequent stage launch is
  * bracketed by a pair of HIP events recorded on the call's stream, up to max_records pairs

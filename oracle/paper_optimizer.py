@@ -4,7 +4,7 @@ Only the test-suite, the package's smoke check and the benchmark's CPU-baseline 
 this module; the product path never calls it.
 
 The configuration-mode oracle (mone_oracle) takes a plain SGD step.  The paper's own optimiser
-(Eq. update, and the implementation details of its experimental setup) replaces it with:
+(Sec. 3.3, Eq. update; implementation details in App. A.2) replaces it with:
   * a per-token learning rate, softplus-activated and predicted from the token;
   * momentum whose decay beta_s in (0, 1) is sigmoid-activated and predicted from the hidden
     states of the segment ("chunk");

@@ -25,10 +25,11 @@ class MoneConfig:
     seg_len: int       # T: tokens per segment
     n_context: int     # N: context tokens; S = N / T segments
     act_dtype: str     # "f32" or "bf16": dtype of x, x_q, W_kv and stored intermediates
-    lr: float          # SGD learning rate
+    lr: float          # learning rate (scales the per-token rates of the paper optimiser)
     loss: str = "mse_sum"   # "mse_sum": c = 2/T ; "mse_mean": c = 2/(T*D)
     n_query: int = 64  # Q: query tokens for the read step
     seed: int = 0
+    optimizer: str = "sgd"  # "sgd" or "paper" (per-token rates, momentum, renormalisation)
 
     @property
     def d_out(self) -> int:

@@ -478,9 +478,10 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   };
   float partial = 0.0f;
-  float aux[2][CPL][8];
+  constexpr int NAUX = Epi::kAux;
+  float aux[2][CPL][NAUX];
   const int rl = lane >> 3, ql = lane & 7;      // row-chunk lane coordinates
-  auto issue_pre = [&](int sb, float (&ax)[CPL][8]) {
+  auto issue_pre = [&](int sb, float (&ax)[CPL][NAUX]) {
     const int grow = m0 + wm * WM + (sb / NSN) * SB, gcol = n0 + wn * WN + (sb % NSN) * SB;
 #pragma unroll
     for (int b = 0; b < CPL; ++b) {
@@ -518,11 +519,23 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       const float4 x1 = *reinterpret_cast<const float4*>(s1);
       v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
       v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
-      if (grow + r >= P.M || gcol + c >= P.N) continue;
-      partial += G.epi.rows8(pi, layer, grow + r, gcol + c, P.M, P.N, v, aux[sb & 1][b]);
-      if constexpr (Epi::kWriteback) {
-        *reinterpret_cast<float4*>(s0) = make_float4(v[0], v[1], v[2], v[3]);
-        *reinterpret_cast<float4*>(s1) = make_float4(v[4], v[5], v[6], v[7]);
+      const bool ok = grow + r < P.M && gcol + c < P.N;
+      float val = 0.0f;
+      if (ok) {
+        val = G.epi.rows8(pi, layer, grow + r, gcol + c, P.M, P.N, v, aux[sb & 1][b]);
+        if constexpr (Epi::kWriteback) {
+          *reinterpret_cast<float4*>(s0) = make_float4(v[0], v[1], v[2], v[3]);
+          *reinterpret_cast<float4*>(s1) = make_float4(v[4], v[5], v[6], v[7]);
+        }
+      }
+      if constexpr (Epi::kRowNorm) {
+        // the 8 lanes of a row segment are lanes 8*rl .. 8*rl+7: a fixed-order tree sum
+        val += __shfl_xor(val, 1, 64);
+        val += __shfl_xor(val, 2, 64);
+        val += __shfl_xor(val, 4, 64);
+        if (ok && ql == 0) G.epi.row_partial(pi, layer, grow + r, gcol / SB, val);
+      } else {
+        partial += val;
       }
     }
     if constexpr (Epi::kCols) {
@@ -556,6 +569,10 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
 struct EpiBase {
   static constexpr int kParts = 1;  // K-concatenated operand parts the problems may have
   static constexpr bool kPre = false;  // pre8 reads memory (loads are issued a batch ahead)
+  static constexpr int kAux = 8;       // floats pre8 reads per row chunk
+  static constexpr bool kRowNorm = false;  // rows8 returns the chunk's sum of squares, which
+                                           // is reduced per 64-column row segment
+  __device__ __forceinline__ void row_partial(int, int, int, int, float) const {}
   static constexpr bool kCols = false;
   static constexpr bool kWriteback = false;
   __device__ __forceinline__ bool has_cols(int) const { return false; }
@@ -624,18 +641,20 @@ struct EpiFwd2 : EpiBase {
   static constexpr bool kCols = true;
   E* g; E* gt;
   float* loss_part;       // [L][parts_per_layer]
+  const float* rate;      // [L][Tp] per-token rates (the paper's optimiser), or null
   long long ls;           // Tp*D
   int D, Tp, n, parts_per_layer;
   float c;
   __device__ __forceinline__ bool has_cols(int) const { return true; }
   __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
                                          float (&v)[8], const float (&)[8]) const {
+    const float cr = rate ? c * rate[(long long)layer * Tp + row] : c;
     float gv[8], s = 0.0f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float r = row < n ? -v[e] : 0.0f;
       s += r * r;
-      gv[e] = c * r;
+      gv[e] = cr * r;
     }
     store8(g + (long long)layer * ls + (long long)row * D + col, gv);
     return s;
@@ -644,7 +663,10 @@ struct EpiFwd2 : EpiBase {
                                         const float (&v)[8]) const {
     float gv[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) gv[e] = row + e < n ? -c * v[e] : 0.0f;
+    for (int e = 0; e < 8; ++e) {
+      const float cr = rate ? c * rate[(long long)layer * Tp + row + e] : c;
+      gv[e] = row + e < n ? -cr * v[e] : 0.0f;
+    }
     store8(gt + (long long)layer * ls + (long long)col * Tp + row, gv);
   }
   __device__ __forceinline__ void finish(int layer, int tile, int wave, int lane, float s) const {
@@ -660,11 +682,16 @@ struct EpiFwd2 : EpiBase {
 // [D][h]; fp32 read-modify-write of the master (rows), then the copies the next segment reads:
 // -W2 [D][h] (rows) and W2^T [h][D] (columns).  The backward reads the W2^T copy of the
 // weights the step started from; the update writes the other copy of a ping-pong pair.
-template <typename E>
+// With the paper's optimiser (PAPER), problem 1 updates the momentum, mu2 = beta mu2 + G^T A
+// (the rates are already in G), and the master, W2 - mu2, both fp32; it returns each row
+// chunk's sum of squares for the renormalisation, which writes the copies afterwards.
+template <typename E, bool PAPER = false>
 struct EpiBwdW2 : EpiBase {
   static constexpr bool kPre = true;
-  static constexpr bool kCols = true;
-  static constexpr bool kWriteback = true;
+  static constexpr int kAux = PAPER ? 16 : 8;
+  static constexpr bool kRowNorm = PAPER;
+  static constexpr bool kCols = !PAPER;
+  static constexpr bool kWriteback = !PAPER;
   const E* dst; E* dzt;
   long long lst;       // Tp*h
   int Tp, n;
@@ -672,16 +699,23 @@ struct EpiBwdW2 : EpiBase {
   long long ls2;       // D*h
   int h, D;
   float lr;
-  __device__ __forceinline__ bool has_cols(int pi) const { return pi == 1; }
+  float* mom2;         // PAPER: [L][D][h] momentum
+  const float* beta;   // PAPER: [L] momentum decay of this segment
+  float* ss2;          // PAPER: [L][D][h/64] row-segment sums of squares
+  __device__ __forceinline__ bool has_cols(int pi) const { return !PAPER && pi == 1; }
   __device__ __forceinline__ void pre8(int pi, int layer, int row, int col, int, int,
-                                       float (&x)[8]) const {
-    if (pi == 0)
-      load8(dst + (long long)layer * lst + (long long)row * Tp + col, x);
-    else
-      load8(w2 + (long long)layer * ls2 + (long long)row * h + col, x);
+                                       float (&x)[kAux]) const {
+    float (&x0)[8] = *reinterpret_cast<float(*)[8]>(&x[0]);
+    if (pi == 0) {
+      load8(dst + (long long)layer * lst + (long long)row * Tp + col, x0);
+    } else {
+      const long long o = (long long)layer * ls2 + (long long)row * h + col;
+      load8(w2 + o, x0);
+      if constexpr (PAPER) load8(mom2 + o, *reinterpret_cast<float(*)[8]>(&x[8]));
+    }
   }
   __device__ __forceinline__ float rows8(int pi, int layer, int row, int col, int, int,
-                                         float (&v)[8], const float (&x)[8]) const {
+                                         float (&v)[8], const float (&x)[kAux]) const {
     if (pi == 0) {
       float dz[8];
 #pragma unroll
@@ -689,18 +723,35 @@ struct EpiBwdW2 : EpiBase {
       store8(dzt + (long long)layer * lst + (long long)row * Tp + col, dz);
       return 0.0f;
     }
-    float nw[8], cp[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      nw[e] = x[e] - lr * v[e];
-      cp[e] = -nw[e];
-    }
     const long long o = (long long)layer * ls2 + (long long)row * h + col;
-    store8(w2 + o, nw);
-    store8(w2n + o, cp);
+    if constexpr (PAPER) {
+      const float b = beta[layer];
+      float m[8], nw[8], ss = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = nw[e];
-    return 0.0f;
+      for (int e = 0; e < 8; ++e) {
+        m[e] = b * x[8 + e] + v[e];
+        nw[e] = x[e] - m[e];
+        ss += nw[e] * nw[e];
+      }
+      store8(mom2 + o, m);
+      store8(w2 + o, nw);
+      return ss;
+    } else {
+      float nw[8], cp[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        nw[e] = x[e] - lr * v[e];
+        cp[e] = -nw[e];
+      }
+      store8(w2 + o, nw);
+      store8(w2n + o, cp);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = nw[e];
+      return 0.0f;
+    }
+  }
+  __device__ __forceinline__ void row_partial(int pi, int layer, int row, int cb, float ss) const {
+    if (PAPER && pi == 1) ss2[((long long)layer * D + row) * (h / 64) + cb] = ss;
   }
   __device__ __forceinline__ void cols8(int, int layer, int row, int col, int, int,
                                         const float (&v)[8]) const {
@@ -710,27 +761,54 @@ struct EpiBwdW2 : EpiBase {
 
 // W1 update: tile of dZ^T X = dL/dW1 of W1 [h][d]; fp32 read-modify-write of the master, and
 // in bf16 mode the rounded copy the next segment's forward reads (fp32 mode reads the master).
-template <typename E>
+// With the paper's optimiser (PAPER): mu1 = beta mu1 + dZ^T X, W1 - mu1 (fp32), and each row
+// chunk's sum of squares for the renormalisation, which writes the copy afterwards.
+template <typename E, bool PAPER = false>
 struct EpiW1 : EpiBase {
   static constexpr bool kPre = true;
+  static constexpr int kAux = PAPER ? 16 : 8;
+  static constexpr bool kRowNorm = PAPER;
   float* w1; E* w1s;
   long long ls1;  // h*d
   int d;
   int w1_copy;
   float lr;
+  float* mom1;         // PAPER: [L][h][d] momentum
+  const float* beta;   // PAPER: [L]
+  float* ss1;          // PAPER: [L][h][d/64] row-segment sums of squares
+  int h;
   __device__ __forceinline__ void pre8(int, int layer, int row, int col, int, int,
-                                       float (&w)[8]) const {
-    load8(w1 + (long long)layer * ls1 + (long long)row * d + col, w);
+                                       float (&w)[kAux]) const {
+    const long long o = (long long)layer * ls1 + (long long)row * d + col;
+    load8(w1 + o, *reinterpret_cast<float(*)[8]>(&w[0]));
+    if constexpr (PAPER) load8(mom1 + o, *reinterpret_cast<float(*)[8]>(&w[8]));
   }
   __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
-                                         float (&v)[8], const float (&w)[8]) const {
-    float nw[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) nw[e] = w[e] - lr * v[e];
+                                         float (&v)[8], const float (&w)[kAux]) const {
     const long long o = (long long)layer * ls1 + (long long)row * d + col;
-    store8(w1 + o, nw);
-    if (w1_copy) store8(w1s + o, nw);
-    return 0.0f;
+    if constexpr (PAPER) {
+      const float b = beta[layer];
+      float m[8], nw[8], ss = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        m[e] = b * w[8 + e] + v[e];
+        nw[e] = w[e] - m[e];
+        ss += nw[e] * nw[e];
+      }
+      store8(mom1 + o, m);
+      store8(w1 + o, nw);
+      return ss;
+    } else {
+      float nw[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) nw[e] = w[e] - lr * v[e];
+      store8(w1 + o, nw);
+      if (w1_copy) store8(w1s + o, nw);
+      return 0.0f;
+    }
+  }
+  __device__ __forceinline__ void row_partial(int, int layer, int row, int cb, float ss) const {
+    if (PAPER) ss1[((long long)layer * h + row) * (d / 64) + cb] = ss;
   }
 };
 
@@ -872,6 +950,165 @@ __global__ void loss_finalize_kernel(const float* __restrict__ part, int per_lay
     __syncthreads();
   }
   if (threadIdx.x == 0) out[l] = red[0] * scale;
+}
+
+// ------------------------------------------------------------------------------------------
+// The paper's optimiser: per-token rates, momentum decay, row renormalisation
+
+__device__ __forceinline__ float softplusf_(float z) {
+  return fmaxf(z, 0.0f) + log1pf(__expf(-fabsf(z)));
+}
+
+// Dot products of a row of n_el elements with a float vector, summed by a whole wave in a fixed
+// order (lane-strided 8-element chunks, then a xor tree).
+template <typename E>
+__device__ __forceinline__ void wave_dot2(const E* __restrict__ row, const float* __restrict__ u,
+                                          const float* __restrict__ v, int n_el, int lane,
+                                          float* pu, float* pv) {
+  float su = 0.0f, sv = 0.0f;
+  for (int c = lane * 8; c < n_el; c += 64 * 8) {
+    float x[8];
+    if constexpr (sizeof(E) == 2) {
+      load8(reinterpret_cast<const bf16_t*>(row) + c, x);
+    } else {
+      const float4 a = *reinterpret_cast<const float4*>(row + c);
+      const float4 b = *reinterpret_cast<const float4*>(row + c + 4);
+      x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      su += x[e] * u[c + e];
+      sv += x[e] * v[c + e];
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    su += __shfl_xor(su, off, 64);
+    sv += __shfl_xor(sv, off, 64);
+  }
+  *pu = su;
+  *pv = sv;
+}
+
+// Per-token rates rate[l][j] = lr * softplus(u_l . x_j + b_u[l]) for j < n (0 for n <= j < Tp),
+// and per-block sums of v_l . x_j over the block's tokens (64 tokens per block, summed in token
+// order), from which decay_kernel forms the momentum decay.  Grid (Tp / 64, L), 256 threads.
+template <typename E>
+__global__ __launch_bounds__(256) void rate_kernel(const E* __restrict__ x, long long x_ls, int d,
+                                                   int n, const float* __restrict__ u,
+                                                   const float* __restrict__ bu,
+                                                   const float* __restrict__ v, float lr,
+                                                   float* __restrict__ rate, int Tp,
+                                                   float* __restrict__ vpart) {
+  const int l = blockIdx.y, j0 = blockIdx.x * 64, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __shared__ float wsum[4];
+  float acc = 0.0f;
+  for (int t = 0; t < 16; ++t) {
+    const int j = j0 + wave * 16 + t;
+    float pu = 0.0f, pv = 0.0f;
+    if (j < n)
+      wave_dot2(x + (long long)l * x_ls + (long long)j * d, u + (long long)l * d,
+                v + (long long)l * d, d, lane, &pu, &pv);
+    if (lane == 0) {
+      rate[(long long)l * Tp + j] = j < n ? lr * softplusf_(pu + bu[l]) : 0.0f;
+      acc += pv;
+    }
+  }
+  if (lane == 0) wsum[wave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    vpart[(long long)l * (Tp / 64) + blockIdx.x] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+}
+
+// beta[l] = sigmoid(mean_j (v_l . x_j) + b_v[l]) = sigmoid(v_l . xbar + b_v[l]).
+__global__ void decay_kernel(const float* __restrict__ vpart, int nblk, int n,
+                             const float* __restrict__ bv, float* __restrict__ beta, int L) {
+  const int l = blockIdx.x * blockDim.x + threadIdx.x;
+  if (l >= L) return;
+  float s = 0.0f;
+  for (int b = 0; b < nblk; ++b) s += vpart[(long long)l * nblk + b];
+  beta[l] = sigmoidf_(s / (float)n + bv[l]);
+}
+
+// L2 norm of every row of w [L][R][C] (fp32): one wave per row.  Grid (ceil(R / 4), L).
+__global__ __launch_bounds__(256) void row_norm_kernel(const float* __restrict__ w, int R, int C,
+                                                       float* __restrict__ norms) {
+  const int l = blockIdx.y, r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= R) return;
+  const float* row = w + ((long long)l * R + r) * C;
+  float s = 0.0f;
+  for (int c = lane * 4; c < C; c += 256) {
+    const float4 a = *reinterpret_cast<const float4*>(row + c);
+    s += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+  if (lane == 0) norms[(long long)l * R + r] = sqrtf(s);
+}
+
+// Row scales of the renormalisation: scale[l][r] = norm0[l][r] / ||row||, with ||row||^2 the
+// sum of the row's nseg segment sums (fixed order); a row of norm 0 keeps scale 1.
+__global__ void row_scale_kernel(const float* __restrict__ ss, int nseg, const float* __restrict__ norm0,
+                                 float* __restrict__ scale, long long rows) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows) return;
+  float s = 0.0f;
+  for (int b = 0; b < nseg; ++b) s += ss[i * nseg + b];
+  scale[i] = s > 0.0f ? norm0[i] * rsqrtf(s) : 1.0f;
+}
+
+// W1 renormalisation: w1[l][r][:] *= scale[l][r]; in bf16 mode also the rounded copy w1s.
+// Grid (ceil(h * d / 2048), L), 256 threads, 8 elements per thread.
+template <typename E>
+__global__ __launch_bounds__(256) void renorm_w1_kernel(float* __restrict__ w1, E* __restrict__ w1s,
+                                                        const float* __restrict__ scale, int h, int d) {
+  const int l = blockIdx.y;
+  const long long i = ((long long)blockIdx.x * 256 + threadIdx.x) * 8;
+  if (i >= (long long)h * d) return;
+  const long long o = (long long)l * h * d + i;
+  const float sc = scale[(long long)l * h + i / d];
+  float v[8];
+  load8(w1 + o, v);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] *= sc;
+  store8(w1 + o, v);
+  if (w1s) store8(w1s + o, v);
+}
+
+// W2 renormalisation: w2[l][r][c] *= scale[l][r]; writes the copies the next segment reads,
+// -W2 [D][h] and W2^T [h][D].  64 x 64 tiles through LDS; grid (h / 64, D / 64, L).
+template <typename E>
+__global__ __launch_bounds__(256) void renorm_w2_kernel(float* __restrict__ w2, E* __restrict__ w2n,
+                                                        E* __restrict__ w2t,
+                                                        const float* __restrict__ scale, int D, int h) {
+  __shared__ float tile[64][65];
+  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64, l = blockIdx.z;
+  const long long base = (long long)l * D * h;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {  // 64 rows x 8 chunks of 8 columns
+    const int idx = threadIdx.x + 256 * i, r = idx >> 3, cc = (idx & 7) * 8;
+    const long long o = base + (long long)(r0 + r) * h + c0 + cc;
+    const float sc = scale[(long long)l * D + r0 + r];
+    float v[8], nv[8];
+    load8(w2 + o, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      v[e] *= sc;
+      nv[e] = -v[e];
+      tile[r][cc + e] = v[e];
+    }
+    store8(w2 + o, v);
+    store8(w2n + o, nv);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {  // 64 columns x 8 chunks of 8 rows, transposed
+    const int idx = threadIdx.x + 256 * i, c = idx >> 3, rr = (idx & 7) * 8;
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = tile[rr + e][c];
+    store8(w2t + base + (long long)(c0 + c) * D + r0 + rr, v);
+  }
 }
 
 }  // namespace mone

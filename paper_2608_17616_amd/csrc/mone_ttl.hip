@@ -14,6 +14,9 @@
 //                  G   [L][Tp][D], G^T [L][D][Tp]
 //                  dZ^T [L][h][Tp], X^T [L][d][Tp]
 //                  loss partials [L][P], loss [L] fp32
+//                  paper optimiser only (fp32): rates [L][Tp], decay block sums [L][Tp/64],
+//                  decay [L], initial row norms [L][h] and [L][D], row-segment sums of
+//                  squares [L][h][d/64] and [L][D][h/64], row scales [L][h] and [L][D]
 // Tp = seg_len rounded up to 256; rows and columns beyond the segment's n tokens are zero, so
 // the token-contracting GEMMs run over n rounded up to their K step with no masking.
 //
@@ -24,6 +27,9 @@
 //   BWD  dA^T = W2^T G^T  and  G^T A     epilogues: dZ^T = dA^T * SiLU'(Z)^T; fp32 SGD
 //        (2 problems)                    read-modify-write of W2 + its copies
 //   UPD  dZ^T X                          epilogue: fp32 SGD read-modify-write of W1 + copy
+// With the paper's optimiser: RATE (per-token rates, momentum decay) after XT; FWD2 scales G by
+// the rates; the BWD and UPD epilogues update momentum and masters and write row sums of
+// squares; RENORM rescales the rows of W1 and W2 and writes their copies.
 // The W2 update shares the backward's launch: it needs only G and A, and writes the W2^T copy
 // the backward does not read, so CUs in its memory-bound epilogue overlap CUs computing the
 // backward's MFMAs.
@@ -66,7 +72,9 @@ long long round_up(long long v, long long a) { return (v + a - 1) / a * a; }
 struct Layout {
   int Tp;
   int loss_per_layer;
-  size_t w1c, w2c, w2t, a, at, dst, g, gt, dzt, xt, loss_part, loss_out, total;
+  size_t w1c, w2c, w2t, a, at, dst, g, gt, dzt, xt, loss_part, loss_out;
+  size_t rate, vpart, beta, norm1, norm2, ss1, ss2, scale1, scale2;  // paper optimiser
+  size_t total;
 };
 
 int check_config(const mone_ttl_config* c) {
@@ -79,6 +87,8 @@ int check_config(const mone_ttl_config* c) {
   if (c->loss != MONE_LOSS_MSE_SUM && c->loss != MONE_LOSS_MSE_MEAN)
     return fail(MONE_EINVAL, "loss %d is not a mone_loss", c->loss);
   if (!std::isfinite(c->lr)) return fail(MONE_EINVAL, "lr is not finite");
+  if (c->optimizer != MONE_OPT_SGD && c->optimizer != MONE_OPT_PAPER)
+    return fail(MONE_EINVAL, "optimizer %d is not a mone_optimizer", c->optimizer);
   if (c->d_model % 64 || c->d_hidden % 64 || c->d_kv % 64)
     return fail(MONE_EUNSUPPORTED, "d_model, d_hidden and d_kv must be multiples of 64");
   if (c->seg_len > 65536) return fail(MONE_EUNSUPPORTED, "seg_len above 65536");
@@ -121,6 +131,17 @@ Layout make_layout(const mone_ttl_config* c) {
   L.xt = take(nl * d * Tp * E);
   L.loss_part = take(nl * (size_t)L.loss_per_layer * 4);
   L.loss_out = take(nl * 4);
+  if (c->optimizer == MONE_OPT_PAPER) {
+    L.rate = take(nl * Tp * 4);
+    L.vpart = take(nl * (Tp / 64) * 4);
+    L.beta = take(nl * 4);
+    L.norm1 = take(nl * h * 4);
+    L.norm2 = take(nl * D * 4);
+    L.ss1 = take(nl * h * (d / 64) * 4);
+    L.ss2 = take(nl * D * (h / 64) * 4);
+    L.scale1 = take(nl * h * 4);
+    L.scale2 = take(nl * D * 4);
+  }
   L.total = off;
   return L;
 }
@@ -213,6 +234,7 @@ struct mone_ttl {
   float* w1;
   float* w2;
   unsigned char* ws;
+  mone_paper_optimizer opt;  // MONE_OPT_PAPER only
   int last_n;           // tokens of the last non-empty segment (0: none yet)
   int w2t_cur;          // which copy of the W2^T ping-pong pair holds the current weights
   int last_loss_count;  // loss partials per layer written by that segment
@@ -245,7 +267,7 @@ struct mone_ttl {
 
 namespace {
 
-template <typename E>
+template <typename E, bool PAPER>
 int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
   const mone_ttl_config& c = H->cfg;
   const Layout& Ly = H->lay;
@@ -275,6 +297,18 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
       reinterpret_cast<const E*>(x), lsx, d, n, d, Xt, ltx, Tp, nz);
   if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch XT");
   H->timing_end(MONE_STAGE_XT, s);
+
+  // RATE (paper optimiser): per-token rates and the momentum decay of this segment
+  if constexpr (PAPER) {
+    H->timing_begin(MONE_STAGE_RATE, s);
+    rate_kernel<E><<<dim3(Tp / 64, Lc), dim3(256), 0, s>>>(
+        reinterpret_cast<const E*>(x), lsx, d, n, H->opt.rate_w, H->opt.rate_b, H->opt.decay_w,
+        c.lr, H->at<float>(Ly.rate), Tp, H->at<float>(Ly.vpart));
+    decay_kernel<<<dim3((Lc + 63) / 64), dim3(64), 0, s>>>(H->at<float>(Ly.vpart), Tp / 64, n,
+                                                           H->opt.decay_b, H->at<float>(Ly.beta), Lc);
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch RATE");
+    H->timing_end(MONE_STAGE_RATE, s);
+  }
 
   // FWD1: Z = X W1^T  ->  A, A^T, SiLU'(Z)^T
   {
@@ -312,6 +346,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     epi.g = Gm; epi.gt = Gt; epi.loss_part = H->at<float>(Ly.loss_part); epi.ls = ltd;
     epi.D = D; epi.Tp = Tp; epi.n = n; epi.parts_per_layer = Ly.loss_per_layer;
     epi.c = c.loss == MONE_LOSS_MSE_SUM ? 2.0f / (float)n : 2.0f / ((float)n * (float)D);
+    epi.rate = PAPER ? H->at<float>(Ly.rate) : nullptr;
     int tiles = 0;
     H->timing_begin(MONE_STAGE_FWD2, s);
     if ((e = launch_gemm<E>(pick_tile(n, D, Lc), &sp, 1, Lc, epi, s, &tiles)) != hipSuccess)
@@ -340,10 +375,13 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     sp[1].n = h;
     sp[1].m_store = D;
     sp[1].n_store = h;
-    EpiBwdW2<E> epi;
+    EpiBwdW2<E, PAPER> epi;
     epi.dst = dSt; epi.dzt = dZt; epi.lst = lth; epi.Tp = Tp; epi.n = n;
     epi.w2 = H->w2; epi.w2n = H->at<E>(Ly.w2c); epi.w2t = w2t_new;
     epi.ls2 = (long long)D * h; epi.h = h; epi.D = D; epi.lr = c.lr;
+    epi.mom2 = PAPER ? H->opt.mom2 : nullptr;
+    epi.beta = PAPER ? H->at<float>(Ly.beta) : nullptr;
+    epi.ss2 = PAPER ? H->at<float>(Ly.ss2) : nullptr;
     H->timing_begin(MONE_STAGE_BWD, s);
     if ((e = launch_gemm<E>(pick_tile(h, n, Lc), sp, 2, Lc, epi, s)) != hipSuccess)
       return hip_fail(e, "launch BWD");
@@ -361,13 +399,34 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     sp.n = d;
     sp.m_store = h;
     sp.n_store = d;
-    EpiW1<E> epi;
+    EpiW1<E, PAPER> epi;
     epi.w1 = H->w1; epi.w1s = bf ? H->at<E>(Ly.w1c) : nullptr;
     epi.ls1 = (long long)h * d; epi.d = d; epi.w1_copy = bf ? 1 : 0; epi.lr = c.lr;
+    epi.mom1 = PAPER ? H->opt.mom1 : nullptr;
+    epi.beta = PAPER ? H->at<float>(Ly.beta) : nullptr;
+    epi.ss1 = PAPER ? H->at<float>(Ly.ss1) : nullptr;
+    epi.h = h;
     H->timing_begin(MONE_STAGE_UPD, s);
     if ((e = launch_gemm<E>(pick_tile(h, d, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
       return hip_fail(e, "launch UPD");
     H->timing_end(MONE_STAGE_UPD, s);
+  }
+  // RENORM (paper optimiser): rows of W1 and W2 back to their initial norms; the copies the
+  // next segment reads (W1 in bf16 mode, -W2, and W2^T into the other ping-pong copy)
+  if constexpr (PAPER) {
+    H->timing_begin(MONE_STAGE_RENORM, s);
+    const long long r1 = (long long)Lc * h, r2 = (long long)Lc * D;
+    row_scale_kernel<<<dim3((unsigned)((r1 + 255) / 256)), dim3(256), 0, s>>>(
+        H->at<float>(Ly.ss1), d / 64, H->at<float>(Ly.norm1), H->at<float>(Ly.scale1), r1);
+    row_scale_kernel<<<dim3((unsigned)((r2 + 255) / 256)), dim3(256), 0, s>>>(
+        H->at<float>(Ly.ss2), h / 64, H->at<float>(Ly.norm2), H->at<float>(Ly.scale2), r2);
+    const long long hd = (long long)h * d;
+    renorm_w1_kernel<E><<<dim3((unsigned)((hd + 2047) / 2048), Lc), dim3(256), 0, s>>>(
+        H->w1, bf ? H->at<E>(Ly.w1c) : nullptr, H->at<float>(Ly.scale1), h, d);
+    renorm_w2_kernel<E><<<dim3(h / 64, D / 64, Lc), dim3(256), 0, s>>>(
+        H->w2, H->at<E>(Ly.w2c), w2t_new, H->at<float>(Ly.scale2), D, h);
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch RENORM");
+    H->timing_end(MONE_STAGE_RENORM, s);
   }
   H->w2t_cur ^= 1;
   H->last_n = n;
@@ -430,17 +489,11 @@ int run_kv(mone_ttl* H, const void* xq, int q, void* kv, int kv_bf16, hipStream_
 
 }  // namespace
 
-extern "C" {
+namespace {
 
-size_t mone_ttl_workspace_bytes(const mone_ttl_config* cfg) {
-  g_err[0] = 0;
-  if (check_config(cfg) != MONE_OK) return 0;
-  return make_layout(cfg).total;
-}
-
-int mone_ttl_init(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, float* w1,
-                  float* w2, void* workspace, size_t workspace_bytes, void* stream) {
-  g_err[0] = 0;
+int create_handle(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, float* w1,
+                  float* w2, const mone_paper_optimizer* opt, void* workspace,
+                  size_t workspace_bytes, void* stream) {
   if (!out) return fail(MONE_EINVAL, "out is NULL");
   *out = nullptr;
   int rc = check_config(cfg);
@@ -466,6 +519,7 @@ int mone_ttl_init(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, f
   H->last_n = 0;
   H->last_loss_count = 0;
   H->w2t_cur = 0;
+  if (opt) H->opt = *opt;
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int Lc = cfg->n_layers, d = cfg->d_model, h = cfg->d_hidden, D = 2 * cfg->d_kv;
@@ -485,12 +539,52 @@ int mone_ttl_init(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, f
     transpose_kernel<float, float><<<dim3((h + 63) / 64, (D + 63) / 64, Lc), dim3(256), 0, s>>>(
         w2, (long long)D * h, h, D, h, H->at<float>(Ly.w2t), (long long)h * D, D, D);
   }
+  if (opt) {  // the renormalisation targets: row norms of the initial weights
+    row_norm_kernel<<<dim3((h + 3) / 4, Lc), dim3(256), 0, s>>>(w1, h, d, H->at<float>(Ly.norm1));
+    row_norm_kernel<<<dim3((D + 3) / 4, Lc), dim3(256), 0, s>>>(w2, D, h, H->at<float>(Ly.norm2));
+  }
   if ((e = hipGetLastError()) != hipSuccess) {
     delete H;
     return hip_fail(e, "building the weight copies");
   }
   *out = H;
   return MONE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t mone_ttl_workspace_bytes(const mone_ttl_config* cfg) {
+  g_err[0] = 0;
+  if (check_config(cfg) != MONE_OK) return 0;
+  return make_layout(cfg).total;
+}
+
+int mone_ttl_init(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, float* w1,
+                  float* w2, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  if (cfg && cfg->optimizer != MONE_OPT_SGD) {
+    if (out) *out = nullptr;
+    return fail(MONE_EINVAL, "optimizer %d needs mone_ttl_init_paper", cfg->optimizer);
+  }
+  return create_handle(out, cfg, wkv, w1, w2, nullptr, workspace, workspace_bytes, stream);
+}
+
+int mone_ttl_init_paper(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, float* w1,
+                        float* w2, const mone_paper_optimizer* opt, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  if (out) *out = nullptr;
+  if (cfg && cfg->optimizer != MONE_OPT_PAPER)
+    return fail(MONE_EINVAL, "mone_ttl_init_paper needs optimizer MONE_OPT_PAPER");
+  if (!opt) return fail(MONE_EINVAL, "opt is NULL");
+  if (!opt->rate_w || !opt->rate_b || !opt->decay_w || !opt->decay_b || !opt->mom1 || !opt->mom2)
+    return fail(MONE_EINVAL, "every pointer of the optimiser state must be non-NULL");
+  if (!aligned16(opt->rate_w) || !aligned16(opt->decay_w) || !aligned16(opt->mom1) ||
+      !aligned16(opt->mom2))
+    return fail(MONE_EINVAL, "rate_w, decay_w, mom1 and mom2 must be 16-byte aligned");
+  return create_handle(out, cfg, wkv, w1, w2, opt, workspace, workspace_bytes, stream);
 }
 
 int mone_ttl_segment(mone_ttl* H, const void* x, int32_t n_tokens, void* stream) {
@@ -502,8 +596,12 @@ int mone_ttl_segment(mone_ttl* H, const void* x, int32_t n_tokens, void* stream)
   if (!x) return fail(MONE_EINVAL, "x is NULL");
   if (!aligned16(x)) return fail(MONE_EINVAL, "x must be 16-byte aligned");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  return H->cfg.act_dtype == MONE_BF16 ? run_segment<bf16_t>(H, x, n_tokens, s)
-                                       : run_segment<float>(H, x, n_tokens, s);
+  const bool paper = H->cfg.optimizer == MONE_OPT_PAPER;
+  if (H->cfg.act_dtype == MONE_BF16)
+    return paper ? run_segment<bf16_t, true>(H, x, n_tokens, s)
+                 : run_segment<bf16_t, false>(H, x, n_tokens, s);
+  return paper ? run_segment<float, true>(H, x, n_tokens, s)
+               : run_segment<float, false>(H, x, n_tokens, s);
 }
 
 int mone_memory_kv(mone_ttl* H, const void* xq, int32_t q, void* kv, int32_t kv_dtype,

@@ -19,11 +19,13 @@ LIB_PATH = os.path.join(PKG, "libmone_ttl.so")
 MONE_OK, MONE_EINVAL, MONE_EUNSUPPORTED, MONE_EHIP, MONE_ESTATE = 0, -1, -2, -3, -4
 MONE_F32, MONE_BF16 = 0, 1
 MONE_LOSS_MSE_SUM, MONE_LOSS_MSE_MEAN = 0, 1
-STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2")
+MONE_OPT_SGD, MONE_OPT_PAPER = 0, 1
+STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2", "rate", "renorm")
 MONE_N_STAGES = len(STAGES)
 
 # every symbol include/mone_ttl.h declares
-EXPORTS = ("mone_ttl_workspace_bytes", "mone_ttl_init", "mone_ttl_segment", "mone_memory_kv",
+EXPORTS = ("mone_ttl_workspace_bytes", "mone_ttl_init", "mone_ttl_init_paper",
+           "mone_ttl_segment", "mone_memory_kv",
            "mone_ttl_loss", "mone_ttl_destroy", "mone_ttl_last_error",
            "mone_ttl_set_stage_timing", "mone_ttl_stage_times")
 
@@ -38,7 +40,14 @@ class mone_ttl_config(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
                 ("d_hidden", ctypes.c_int32), ("d_kv", ctypes.c_int32),
                 ("seg_len", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
-                ("loss", ctypes.c_int32), ("lr", ctypes.c_float)]
+                ("loss", ctypes.c_int32), ("lr", ctypes.c_float),
+                ("optimizer", ctypes.c_int32)]
+
+
+class mone_paper_optimizer(ctypes.Structure):
+    _fields_ = [("rate_w", ctypes.c_void_p), ("rate_b", ctypes.c_void_p),
+                ("decay_w", ctypes.c_void_p), ("decay_b", ctypes.c_void_p),
+                ("mom1", ctypes.c_void_p), ("mom2", ctypes.c_void_p)]
 
 
 _lib = None
@@ -56,6 +65,9 @@ def lib() -> ctypes.CDLL:
         L.mone_ttl_workspace_bytes.argtypes = [cfgp]
         L.mone_ttl_workspace_bytes.restype = ctypes.c_size_t
         L.mone_ttl_init.argtypes = [ctypes.POINTER(vp), cfgp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        L.mone_ttl_init_paper.argtypes = [ctypes.POINTER(vp), cfgp, vp, vp, vp,
+                                          ctypes.POINTER(mone_paper_optimizer), vp,
+                                          ctypes.c_size_t, vp]
         L.mone_ttl_segment.argtypes = [vp, vp, i32, vp]
         L.mone_memory_kv.argtypes = [vp, vp, i32, vp, i32, vp]
         L.mone_ttl_loss.argtypes = [vp, ctypes.POINTER(ctypes.c_float), vp]
@@ -94,17 +106,19 @@ def _stream(s) -> int | None:
     return s.cuda_stream
 
 
-def make_config(n_layers, d_model, d_hidden, d_kv, seg_len, act_dtype, loss, lr):
+def make_config(n_layers, d_model, d_hidden, d_kv, seg_len, act_dtype, loss, lr,
+                optimizer="sgd"):
     dt = {"f32": MONE_F32, "bf16": MONE_BF16}.get(act_dtype, act_dtype)
     ls = {"mse_sum": MONE_LOSS_MSE_SUM, "mse_mean": MONE_LOSS_MSE_MEAN}.get(loss, loss)
+    op = {"sgd": MONE_OPT_SGD, "paper": MONE_OPT_PAPER}.get(optimizer, optimizer)
     return mone_ttl_config(int(n_layers), int(d_model), int(d_hidden), int(d_kv), int(seg_len),
-                           int(dt), int(ls), float(lr))
+                           int(dt), int(ls), float(lr), int(op))
 
 
 def config_from(cfg) -> mone_ttl_config:
     """C config of a configs.MoneConfig."""
     return make_config(cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_kv, cfg.seg_len,
-                       cfg.act_dtype, cfg.loss, cfg.lr)
+                       cfg.act_dtype, cfg.loss, cfg.lr, cfg.optimizer)
 
 
 def mone_ttl_last_error() -> str:
@@ -124,6 +138,20 @@ def mone_ttl_init(cfg: mone_ttl_config, wkv, w1, w2, workspace, workspace_bytes:
     _check(lib().mone_ttl_init(ctypes.byref(h), ctypes.byref(cfg), _ptr(wkv), _ptr(w1), _ptr(w2),
                                _ptr(workspace), int(workspace_bytes), _stream(stream)))
     return h.value
+
+
+def mone_ttl_init_paper(cfg: mone_ttl_config, wkv, w1, w2, opt: mone_paper_optimizer,
+                        workspace, workspace_bytes: int, stream=None) -> int:
+    h = ctypes.c_void_p()
+    _check(lib().mone_ttl_init_paper(ctypes.byref(h), ctypes.byref(cfg), _ptr(wkv), _ptr(w1),
+                                     _ptr(w2), ctypes.byref(opt) if opt is not None else None,
+                                     _ptr(workspace), int(workspace_bytes), _stream(stream)))
+    return h.value
+
+
+def paper_optimizer(rate_w, rate_b, decay_w, decay_b, mom1, mom2) -> mone_paper_optimizer:
+    """C struct of the paper optimiser's buffers (device tensors or raw addresses)."""
+    return mone_paper_optimizer(*(_ptr(t) for t in (rate_w, rate_b, decay_w, decay_b, mom1, mom2)))
 
 
 def mone_ttl_segment(handle: int, x, n_tokens: int, stream=None) -> None:
@@ -163,14 +191,23 @@ class TtlSession:
     on the GPU; the workspace is allocated here with torch (the library allocates nothing).
     """
 
-    def __init__(self, cfg, wkv, w1, w2, stream=None):
+    def __init__(self, cfg, wkv, w1, w2, stream=None, opt=None):
+        """opt: for cfg.optimizer == "paper", the tensors (rate_w [L, d], rate_b [L],
+        decay_w [L, d], decay_b [L], mom1 [L, h, d], mom2 [L, D, h]), all fp32 on the GPU."""
         import torch
         self.cfg = cfg
         self.ccfg = config_from(cfg)
         self.wkv, self.w1, self.w2 = wkv, w1, w2
+        self.opt = opt
         self.ws_bytes = mone_ttl_workspace_bytes(self.ccfg)
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=w1.device)
-        self.handle = mone_ttl_init(self.ccfg, wkv, w1, w2, self.workspace, self.ws_bytes, stream)
+        if cfg.optimizer == "paper":
+            self.copt = paper_optimizer(*opt)
+            self.handle = mone_ttl_init_paper(self.ccfg, wkv, w1, w2, self.copt, self.workspace,
+                                              self.ws_bytes, stream)
+        else:
+            self.handle = mone_ttl_init(self.ccfg, wkv, w1, w2, self.workspace, self.ws_bytes,
+                                        stream)
 
     def segment(self, x, n_tokens=None, stream=None):
         n = x.shape[1] if n_tokens is None else n_tokens

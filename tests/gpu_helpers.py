@@ -65,3 +65,29 @@ class DeviceProblem:
             hx[l] = inputs.query_x(cfg, l, q, index)
             xq[l].copy_(torch.from_numpy(hx[l]))
         return xq, hx
+
+    def paper_state(self):
+        """Optimiser buffers of the paper's optimiser, as the tuple TtlSession takes: rate and
+        decay projections and biases (checked layers from the keyed generator, the others on
+        the device), and zero momentum.  Records the checked layers' host meta-parameters."""
+        torch = self.torch
+        cfg = self.cfg
+        L, d, h, D = cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out
+        dev = self.device
+        u = inputs.device_normal_(torch.empty(L, d, dtype=torch.float32, device=dev),
+                                  1 / np.sqrt(d), self.gen)
+        v = inputs.device_normal_(torch.empty(L, d, dtype=torch.float32, device=dev),
+                                  1 / np.sqrt(d), self.gen)
+        bu = torch.full((L,), inputs.B_U, dtype=torch.float32, device=dev)
+        bv = torch.full((L,), inputs.B_V, dtype=torch.float32, device=dev)
+        for l in self.checked:
+            mu, mbu, mv, mbv = inputs.layer_meta(cfg, l)
+            self.host[l]["meta"] = (mu.astype(np.float64), float(mbu), mv.astype(np.float64),
+                                    float(mbv))
+            u[l].copy_(torch.from_numpy(mu))
+            v[l].copy_(torch.from_numpy(mv))
+            bu[l] = float(mbu)
+            bv[l] = float(mbv)
+        m1 = torch.zeros(L, h, d, dtype=torch.float32, device=dev)
+        m2 = torch.zeros(L, D, h, dtype=torch.float32, device=dev)
+        return (u, bu, v, bv, m1, m2)

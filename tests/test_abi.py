@@ -105,3 +105,42 @@ def test_library_is_built_from_the_current_sources():
     lib_t = os.path.getmtime(mone.LIB_PATH)
     stale = [p for p in build.DEPENDS if os.path.getmtime(p) > lib_t]
     assert not stale, f"rebuild libmone_ttl.so (python -m paper_2608_17616_amd.build): {stale}"
+
+
+def test_paper_optimizer_workspace_adds_only_its_small_buffers():
+    c = _cfg()
+    p = _cfg(optimizer="paper")
+    n, n_p = mone.mone_ttl_workspace_bytes(c), mone.mone_ttl_workspace_bytes(p)
+    L, d, h, D, Tp = 2, 128, 192, 128, 256
+    extra = 4 * L * (Tp + Tp // 64 + 1 + h + D + h * (d // 64) + D * (h // 64) + h + D)
+    assert extra <= n_p - n <= extra + 9 * 256
+
+
+def test_optimizer_mismatch_and_paper_init_argument_checks():
+    L = mone.lib()
+    h = ctypes.c_void_p()
+    p = _cfg(optimizer="paper")
+    need = mone.mone_ttl_workspace_bytes(p)
+    # mone_ttl_init refuses the paper optimiser, mone_ttl_init_paper anything else
+    assert L.mone_ttl_init(ctypes.byref(h), ctypes.byref(p), 16, 16, 16, 256, need,
+                           None) == mone.MONE_EINVAL
+    assert "mone_ttl_init_paper" in mone.mone_ttl_last_error()
+    opt = mone.mone_paper_optimizer(16, 16, 16, 16, 16, 16)
+    s = _cfg()
+    assert L.mone_ttl_init_paper(ctypes.byref(h), ctypes.byref(s), 16, 16, 16, ctypes.byref(opt),
+                                 256, need, None) == mone.MONE_EINVAL
+    assert L.mone_ttl_init_paper(ctypes.byref(h), ctypes.byref(p), 16, 16, 16, None, 256, need,
+                                 None) == mone.MONE_EINVAL
+    bad = mone.mone_paper_optimizer(16, 16, 16, 16, None, 16)
+    assert L.mone_ttl_init_paper(ctypes.byref(h), ctypes.byref(p), 16, 16, 16, ctypes.byref(bad),
+                                 256, need, None) == mone.MONE_EINVAL
+    mis = mone.mone_paper_optimizer(16, 16, 24, 16, 16, 16)
+    assert L.mone_ttl_init_paper(ctypes.byref(h), ctypes.byref(p), 16, 16, 16, ctypes.byref(mis),
+                                 256, need, None) == mone.MONE_EINVAL
+    assert "aligned" in mone.mone_ttl_last_error()
+    assert L.mone_ttl_init_paper(ctypes.byref(h), ctypes.byref(p), 16, 16, 16, ctypes.byref(opt),
+                                 256, need - 1, None) == mone.MONE_EINVAL
+    assert "workspace" in mone.mone_ttl_last_error()
+    assert h.value is None
+    bad_opt = _cfg(optimizer=5)
+    assert mone.lib().mone_ttl_workspace_bytes(ctypes.byref(bad_opt)) == 0
