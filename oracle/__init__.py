@@ -7,3 +7,4 @@ from .paper_optimizer import (  # noqa: F401
     momentum_decay, paper_run, paper_step, renormalise, row_norms, softplus, token_rates,
     weighted_grad,
 )
+from .memory_attention import memory_attention  # noqa: F401
