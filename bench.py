@@ -38,6 +38,11 @@ def stage_work(cfg, q):
     """Algorithmic FLOPs and bytes of one launch of each stage (all layers)."""
     L, d, h, D, T = cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out, cfg.seg_len
     E = 2 if cfg.act_dtype == "bf16" else 4
+    hkv = max(1, cfg.d_kv // 128)
+    hq, dh = 4 * hkv, cfg.d_kv // hkv
+    # causal scores and weighted sums over q query keys and q memory keys per query row
+    attn = (L * hq * 2 * (q * (q + 1)) * 2 * dh,
+            L * q * ((hq + 2 * hkv) * dh * E + D * 4 + hq * dh * 4))
     if cfg.optimizer == "paper":
         # momentum read-modify-write in the update epilogues; the copies move to RENORM
         cp1 = E if cfg.act_dtype == "bf16" else 0
@@ -53,6 +58,7 @@ def stage_work(cfg, q):
             "renorm": (0, L * (h * d * (8 + cp1) + D * h * (8 + 2 * E))),
             "kv1": (L * 2 * q * d * h, L * (q * d + h * d + q * h) * E),
             "kv2": (L * 2 * q * h * D, L * (q * h + D * h) * E + L * q * D * 4),
+            "attn": attn,
         }
     return {
         "xt": (0, L * T * d * E * 2),
@@ -65,6 +71,7 @@ def stage_work(cfg, q):
         "upd": (L * 2 * T * h * d, L * ((h * T + d * T) * E + h * d * 8)),
         "kv1": (L * 2 * q * d * h, L * (q * d + h * d + q * h) * E),
         "kv2": (L * 2 * q * h * D, L * (q * h + D * h) * E + L * q * D * 4),
+        "attn": attn,
     }
 
 
@@ -168,6 +175,15 @@ def main():
         inputs.device_normal_(ctx[s], 1.0, gen)
     xq = inputs.device_normal_(torch.empty(L, Q, d, dtype=act, device=dev), 1.0, gen)
     kv = torch.empty(L, Q, D, dtype=torch.float32, device=dev)
+    # memory injection into attention after the read: grouped-query heads of width 128 (64 when
+    # d_kv is smaller), four query heads per key/value head
+    hkv = max(1, cfg.d_kv // 128)
+    hq = 4 * hkv
+    dh = cfg.d_kv // hkv
+    aq = inputs.device_normal_(torch.empty(L, Q, hq * dh, dtype=act, device=dev), 1.0, gen)
+    ak = inputs.device_normal_(torch.empty(L, Q, hkv * dh, dtype=act, device=dev), 1.0, gen)
+    av = inputs.device_normal_(torch.empty(L, Q, hkv * dh, dtype=act, device=dev), 1.0, gen)
+    aout = torch.empty(L, Q, hq * dh, dtype=torch.float32, device=dev)
     # CPU-baseline sample: layer 0 of the same workload, before any step changes the state
     n_cpu = 0 if args.no_cpu_baseline else min(S, 4)
     cpu_in = None
@@ -195,6 +211,8 @@ def main():
         for s in range(S):
             mone.mone_ttl_segment(H, ctx[s], T, sptr)
         mone.mone_memory_kv(H, xq, Q, kv, mone.MONE_F32, sptr)
+        mone.mone_memory_attention(H, aq, ak, av, kv, mone.MONE_F32, Q, hq, hkv, aout,
+                                   mone.MONE_F32, sptr)
 
     for _ in range(args.warmup):
         step()
@@ -207,7 +225,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    mone.mone_ttl_set_stage_timing(H, args.steps * (S * 7 + 2))
+    mone.mone_ttl_set_stage_timing(H, args.steps * (S * 7 + 3))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):

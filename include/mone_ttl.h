@@ -155,6 +155,27 @@ int mone_ttl_segment(mone_ttl* h, const void* x, int32_t n_tokens, void* stream)
 int mone_memory_kv(mone_ttl* h, const void* xq, int32_t q, void* kv, int32_t kv_dtype,
                    void* stream);
 
+/* Memory injection into attention at read time (Eq. attn, with the scaled softmax attention of
+ * Eq. std_attn).  The memory's K/V rows for the query tokens (mone_memory_kv's output) join the
+ * keys and values of those tokens in one softmax, per layer l and query head a:
+ *   out_i = softmax over j <= i of [ q_i.k_j / sqrt(dh) , q_i.km_j / sqrt(dh) ]
+ *           applied to [ v_j , vm_j ]
+ * where head a reads key/value head a / (n_heads / n_kv_heads) (grouped-query attention) and
+ * the memory row j = [km_j | vm_j] is the memory's output on query token j.  In this form the
+ * memory's output is already in key/value space (it is trained against [W_k x ; W_v x]), so it
+ * is used as it is.
+ *   qh      [L][q][n_heads*dh] act_dtype: the query tokens' attention queries
+ *   kh, vh  [L][q][n_kv_heads*dh] act_dtype: their keys and values; dh = d_kv / n_kv_heads,
+ *           at most 256
+ *   kv_mem  [L][q][D] of kv_dtype (MONE_F32 or MONE_BF16), K columns [0, d_kv), V [d_kv, D)
+ *   out     [L][q][n_heads*dh] of out_dtype
+ * n_heads must be a multiple of n_kv_heads and n_kv_heads must divide d_kv.  Uses nothing of
+ * the handle but its shape (L, d_kv, act_dtype); q = 0 is a no-op.  The work is O(q^2) per
+ * head (one query row per wavefront): it is meant for query batches, not for long prefills. */
+int mone_memory_attention(mone_ttl* h, const void* qh, const void* kh, const void* vh,
+                          const void* kv_mem, int32_t kv_dtype, int32_t q, int32_t n_heads,
+                          int32_t n_kv_heads, void* out, int32_t out_dtype, void* stream);
+
 /* The segment loss L_s of the last mone_ttl_segment call, per layer, evaluated at the weights
  * that step started from (the loss of Sec. 3.3 for that segment).  out_host: host float[L].
  * Synchronises `stream`.  MONE_ESTATE if no non-empty segment has been processed yet. */
@@ -179,7 +200,8 @@ const char* mone_ttl_last_error(void);
 #define MONE_STAGE_KV2 6   /* read: KV = A_q W2^T */
 #define MONE_STAGE_RATE 7  /* MONE_OPT_PAPER: per-token rates and the momentum decay */
 #define MONE_STAGE_RENORM 8 /* MONE_OPT_PAPER: row renormalisation of W1, W2 and their copies */
-#define MONE_N_STAGES 9
+#define MONE_STAGE_ATTN 9  /* mone_memory_attention */
+#define MONE_N_STAGES 10
 
 /* Enable (max_records > 0) or disable (0) per-stage timing: each subsequent stage launch is
  * bracketed by a pair of HIP events recorded on the call's stream, up to max_records pairs

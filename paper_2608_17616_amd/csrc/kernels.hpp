@@ -1111,4 +1111,72 @@ __global__ __launch_bounds__(256) void renorm_w2_kernel(float* __restrict__ w2, 
   }
 }
 
+// ------------------------------------------------------------------------------------------
+// Memory injection into attention (read time)
+
+// out[l][i][a] = softmax over j <= i of the scaled scores of q_i against the query-side keys
+// k_j and the memory keys km_j, applied to [v_j ; vm_j] (one softmax over both sets).  Head a
+// of Q reads key/value head a / (n_heads / n_kv_heads); head width dh <= 256.  One wave per
+// (layer, head, query row), online softmax over the keys in order (deterministic).
+// Grid (ceil(q / 4), n_heads, L), 256 threads.
+template <typename E, typename EK, typename EO>
+__global__ __launch_bounds__(256) void memory_attention_kernel(
+    const E* __restrict__ qh, const E* __restrict__ kh, const E* __restrict__ vh,
+    const EK* __restrict__ kvm, EO* __restrict__ out, int q, int n_heads, int n_kv_heads, int dh,
+    int d_kv, float scale) {
+  const int l = blockIdx.z, a = blockIdx.y;
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (i >= q) return;
+  const int g = a / (n_heads / n_kv_heads);
+  const long long qw = (long long)n_heads * dh, kw = (long long)n_kv_heads * dh;
+  const E* qi = qh + ((long long)l * q + i) * qw + (long long)a * dh;
+  const E* kl = kh + (long long)l * q * kw + (long long)g * dh;
+  const E* vl = vh + (long long)l * q * kw + (long long)g * dh;
+  const EK* ml = kvm + (long long)l * q * 2 * d_kv + (long long)g * dh;
+  float qv[4], acc[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int e = lane + 64 * t;
+    qv[t] = e < dh ? to_f32(qi[e]) * scale : 0.0f;
+    acc[t] = 0.0f;
+  }
+  float m = -INFINITY, lsum = 0.0f;
+  for (int j = 0; j <= i; ++j) {
+    const E* kj = kl + (long long)j * kw;
+    const EK* mj = ml + (long long)j * 2 * d_kv;
+    float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int e = lane + 64 * t;
+      if (e < dh) {
+        s1 += qv[t] * to_f32(kj[e]);
+        s2 += qv[t] * to_f32(mj[e]);
+      }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      s1 += __shfl_xor(s1, off, 64);
+      s2 += __shfl_xor(s2, off, 64);
+    }
+    const float mn = fmaxf(m, fmaxf(s1, s2));
+    const float c = __expf(m - mn), p1 = __expf(s1 - mn), p2 = __expf(s2 - mn);
+    lsum = lsum * c + p1 + p2;
+    const E* vj = vl + (long long)j * kw;
+    const EK* vmj = mj + d_kv;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int e = lane + 64 * t;
+      if (e < dh) acc[t] = acc[t] * c + p1 * to_f32(vj[e]) + p2 * to_f32(vmj[e]);
+    }
+    m = mn;
+  }
+  EO* oi = out + ((long long)l * q + i) * qw + (long long)a * dh;
+  const float inv = 1.0f / lsum;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int e = lane + 64 * t;
+    if (e < dh) oi[e] = from_f32<EO>(acc[t] * inv);
+  }
+}
+
 }  // namespace mone

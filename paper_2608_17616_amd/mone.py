@@ -20,12 +20,12 @@ MONE_OK, MONE_EINVAL, MONE_EUNSUPPORTED, MONE_EHIP, MONE_ESTATE = 0, -1, -2, -3,
 MONE_F32, MONE_BF16 = 0, 1
 MONE_LOSS_MSE_SUM, MONE_LOSS_MSE_MEAN = 0, 1
 MONE_OPT_SGD, MONE_OPT_PAPER = 0, 1
-STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2", "rate", "renorm")
+STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2", "rate", "renorm", "attn")
 MONE_N_STAGES = len(STAGES)
 
 # every symbol include/mone_ttl.h declares
 EXPORTS = ("mone_ttl_workspace_bytes", "mone_ttl_init", "mone_ttl_init_paper",
-           "mone_ttl_segment", "mone_memory_kv",
+           "mone_ttl_segment", "mone_memory_kv", "mone_memory_attention",
            "mone_ttl_loss", "mone_ttl_destroy", "mone_ttl_last_error",
            "mone_ttl_set_stage_timing", "mone_ttl_stage_times")
 
@@ -70,6 +70,7 @@ def lib() -> ctypes.CDLL:
                                           ctypes.c_size_t, vp]
         L.mone_ttl_segment.argtypes = [vp, vp, i32, vp]
         L.mone_memory_kv.argtypes = [vp, vp, i32, vp, i32, vp]
+        L.mone_memory_attention.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, i32, vp]
         L.mone_ttl_loss.argtypes = [vp, ctypes.POINTER(ctypes.c_float), vp]
         L.mone_ttl_destroy.argtypes = [vp]
         L.mone_ttl_last_error.argtypes = []
@@ -161,6 +162,13 @@ def mone_ttl_segment(handle: int, x, n_tokens: int, stream=None) -> None:
 def mone_memory_kv(handle: int, xq, q: int, kv, kv_dtype: int, stream=None) -> None:
     _check(lib().mone_memory_kv(handle, _ptr(xq), int(q), _ptr(kv), int(kv_dtype),
                                 _stream(stream)))
+
+
+def mone_memory_attention(handle: int, qh, kh, vh, kv_mem, kv_dtype: int, q: int, n_heads: int,
+                          n_kv_heads: int, out, out_dtype: int, stream=None) -> None:
+    _check(lib().mone_memory_attention(handle, _ptr(qh), _ptr(kh), _ptr(vh), _ptr(kv_mem),
+                                       int(kv_dtype), int(q), int(n_heads), int(n_kv_heads),
+                                       _ptr(out), int(out_dtype), _stream(stream)))
 
 
 def mone_ttl_loss(handle: int, n_layers: int, stream=None) -> list[float]:

@@ -144,3 +144,8 @@ def test_optimizer_mismatch_and_paper_init_argument_checks():
     assert h.value is None
     bad_opt = _cfg(optimizer=5)
     assert mone.lib().mone_ttl_workspace_bytes(ctypes.byref(bad_opt)) == 0
+
+
+def test_memory_attention_null_handle():
+    assert mone.lib().mone_memory_attention(None, 16, 16, 16, 16, 0, 4, 4, 2, 16, 0,
+                                            None) == mone.MONE_EINVAL
