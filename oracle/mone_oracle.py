@@ -18,7 +18,9 @@ of the paper's richer defaults; each choice is stated where it is made):
     and W2 = W_out^T is [D, h], both acting on column vectors as in the paper.
   * targets: t_j = [W_k x_j ; W_v x_j] (Eq. proj), frozen projections, raw (no SiLU/L2 norm/RoPE).
   * per-token loss l_j = ||M(x_j) - t_j||^2 summed over the D outputs ("mse_sum"), or divided by
-    D ("mse_mean"); segment loss L_s = (1/T) sum_j l_j (the segment-level average of Sec. 3.3).
+    D ("mse_mean"); or the paper's negative inner product l_j = -t_j . M(x_j) (Eq. mem_loss;
+    "nip"), whose value target in this form is the whole [K | V] row t_j; segment loss
+    L_s = (1/T) sum_j l_j (the segment-level average of Sec. 3.3).
   * update: W_s = W_{s-1} - lr * grad L_s(W_{s-1})  (Eq. update with mu_s = lr * gradient).
 
 Everything is float64 NumPy.  Matrix products use numpy's matmul as a library primitive; there is
@@ -33,7 +35,7 @@ from __future__ import annotations
 
 import numpy as np
 
-LOSSES = ("mse_sum", "mse_mean")
+LOSSES = ("mse_sum", "mse_mean", "nip")
 
 
 def sigmoid(z):
@@ -76,12 +78,32 @@ def targets(x, wkv):
 
 
 def _loss_scale(n: int, d_out: int, loss: str) -> float:
-    """Factor c with dL_s/dY = c * (Y - targets)."""
+    """Factor c with dL_s/dY = c * (Y - targets) (mse) or dL_s/dY = -c * targets (nip)."""
     if loss == "mse_sum":
         return 2.0 / n
     if loss == "mse_mean":
         return 2.0 / (n * d_out)
+    if loss == "nip":
+        return 1.0 / n
     raise ValueError(loss)
+
+
+def _per_token_loss(y, t, loss: str):
+    """l_j for the rows of Y and the targets."""
+    if loss == "nip":
+        return -np.sum(t * y, axis=1)
+    r = y - t
+    per_token = np.sum(r * r, axis=1)
+    if loss == "mse_mean":
+        per_token = per_token / r.shape[1]
+    elif loss != "mse_sum":
+        raise ValueError(loss)
+    return per_token
+
+
+def _output_grad(y, t, c: float, loss: str):
+    """dL_s/dY: c (Y - T) for the squared errors, -c T for the negative inner product."""
+    return -c * t if loss == "nip" else c * (y - t)
 
 
 def segment_loss(x, w1, w2, wkv, loss: str = "mse_sum") -> float:
@@ -91,20 +113,14 @@ def segment_loss(x, w1, w2, wkv, loss: str = "mse_sum") -> float:
     if n == 0:
         return 0.0
     _, _, y = memory_forward(x, w1, w2)
-    r = y - targets(x, wkv)
-    per_token = np.sum(r * r, axis=1)
-    if loss == "mse_mean":
-        per_token = per_token / r.shape[1]
-    elif loss != "mse_sum":
-        raise ValueError(loss)
-    return float(np.sum(per_token) / n)
+    return float(np.sum(_per_token_loss(y, targets(x, wkv), loss)) / n)
 
 
 def segment_grad(x, w1, w2, wkv, loss: str = "mse_sum"):
     """Gradient of L_s with respect to this layer's own fast weights only (Sec. 3.4).
 
     Returns (dL/dW1 [h, d], dL/dW2 [D, h], L_s).  Backpropagation through the two matrices:
-      G  = dL/dY = c (Y - targets)
+      G  = dL/dY = c (Y - targets)   (squared errors; -c targets for the negative inner product)
       dL/dW2 = G^T A
       dZ = (G W2) * SiLU'(Z)
       dL/dW1 = dZ^T x
@@ -115,16 +131,13 @@ def segment_grad(x, w1, w2, wkv, loss: str = "mse_sum"):
     if n == 0:
         return np.zeros_like(w1), np.zeros_like(w2), 0.0
     z, a, y = memory_forward(x, w1, w2)
-    r = y - targets(x, wkv)
+    t = targets(x, wkv)
     c = _loss_scale(n, w2.shape[0], loss)
-    g = c * r
+    g = _output_grad(y, t, c, loss)
     gw2 = g.T @ a
     dz = (g @ w2) * silu_grad(z)
     gw1 = dz.T @ x
-    per_token = np.sum(r * r, axis=1)
-    if loss == "mse_mean":
-        per_token = per_token / r.shape[1]
-    return gw1, gw2, float(np.sum(per_token) / n)
+    return gw1, gw2, float(np.sum(_per_token_loss(y, t, loss)) / n)
 
 
 def ttl_step(x, w1, w2, wkv, lr: float, loss: str = "mse_sum"):

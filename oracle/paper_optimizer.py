@@ -27,7 +27,8 @@ from __future__ import annotations
 
 import numpy as np
 
-from .mone_oracle import _loss_scale, memory_forward, sigmoid, silu_grad, targets
+from .mone_oracle import (_loss_scale, _output_grad, _per_token_loss, memory_forward, sigmoid,
+                          silu_grad, targets)
 
 
 def _f64(a):
@@ -72,16 +73,13 @@ def weighted_grad(x, w1, w2, wkv, eta, loss: str = "mse_sum"):
     x, w1, w2, wkv, eta = _f64(x), _f64(w1), _f64(w2), _f64(wkv), _f64(eta)
     n = x.shape[0]
     z, a, y = memory_forward(x, w1, w2)
-    r = y - targets(x, wkv)
+    t = targets(x, wkv)
     c = _loss_scale(n, w2.shape[0], loss)
-    g = c * eta[:, None] * r
+    g = eta[:, None] * _output_grad(y, t, c, loss)
     gw2 = g.T @ a
     dz = (g @ w2) * silu_grad(z)
     gw1 = dz.T @ x
-    per_token = np.sum(r * r, axis=1)
-    if loss == "mse_mean":
-        per_token = per_token / r.shape[1]
-    return gw1, gw2, float(np.sum(per_token) / n)
+    return gw1, gw2, float(np.sum(_per_token_loss(y, t, loss)) / n)
 
 
 def paper_step(x, w1, w2, m1, m2, wkv, meta, norms0, lr, loss: str = "mse_sum"):

@@ -85,7 +85,10 @@ def _brute_forward_and_loss(x, w1, w2, wkv, loss):
             a.append(z / (1.0 + math.exp(-z)))
         y = [sum(w2[o][i] * a[i] for i in range(h)) for o in range(D)]
         t = [sum(wkv[o][k] * x[j][k] for k in range(d)) for o in range(D)]
-        lj = sum((y[o] - t[o]) ** 2 for o in range(D))
+        if loss == "nip":  # negative inner product with the target row
+            lj = -sum(y[o] * t[o] for o in range(D))
+        else:
+            lj = sum((y[o] - t[o]) ** 2 for o in range(D))
         if loss == "mse_mean":
             lj /= D
         total += lj
@@ -165,8 +168,10 @@ def test_steps_match_torch_autograd(loss):
         tgt = F.linear(tx, twkv)
         if loss == "mse_sum":
             ls = F.mse_loss(y, tgt, reduction="sum") / T
-        else:
+        elif loss == "mse_mean":
             ls = F.mse_loss(y, tgt, reduction="mean")
+        else:
+            ls = -(y * tgt).sum() / T
         ls.backward()
         with torch.no_grad():
             tw1 = p1 - lr * p1.grad
@@ -302,3 +307,15 @@ def test_memory_kv_is_read_only():
     y2 = orc.memory_kv(x, w1, w2)
     assert np.array_equal(y1, y2)
     assert np.array_equal(w1, c1) and np.array_equal(w2, c2) and np.array_equal(x, cx)
+
+
+def test_negative_inner_product_gradient_of_w2_does_not_depend_on_w2():
+    # dL/dY = -T/n does not involve Y, so dL/dW2 = -(1/n) T^T A is the same at any W2, and
+    # dL/dW1 is linear in W2
+    rng = np.random.default_rng(12)
+    x, w1, w2, wkv = _rand_layer(rng, 5, 6, 4, 7)
+    g1a, g2a, _ = orc.segment_grad(x, w1, w2, wkv, "nip")
+    g1b, g2b, _ = orc.segment_grad(x, w1, 3.0 * w2 + 1.0, wkv, "nip")
+    np.testing.assert_allclose(g2a, g2b, rtol=1e-13, atol=1e-15)
+    g1c, _, _ = orc.segment_grad(x, w1, 3.0 * w2, wkv, "nip")
+    np.testing.assert_allclose(g1c, 3.0 * g1a, rtol=1e-12, atol=1e-15)
