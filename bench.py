@@ -60,10 +60,13 @@ def stage_work(cfg, q):
             "kv2": (L * 2 * q * h * D, L * (q * h + D * h) * E + L * q * D * 4),
             "attn": attn,
         }
+    fwd2 = (L * 2 * T * D * (h + d), L * (T * h + D * h + T * d + D * d + 2 * T * D) * E)
+    if cfg.loss == "nip":  # the targets alone
+        fwd2 = (L * 2 * T * D * d, L * (T * d + D * d + 2 * T * D) * E)
     return {
         "xt": (0, L * T * d * E * 2),
         "fwd1": (L * 2 * T * d * h, L * (T * d + h * d + T * h * 3) * E),
-        "fwd2": (L * 2 * T * D * (h + d), L * (T * h + D * h + T * d + D * d + 2 * T * D) * E),
+        "fwd2": fwd2,
         # backward (G W2 -> dZ^T) and the W2 update (G^T A) share one launch
         "bwd": (L * (2 * T * D * h + 2 * T * D * h),
                 L * ((T * D + h * D + 2 * T * h + D * T + h * T) * E + D * h * 8)),
@@ -140,6 +143,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this size (HBM counter calibration)")
+    ap.add_argument("--loss", default=None, choices=("mse_sum", "mse_mean", "nip"),
+                    help="override the configuration's loss (nip: the paper's negative inner "
+                         "product, whose step skips the output layer's forward)")
     ap.add_argument("--optimizer", default="sgd", choices=("sgd", "paper"),
                     help="the configuration's SGD, or the paper's optimiser (per-token rates, "
                          "momentum, row renormalisation)")
@@ -156,6 +162,8 @@ def main():
     from paper_2608_17616_amd import configs, inputs, mone
 
     cfg = configs.CONFIGS[args.config].with_(optimizer=args.optimizer)
+    if args.loss:
+        cfg = cfg.with_(loss=args.loss)
     L, d, h, D, T, Q = (cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out, cfg.seg_len,
                         cfg.n_query)
     S = args.segments or cfg.n_segments
@@ -277,9 +285,11 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": cfg.act_dtype, "data": "synthetic",
         "config": {"workload": f"{cfg.name}-class TTL: L={L} d={d} h={h} D={D} T={T} "
                                f"N={S * T} ({S} segments) + read Q={Q}"
-                               + (", paper optimiser" if cfg.optimizer == "paper" else ""),
+                               + (", paper optimiser" if cfg.optimizer == "paper" else "")
+                               + (f", loss {cfg.loss}" if args.loss else ""),
                    "n_layers": L, "d_model": d, "d_hidden": h, "d_out": D, "seg_len": T,
-                   "n_context": S * T, "n_query": Q, "lr": cfg.lr, "optimizer": cfg.optimizer},
+                   "n_context": S * T, "n_query": Q, "lr": cfg.lr, "optimizer": cfg.optimizer,
+                   "loss": cfg.loss},
         "mfma_pct": round(mfma_pct, 2),
         "flop_per_token": flop_tok,
         "roofline": roof,

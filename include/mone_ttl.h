@@ -12,7 +12,9 @@
  *            output [K | V] (the SwiGLU memory of Eq. swiglu without its gate branch);
  *   targets  t = [W_k x ; W_v x] from the frozen projections (Eq. proj), no preprocessing;
  *   loss     L_s = (1/n) sum_j ||M(x_j) - t_j||^2 over the n tokens of the segment
- *            (segment-level average of Sec. 3.3; MONE_LOSS_MSE_MEAN also divides by D);
+ *            (segment-level average of Sec. 3.3; MONE_LOSS_MSE_MEAN also divides by D), or
+ *            the paper's negative inner product L_s = -(1/n) sum_j t_j . M(x_j)
+ *            (Eq. mem_loss; MONE_LOSS_NIP);
  *   update   W <- W - lr * dL_s/dW for W1 and W2, both gradients taken at W_{s-1}
  *            (Eq. update with a plain SGD step),
  *            or, with MONE_OPT_PAPER (mone_ttl_init_paper), the paper's own optimiser: a
@@ -57,7 +59,10 @@ typedef enum { MONE_F32 = 0, MONE_BF16 = 1 } mone_dtype;
 
 typedef enum {
   MONE_LOSS_MSE_SUM = 0,  /* l_j = ||y_j - t_j||^2; dL_s/dY = (2/n)(Y - T) */
-  MONE_LOSS_MSE_MEAN = 1  /* l_j = ||y_j - t_j||^2 / D; dL_s/dY = (2/(n D))(Y - T) */
+  MONE_LOSS_MSE_MEAN = 1, /* l_j = ||y_j - t_j||^2 / D; dL_s/dY = (2/(n D))(Y - T) */
+  MONE_LOSS_NIP = 2       /* the paper's negative inner product (Eq. mem_loss) with the whole
+                             target row: l_j = -t_j . y_j; dL_s/dY = -(1/n) T, which does not
+                             involve Y, so the forward of the memory's output layer is skipped */
 } mone_loss;
 
 typedef enum {
@@ -178,7 +183,9 @@ int mone_memory_attention(mone_ttl* h, const void* qh, const void* kh, const voi
 
 /* The segment loss L_s of the last mone_ttl_segment call, per layer, evaluated at the weights
  * that step started from (the loss of Sec. 3.3 for that segment).  out_host: host float[L].
- * Synchronises `stream`.  MONE_ESTATE if no non-empty segment has been processed yet. */
+ * Synchronises `stream`.  MONE_ESTATE if no non-empty segment has been processed yet;
+ * MONE_EUNSUPPORTED for MONE_LOSS_NIP with MONE_OPT_PAPER (the step there only forms the
+ * rate-weighted gradient, not the plain loss). */
 int mone_ttl_loss(mone_ttl* h, float* out_host, void* stream);
 
 /* Destroy a handle (host memory only; the caller frees its device buffers afterwards, once

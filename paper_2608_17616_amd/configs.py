@@ -26,7 +26,7 @@ class MoneConfig:
     n_context: int     # N: context tokens; S = N / T segments
     act_dtype: str     # "f32" or "bf16": dtype of x, x_q, W_kv and stored intermediates
     lr: float          # learning rate (scales the per-token rates of the paper optimiser)
-    loss: str = "mse_sum"   # "mse_sum": c = 2/T ; "mse_mean": c = 2/(T*D)
+    loss: str = "mse_sum"   # "mse_sum": c = 2/T ; "mse_mean": c = 2/(T*D) ; "nip": -t.y
     n_query: int = 64  # Q: query tokens for the read step
     seed: int = 0
     optimizer: str = "sgd"  # "sgd" or "paper" (per-token rates, momentum, renormalisation)
@@ -42,11 +42,14 @@ class MoneConfig:
     def flops_per_token_layer(self, with_targets: bool = True) -> int:
         """Algorithmic FLOPs of one TTL step per context token per layer.
 
-        forward 1 (2dh) + forward 2 (2hD) + target projection (2dD) + backward to the hidden
-        layer (2hD) + the two weight gradients (2hD + 2dh).
+        forward 1 (2dh) + forward 2 (2hD; not with the negative inner product) + target
+        projection (2dD) + backward to the hidden layer (2hD) + the two weight gradients
+        (2hD + 2dh).
         """
         d, h, D = self.d_model, self.d_hidden, self.d_out
         f = 2 * (2 * d * h + 3 * h * D)
+        if self.loss == "nip":  # dL/dY = -T/n: the output layer's forward is not needed
+            f -= 2 * h * D
         if with_targets:
             f += 2 * d * D
         return f

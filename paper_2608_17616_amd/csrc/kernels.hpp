@@ -554,7 +554,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       }
     }
   }
-  G.epi.finish(layer, t, wave, lane, partial);
+  G.epi.finish(pi, layer, t, wave, lane, partial);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -578,7 +578,7 @@ struct EpiBase {
   __device__ __forceinline__ bool has_cols(int) const { return false; }
   __device__ __forceinline__ void pre8(int, int, int, int, int, int, float (&)[8]) const {}
   __device__ __forceinline__ void cols8(int, int, int, int, int, int, const float (&)[8]) const {}
-  __device__ __forceinline__ void finish(int, int, int, int, float) const {}
+  __device__ __forceinline__ void finish(int, int, int, int, int, float) const {}
 };
 
 // Forward 1: tile of Z = X W1^T [tokens][h].  Stores A = SiLU(Z) [Tp][h] (rows) and A^T,
@@ -634,7 +634,8 @@ struct EpiFwd1 : EpiBase {
 // Forward 2 and loss gradient: tile of -R [tokens][D], where the GEMM computes
 // A (-W2)^T + X W_kv^T (K-concatenated, from the negated copy of W2), so R = Y - targets.
 // Stores G = c R [Tp][D] (rows) and G^T [D][Tp] (columns); sums R^2 per wave into the loss
-// partials.
+// partials (sq).  For the negative inner product the GEMM is X W_kv^T alone (the targets T)
+// and the same formula gives G = -c T; its loss comes from the W2 update's epilogue instead.
 template <typename E>
 struct EpiFwd2 : EpiBase {
   static constexpr int kParts = 2;
@@ -644,6 +645,7 @@ struct EpiFwd2 : EpiBase {
   const float* rate;      // [L][Tp] per-token rates (the paper's optimiser), or null
   long long ls;           // Tp*D
   int D, Tp, n, parts_per_layer;
+  int sq;                 // write the sum-of-squares loss partials
   float c;
   __device__ __forceinline__ bool has_cols(int) const { return true; }
   __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
@@ -669,7 +671,9 @@ struct EpiFwd2 : EpiBase {
     }
     store8(gt + (long long)layer * ls + (long long)col * Tp + row, gv);
   }
-  __device__ __forceinline__ void finish(int layer, int tile, int wave, int lane, float s) const {
+  __device__ __forceinline__ void finish(int, int layer, int tile, int wave, int lane,
+                                        float s) const {
+    if (!sq) return;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
     if (lane == 0) loss_part[(long long)layer * parts_per_layer + tile * 4 + wave] = s;
@@ -685,6 +689,8 @@ struct EpiFwd2 : EpiBase {
 // With the paper's optimiser (PAPER), problem 1 updates the momentum, mu2 = beta mu2 + G^T A
 // (the rates are already in G), and the master, W2 - mu2, both fp32; it returns each row
 // chunk's sum of squares for the renormalisation, which writes the copies afterwards.
+// For the negative inner product (nip, SGD only) problem 1 also sums <W2_{s-1}, G^T A> per
+// wave into the loss partials: with G = -T/n that is -(1/n) sum_j t_j . y_j = L_s.
 template <typename E, bool PAPER = false>
 struct EpiBwdW2 : EpiBase {
   static constexpr bool kPre = true;
@@ -702,6 +708,9 @@ struct EpiBwdW2 : EpiBase {
   float* mom2;         // PAPER: [L][D][h] momentum
   const float* beta;   // PAPER: [L] momentum decay of this segment
   float* ss2;          // PAPER: [L][D][h/64] row-segment sums of squares
+  float* loss_part;    // nip: [L][parts_per_layer]
+  int parts_per_layer;
+  int nip;
   __device__ __forceinline__ bool has_cols(int pi) const { return !PAPER && pi == 1; }
   __device__ __forceinline__ void pre8(int pi, int layer, int row, int col, int, int,
                                        float (&x)[kAux]) const {
@@ -737,9 +746,10 @@ struct EpiBwdW2 : EpiBase {
       store8(w2 + o, nw);
       return ss;
     } else {
-      float nw[8], cp[8];
+      float nw[8], cp[8], ip = 0.0f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
+        ip += x[e] * v[e];
         nw[e] = x[e] - lr * v[e];
         cp[e] = -nw[e];
       }
@@ -747,8 +757,15 @@ struct EpiBwdW2 : EpiBase {
       store8(w2n + o, cp);
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = nw[e];
-      return 0.0f;
+      return nip ? ip : 0.0f;
     }
+  }
+  __device__ __forceinline__ void finish(int pi, int layer, int tile, int wave, int lane,
+                                        float s) const {
+    if (PAPER || !nip || pi != 1) return;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    if (lane == 0) loss_part[(long long)layer * parts_per_layer + tile * 4 + wave] = s;
   }
   __device__ __forceinline__ void row_partial(int pi, int layer, int row, int cb, float ss) const {
     if (PAPER && pi == 1) ss2[((long long)layer * D + row) * (h / 64) + cb] = ss;

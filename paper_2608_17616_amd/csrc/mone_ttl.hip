@@ -84,7 +84,7 @@ int check_config(const mone_ttl_config* c) {
                 c->n_layers, c->d_model, c->d_hidden, c->d_kv, c->seg_len);
   if (c->act_dtype != MONE_F32 && c->act_dtype != MONE_BF16)
     return fail(MONE_EINVAL, "act_dtype %d is not MONE_F32 or MONE_BF16", c->act_dtype);
-  if (c->loss != MONE_LOSS_MSE_SUM && c->loss != MONE_LOSS_MSE_MEAN)
+  if (c->loss != MONE_LOSS_MSE_SUM && c->loss != MONE_LOSS_MSE_MEAN && c->loss != MONE_LOSS_NIP)
     return fail(MONE_EINVAL, "loss %d is not a mone_loss", c->loss);
   if (!std::isfinite(c->lr)) return fail(MONE_EINVAL, "lr is not finite");
   if (c->optimizer != MONE_OPT_SGD && c->optimizer != MONE_OPT_PAPER)
@@ -111,7 +111,10 @@ Layout make_layout(const mone_ttl_config* c) {
   L.Tp = (int)round_up(c->seg_len, 256);
   const size_t Tp = L.Tp;
   // 4 wave partials per tile of the smallest tile shape (64 rows x 128 columns)
-  L.loss_per_layer = (int)(4 * (Tp / 64) * ((D + 127) / 128));
+  // 4 wave partials per tile of the smallest tile shapes: forward 2's tiles over [Tp][D] and,
+  // for the negative inner product, the W2 update's tiles over [D][h]
+  const size_t lp_fwd2 = (Tp / 64) * ((D + 127) / 128), lp_w2 = ((D + 63) / 64) * ((h + 63) / 64);
+  L.loss_per_layer = (int)(4 * (lp_fwd2 > lp_w2 ? lp_fwd2 : lp_w2));
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -184,7 +187,7 @@ Opnd opnd(const void* p, long long lstride, int ld, int rows) {
 
 template <typename E, int BM, int BN, int WAVES_M, class Epi>
 hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi,
-                        hipStream_t s, int* tiles_per_layer0) {
+                        hipStream_t s, int* tiles_per_layer) {
   GemmLaunch<Epi> G;
   std::memset(&G, 0, sizeof G);
   int begin = 0;
@@ -204,7 +207,8 @@ hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi
   }
   G.nprob = nspec;
   G.epi = epi;
-  if (tiles_per_layer0) *tiles_per_layer0 = G.prob[0].tiles_m * G.prob[0].tiles_n;
+  if (tiles_per_layer)  // tiles per layer of each problem
+    for (int i = 0; i < nspec; ++i) tiles_per_layer[i] = G.prob[i].tiles_m * G.prob[i].tiles_n;
   if (begin == 0) return hipSuccess;
   gemm_nt_kernel<E, BM, BN, WAVES_M, Epi><<<dim3(begin), dim3(256), 0, s>>>(G);
   return hipGetLastError();
@@ -212,16 +216,16 @@ hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi
 
 template <typename E, class Epi>
 hipError_t launch_gemm(TileShape t, const Spec* specs, int nspec, int layers, const Epi& epi,
-                       hipStream_t s, int* tiles_per_layer0 = nullptr) {
+                       hipStream_t s, int* tiles_per_layer = nullptr) {
   switch (t) {
     case TILE_256x256:
-      return launch_tiled<E, 256, 256, 2>(specs, nspec, layers, epi, s, tiles_per_layer0);
+      return launch_tiled<E, 256, 256, 2>(specs, nspec, layers, epi, s, tiles_per_layer);
     case TILE_128x128:
-      return launch_tiled<E, 128, 128, 2>(specs, nspec, layers, epi, s, tiles_per_layer0);
+      return launch_tiled<E, 128, 128, 2>(specs, nspec, layers, epi, s, tiles_per_layer);
     case TILE_256x64:
-      return launch_tiled<E, 256, 64, 4>(specs, nspec, layers, epi, s, tiles_per_layer0);
+      return launch_tiled<E, 256, 64, 4>(specs, nspec, layers, epi, s, tiles_per_layer);
     default:
-      return launch_tiled<E, 64, 256, 1>(specs, nspec, layers, epi, s, tiles_per_layer0);
+      return launch_tiled<E, 64, 256, 1>(specs, nspec, layers, epi, s, tiles_per_layer);
   }
 }
 
@@ -331,13 +335,21 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
   // FWD2: -R = A (-W2)^T + X W_kv^T  ->  G = c R, G^T, loss partials
   {
     Spec sp{};
-    sp.part[0].a = opnd(A, lth, h, n);
-    sp.part[0].b = opnd(w2neg, (long long)D * h, h, D);
-    sp.part[0].k_len = h;
-    sp.part[1].a = opnd(x, lsx, d, n);
-    sp.part[1].b = opnd(H->wkv, (long long)D * d, d, D);
-    sp.part[1].k_len = d;
-    sp.nparts = 2;
+    const bool nip = c.loss == MONE_LOSS_NIP;
+    if (nip) {  // dL/dY = -T/n needs only the targets T = X W_kv^T
+      sp.part[0].a = opnd(x, lsx, d, n);
+      sp.part[0].b = opnd(H->wkv, (long long)D * d, d, D);
+      sp.part[0].k_len = d;
+      sp.nparts = 1;
+    } else {
+      sp.part[0].a = opnd(A, lth, h, n);
+      sp.part[0].b = opnd(w2neg, (long long)D * h, h, D);
+      sp.part[0].k_len = h;
+      sp.part[1].a = opnd(x, lsx, d, n);
+      sp.part[1].b = opnd(H->wkv, (long long)D * d, d, D);
+      sp.part[1].k_len = d;
+      sp.nparts = 2;
+    }
     sp.m_extent = n;
     sp.n = D;
     sp.m_store = -1;
@@ -345,14 +357,17 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     EpiFwd2<E> epi;
     epi.g = Gm; epi.gt = Gt; epi.loss_part = H->at<float>(Ly.loss_part); epi.ls = ltd;
     epi.D = D; epi.Tp = Tp; epi.n = n; epi.parts_per_layer = Ly.loss_per_layer;
-    epi.c = c.loss == MONE_LOSS_MSE_SUM ? 2.0f / (float)n : 2.0f / ((float)n * (float)D);
+    epi.c = c.loss == MONE_LOSS_MSE_SUM   ? 2.0f / (float)n
+            : c.loss == MONE_LOSS_MSE_MEAN ? 2.0f / ((float)n * (float)D)
+                                           : 1.0f / (float)n;
+    epi.sq = nip ? 0 : 1;
     epi.rate = PAPER ? H->at<float>(Ly.rate) : nullptr;
     int tiles = 0;
     H->timing_begin(MONE_STAGE_FWD2, s);
     if ((e = launch_gemm<E>(pick_tile(n, D, Lc), &sp, 1, Lc, epi, s, &tiles)) != hipSuccess)
       return hip_fail(e, "launch FWD2");
     H->timing_end(MONE_STAGE_FWD2, s);
-    H->last_loss_count = 4 * tiles;
+    if (!nip) H->last_loss_count = 4 * tiles;
   }
   // BWD: dA^T = W2^T G^T (A operand W2^T [h][D], B operand G [tokens][D])  ->  dZ^T, and in
   // the same launch W2 -= lr G^T A (A operand G^T [D][tokens], B operand A^T [h][tokens])
@@ -382,10 +397,15 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     epi.mom2 = PAPER ? H->opt.mom2 : nullptr;
     epi.beta = PAPER ? H->at<float>(Ly.beta) : nullptr;
     epi.ss2 = PAPER ? H->at<float>(Ly.ss2) : nullptr;
+    epi.loss_part = H->at<float>(Ly.loss_part);
+    epi.parts_per_layer = Ly.loss_per_layer;
+    epi.nip = c.loss == MONE_LOSS_NIP ? 1 : 0;
+    int tiles[2] = {0, 0};
     H->timing_begin(MONE_STAGE_BWD, s);
-    if ((e = launch_gemm<E>(pick_tile(h, n, Lc), sp, 2, Lc, epi, s)) != hipSuccess)
+    if ((e = launch_gemm<E>(pick_tile(h, n, Lc), sp, 2, Lc, epi, s, tiles)) != hipSuccess)
       return hip_fail(e, "launch BWD");
     H->timing_end(MONE_STAGE_BWD, s);
+    if (c.loss == MONE_LOSS_NIP) H->last_loss_count = 4 * tiles[1];
   }
   // UPD: W1 -= lr dZ^T X (A operand dZ^T [h][tokens], B operand X^T [d][tokens])
   {
@@ -670,10 +690,17 @@ int mone_ttl_loss(mone_ttl* H, float* out_host, void* stream) {
   g_err[0] = 0;
   if (!H || !out_host) return fail(MONE_EINVAL, "handle and out_host must be non-NULL");
   if (H->last_n == 0) return fail(MONE_ESTATE, "no non-empty segment has been processed");
+  if (H->cfg.loss == MONE_LOSS_NIP && H->cfg.optimizer == MONE_OPT_PAPER)
+    return fail(MONE_EUNSUPPORTED, "the negative inner product's loss is not formed with the "
+                "paper optimiser (only its rate-weighted gradient is)");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const mone_ttl_config& c = H->cfg;
   const float n = (float)H->last_n;
-  const float scale = c.loss == MONE_LOSS_MSE_SUM ? 1.0f / n : 1.0f / (n * 2.0f * c.d_kv);
+  // sum-of-squares partials for the squared errors; for the negative inner product the
+  // partials already sum to L_s
+  const float scale = c.loss == MONE_LOSS_MSE_SUM    ? 1.0f / n
+                      : c.loss == MONE_LOSS_MSE_MEAN ? 1.0f / (n * 2.0f * c.d_kv)
+                                                     : 1.0f;
   float* dev_out = H->at<float>(H->lay.loss_out);
   loss_finalize_kernel<<<dim3(c.n_layers), dim3(256), 0, s>>>(
       H->at<float>(H->lay.loss_part), H->lay.loss_per_layer, H->last_loss_count, scale, dev_out);

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(PKG, "libmone_ttl.so")
 
 MONE_OK, MONE_EINVAL, MONE_EUNSUPPORTED, MONE_EHIP, MONE_ESTATE = 0, -1, -2, -3, -4
 MONE_F32, MONE_BF16 = 0, 1
-MONE_LOSS_MSE_SUM, MONE_LOSS_MSE_MEAN = 0, 1
+MONE_LOSS_MSE_SUM, MONE_LOSS_MSE_MEAN, MONE_LOSS_NIP = 0, 1, 2
 MONE_OPT_SGD, MONE_OPT_PAPER = 0, 1
 STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2", "rate", "renorm", "attn")
 MONE_N_STAGES = len(STAGES)
@@ -110,7 +110,8 @@ def _stream(s) -> int | None:
 def make_config(n_layers, d_model, d_hidden, d_kv, seg_len, act_dtype, loss, lr,
                 optimizer="sgd"):
     dt = {"f32": MONE_F32, "bf16": MONE_BF16}.get(act_dtype, act_dtype)
-    ls = {"mse_sum": MONE_LOSS_MSE_SUM, "mse_mean": MONE_LOSS_MSE_MEAN}.get(loss, loss)
+    ls = {"mse_sum": MONE_LOSS_MSE_SUM, "mse_mean": MONE_LOSS_MSE_MEAN,
+          "nip": MONE_LOSS_NIP}.get(loss, loss)
     op = {"sgd": MONE_OPT_SGD, "paper": MONE_OPT_PAPER}.get(optimizer, optimizer)
     return mone_ttl_config(int(n_layers), int(d_model), int(d_hidden), int(d_kv), int(seg_len),
                            int(dt), int(ls), float(lr), int(op))

@@ -28,6 +28,8 @@ CASES = {
     "mean_f32_paper": (MEAN_F32_P, [1], [200, 150, 200]),
     "1b_paper": (configs.ONE_B.with_(name="1b_paper", optimizer="paper", lr=2e-2), [0, 15],
                  [512] * 4),
+    "nip_f32_paper": (RAGGED_F32_P.with_(name="nip_f32_paper", loss="nip", lr=5e-3), [0, 2],
+                      [200, 137, 64, 1, 200, 77]),
     "8b_paper": (configs.EIGHT_B.with_(name="8b_paper", optimizer="paper", lr=2e-2), [0, 31],
                  [2048] * 2),
 }
@@ -57,7 +59,13 @@ def test_paper_optimizer_matches_oracle(torch_cuda, name):
     sess = mone.TtlSession(cfg, prob.wkv, prob.w1, prob.w2, opt=opt)
     for s, n in enumerate(ns):
         sess.segment(prob.segment(s, n), n)
-    gpu_loss = sess.loss()
+    if cfg.loss == "nip":  # only the rate-weighted gradient is formed, not the plain loss
+        with pytest.raises(mone.MoneError) as err:
+            sess.loss()
+        assert err.value.code == mone.MONE_EUNSUPPORTED
+        gpu_loss = None
+    else:
+        gpu_loss = sess.loss()
     xq, hxq = prob.query(q=cfg.n_query)
     kv = torch.empty(cfg.n_layers, cfg.n_query, cfg.d_out, dtype=torch.float32, device="cuda")
     sess.memory_kv(xq, kv)
@@ -77,8 +85,9 @@ def test_paper_optimizer_matches_oracle(torch_cuda, name):
             "dW2": rel_l2(w2[l] - hs["w2"], o2 - hs["w2"]),
             "mu1": rel_l2(m1[l], om1), "mu2": rel_l2(m2[l], om2),
             "KV": rel_l2(kvh[l], orc.memory_kv(hxq[l], o1, o2)),
-            "loss": abs(gpu_loss[l] - losses[-1]) / abs(losses[-1]),
         }
+        if gpu_loss is not None:
+            errs["loss"] = abs(gpu_loss[l] - losses[-1]) / abs(losses[-1])
         print(f"  layer {l}: " + " ".join(f"{k} {v:.2e}" for k, v in errs.items()) +
               f" (|dW1|/|W1| {np.linalg.norm(o1 - hs['w1']) / np.linalg.norm(hs['w1']):.1e})",
               flush=True)

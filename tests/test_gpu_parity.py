@@ -24,6 +24,8 @@ RAGGED_F32 = C("ragged_f32", n_layers=3, d_model=192, d_hidden=320, d_kv=64, seg
                n_context=1000, act_dtype="f32", lr=2e-2)
 RAGGED_BF16 = RAGGED_F32.with_(name="ragged_bf16", act_dtype="bf16")
 MEAN_F32 = RAGGED_F32.with_(name="mean_f32", loss="mse_mean", lr=1.0)
+NIP_F32 = RAGGED_F32.with_(name="nip_f32", loss="nip", lr=5e-3)
+NIP_BF16 = NIP_F32.with_(name="nip_bf16", act_dtype="bf16")
 
 # name -> (config, checked layers, tokens per segment)
 CASES = {
@@ -31,6 +33,9 @@ CASES = {
     "ragged_f32": (RAGGED_F32, [0, 2], [200, 137, 64, 1, 200, 77]),
     "ragged_bf16": (RAGGED_BF16, [0, 2], [200, 137, 64, 1, 200, 77]),
     "mean_f32": (MEAN_F32, [1], [200, 150, 200]),
+    "nip_f32": (NIP_F32, [0, 2], [200, 137, 64, 1, 200, 77]),
+    "nip_bf16": (NIP_BF16, [0, 2], [200, 137, 64, 1, 200, 77]),
+    "1b_nip": (configs.ONE_B.with_(name="1b_nip", loss="nip", lr=1e-3), [0, 15], [512] * 4),
     "1b": (configs.ONE_B, [0, 15], [512] * 4),
     "1b_f32": (configs.ONE_B.with_(name="1b_f32", act_dtype="f32"), [0, 15], [512] * 2),
     "3b": (configs.THREE_B, [0, 27], [1024] * 2),
