@@ -8,3 +8,4 @@ from .paper_optimizer import (  # noqa: F401
     weighted_grad,
 )
 from .memory_attention import memory_attention  # noqa: F401
+from . import swiglu_memory  # noqa: F401  (paper-form memory; names overlap the config form's)
