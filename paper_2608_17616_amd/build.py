@@ -11,9 +11,10 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SOURCES = [os.path.join(PKG, "csrc", "mone_ttl.hip")]
-DEPENDS = SOURCES + [os.path.join(PKG, "csrc", "kernels.hpp"),
-                     os.path.join(ROOT, "include", "mone_ttl.h")]
+SOURCES = [os.path.join(PKG, "csrc", "mone_ttl.hip"), os.path.join(PKG, "csrc", "mone_swiglu.hip")]
+DEPENDS = SOURCES + [os.path.join(PKG, "csrc", f) for f in
+                     ("kernels.hpp", "host_common.hpp", "swiglu_kernels.hpp")] + [
+                     os.path.join(ROOT, "include", f) for f in ("mone_ttl.h", "mone_swiglu.h")]
 LIB = os.path.join(PKG, "libmone_ttl.so")
 ARCH = "gfx950"
 

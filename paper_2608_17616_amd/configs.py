@@ -73,3 +73,54 @@ STRESS = MoneConfig("stress", n_layers=16, d_model=2048, d_hidden=2048, d_kv=512
                     n_context=524288, act_dtype="bf16", lr=1e-3)
 
 CONFIGS = {c.name: c for c in (TINY, ONE_B, THREE_B, EIGHT_B, STRESS)}
+
+
+@dataclass(frozen=True)
+class SwigluConfig:
+    """The paper-form memory (Eq. swiglu): per layer, H fast-weight heads of width d_h, each a
+    SwiGLU MLP of three d_h x d_h matrices, trained on preprocessed keys and values (affine,
+    SiLU, L2 norm and segment-local RoPE on keys; SiLU on values) with the negative inner
+    product loss (Eq. mem_loss).  The memory's width H d_h equals d_model."""
+    name: str
+    n_layers: int
+    d_model: int
+    n_heads: int
+    d_head: int
+    seg_len: int
+    n_context: int
+    act_dtype: str
+    lr: float
+    optimizer: str = "sgd"
+    rope_base: float = 10000.0
+    n_query: int = 64
+    seed: int = 0
+
+    @property
+    def n_segments(self) -> int:
+        return self.n_context // self.seg_len
+
+    def flops_per_token_layer(self) -> int:
+        """Algorithmic FLOPs of one step per context token per layer: the key and value
+        projections (2 d 2d), and per head the hidden activations' gradient (2 d_h^2), the
+        two branches' forward (4 d_h^2) and the three weight gradients (6 d_h^2).  The memory's
+        output is not formed: the loss gradient at the output does not depend on it."""
+        d, dh = self.d_model, self.d_head
+        return 4 * d * d + self.n_heads * 12 * dh * dh
+
+    def flops_per_token(self) -> int:
+        return self.n_layers * self.flops_per_token_layer()
+
+    def with_(self, **kw) -> "SwigluConfig":
+        return replace(self, **kw)
+
+
+# The paper's own memory on Qwen2.5-0.5B (App. A.2: 24 layers, d_model 896, H = 4 heads of
+# d_h = 224, 512-token segments, contexts up to 128K tokens).  The learning rate is synthetic
+# (the paper's rates are learned): with unit-norm keys, lr = 1 moves the weights by about 1e-3
+# of their norm per segment.
+SW_TINY = SwigluConfig("sw_tiny", n_layers=2, d_model=128, n_heads=2, d_head=64, seg_len=128,
+                       n_context=512, act_dtype="f32", lr=1.0)
+SW_PAPER = SwigluConfig("sw_qwen0.5b", n_layers=24, d_model=896, n_heads=4, d_head=224,
+                        seg_len=512, n_context=131072, act_dtype="bf16", lr=1.0)
+
+SW_CONFIGS = {c.name: c for c in (SW_TINY, SW_PAPER)}

@@ -1,0 +1,185 @@
+// Host helpers shared by the library's front ends (the configuration-form memory and the
+// paper-form SwiGLU memory): error reporting, the grouped-GEMM launch helpers and per-stage
+// timing with HIP events.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <vector>
+
+#include "../../include/mone_ttl.h"
+#include "kernels.hpp"
+
+// Message of the last failing call on this thread (defined once, in mone_ttl.hip).
+extern thread_local char g_err[512];
+
+namespace mone {
+namespace {
+
+inline int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+inline int hip_fail(hipError_t e, const char* what) {
+  return fail(MONE_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+inline long long round_up(long long v, long long a) { return (v + a - 1) / a * a; }
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+enum TileShape { TILE_256x256 = 0, TILE_128x128 = 1, TILE_64x256 = 2, TILE_256x64 = 3 };
+
+constexpr int kNumCUs = 256;
+
+// 64-row tiles for short row extents (short segments, query batches), 64-column tiles for
+// short column extents (the token axis of the transposed backward); 256 x 256 when the grouped
+// problem still has at least one such tile per CU; 128 x 128 otherwise.
+inline TileShape pick_tile(int m, int n, int layers) {
+  if (m <= 64) return TILE_64x256;
+  if (n <= 64) return TILE_256x64;
+  const long long big = (long long)((m + 255) / 256) * ((n + 255) / 256) * layers;
+  if (m >= 256 && n >= 256 && big >= kNumCUs) return TILE_256x256;
+  return TILE_128x128;
+}
+
+// Host description of one grouped problem before the tile shape fixes its tiling.
+struct Spec {
+  Part part[2];
+  int nparts;
+  int m_extent;   // rows that are computed (tiles cover them)
+  int n;          // columns that are computed
+  int m_store;    // rows stored by the epilogue; -1 = every computed tile row
+  int n_store;    // columns stored by the epilogue; -1 = every computed tile column
+};
+
+inline Opnd opnd(const void* p, long long lstride, int ld, int rows) {
+  Opnd o;
+  o.p = p;
+  o.lstride = lstride;
+  o.ld = ld;
+  o.rows = rows;
+  return o;
+}
+
+template <typename E, int BM, int BN, int WAVES_M, class Epi>
+hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi,
+                        hipStream_t s, int* tiles_per_layer) {
+  GemmLaunch<Epi> G;
+  std::memset(&G, 0, sizeof G);
+  int begin = 0;
+  for (int i = 0; i < nspec; ++i) {
+    // the kernel reads as many operand parts as the epilogue type declares
+    if (specs[i].nparts < 1 || specs[i].nparts > Epi::kParts) return hipErrorInvalidValue;
+    Problem& P = G.prob[i];
+    P.part[0] = specs[i].part[0];
+    P.part[1] = specs[i].part[1];
+    P.nparts = specs[i].nparts;
+    P.tiles_m = (specs[i].m_extent + BM - 1) / BM;
+    P.tiles_n = (specs[i].n + BN - 1) / BN;
+    P.M = specs[i].m_store >= 0 ? specs[i].m_store : P.tiles_m * BM;
+    P.N = specs[i].n_store >= 0 ? specs[i].n_store : P.tiles_n * BN;
+    P.tile_begin = begin;
+    begin += P.tiles_m * P.tiles_n * layers;
+  }
+  G.nprob = nspec;
+  G.epi = epi;
+  if (tiles_per_layer)  // tiles per layer of each problem
+    for (int i = 0; i < nspec; ++i) tiles_per_layer[i] = G.prob[i].tiles_m * G.prob[i].tiles_n;
+  if (begin == 0) return hipSuccess;
+  gemm_nt_kernel<E, BM, BN, WAVES_M, Epi><<<dim3(begin), dim3(256), 0, s>>>(G);
+  return hipGetLastError();
+}
+
+// Tiles per layer of a problem of m x n under tile shape t (what launch_gemm will use).
+inline int tiles_for(TileShape t, int m, int n) {
+  const int bm = t == TILE_256x256 || t == TILE_256x64 ? 256 : t == TILE_128x128 ? 128 : 64;
+  const int bn = t == TILE_256x256 || t == TILE_64x256 ? 256 : t == TILE_128x128 ? 128 : 64;
+  return ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
+}
+
+template <typename E, class Epi>
+hipError_t launch_gemm(TileShape t, const Spec* specs, int nspec, int layers, const Epi& epi,
+                       hipStream_t s, int* tiles_per_layer = nullptr) {
+  switch (t) {
+    case TILE_256x256:
+      return launch_tiled<E, 256, 256, 2>(specs, nspec, layers, epi, s, tiles_per_layer);
+    case TILE_128x128:
+      return launch_tiled<E, 128, 128, 2>(specs, nspec, layers, epi, s, tiles_per_layer);
+    case TILE_256x64:
+      return launch_tiled<E, 256, 64, 4>(specs, nspec, layers, epi, s, tiles_per_layer);
+    default:
+      return launch_tiled<E, 64, 256, 1>(specs, nspec, layers, epi, s, tiles_per_layer);
+  }
+}
+
+// Per-stage timing: each timed launch is bracketed by two HIP events on the launch's stream.
+struct StageTimer {
+  std::vector<hipEvent_t> ev;
+  std::vector<int> stage;
+  int cap = 0, used = 0;
+
+  void begin(hipStream_t s) {
+    if (used < cap) (void)hipEventRecord(ev[2 * used], s);
+  }
+  void end(int st, hipStream_t s) {
+    if (used < cap) {
+      (void)hipEventRecord(ev[2 * used + 1], s);
+      stage[used] = st;
+      ++used;
+    }
+  }
+  void destroy() {
+    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+    ev.clear();
+    stage.clear();
+    cap = used = 0;
+  }
+  int enable(int max_records) {
+    if (max_records < 0) return fail(MONE_EINVAL, "max_records is negative");
+    destroy();
+    if (max_records == 0) return MONE_OK;
+    ev.assign(2 * (size_t)max_records, nullptr);
+    stage.assign((size_t)max_records, 0);
+    for (size_t i = 0; i < ev.size(); ++i) {
+      hipError_t e = hipEventCreate(&ev[i]);
+      if (e != hipSuccess) {
+        ev.resize(i);
+        destroy();
+        return hip_fail(e, "hipEventCreate");
+      }
+    }
+    cap = max_records;
+    used = 0;
+    return MONE_OK;
+  }
+  int report(double* ms_sum, int32_t* count, int n_stages) {
+    for (int i = 0; i < n_stages; ++i) {
+      ms_sum[i] = 0.0;
+      count[i] = 0;
+    }
+    for (int i = 0; i < used; ++i) {
+      hipError_t e = hipEventSynchronize(ev[2 * i + 1]);
+      if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+      float ms = 0.0f;
+      if ((e = hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1])) != hipSuccess)
+        return hip_fail(e, "hipEventElapsedTime");
+      ms_sum[stage[i]] += ms;
+      count[stage[i]] += 1;
+    }
+    used = 0;
+    return MONE_OK;
+  }
+};
+
+}  // namespace
+}  // namespace mone

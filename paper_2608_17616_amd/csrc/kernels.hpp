@@ -23,13 +23,12 @@
 // k-values from the same fragment positions, so the k order inside an instruction does not
 // matter.  Accumulator register r of lane l holds C[8*(r/4) + 4*(l/32) + r%4][l % 32].
 //
-// Epilogue.  The fp32 tile is staged through LDS in passes of up to 128 rows, then processed in
-// chunks of 8 consecutive elements: a row pass (8 columns of one row: 16- or 32-byte vector
-// accesses, a wave covering whole rows) and, where a transposed copy is stored, a column pass
-// (8 rows of one column; 16 lanes cover 128 consecutive rows of a column, so each wave writes
-// contiguous 256-byte runs).  The staging layout pads rows by 8 floats and XOR-swizzles the
-// column by 4 * ((row / 8) % 16), which keeps the MFMA-layout writes, the row reads and the
-// column reads free of bank conflicts.
+// Epilogue.  Each wave stages its own accumulators through a private LDS region, one 64 x 64
+// sub-block at a time, then processes them in chunks of 8 consecutive elements: a row pass (8
+// columns of one row: 16- or 32-byte vector accesses) and, where a transposed copy is stored, a
+// column pass (8 rows of one column).  An epilogue may also take its rows in pairs (rows 2i and
+// 2i + 1 of a sub-block reach the same lane), for results that combine two interleaved output
+// rows.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -38,6 +37,8 @@
 #include <utility>
 
 namespace mone {
+// Internal linkage: every library source file that includes this header has its own copies.
+namespace {
 
 typedef uint16_t bf16_t;  // raw bf16 storage (same bits as torch.bfloat16)
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -479,14 +480,19 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   };
   float partial = 0.0f;
   constexpr int NAUX = Epi::kAux;
-  float aux[2][CPL][NAUX];
+  // Row chunks per lane: 8, or 4 pairs of rows (2i, 2i + 1) when the epilogue pairs rows.
+  constexpr int RS = Epi::kPairRows ? 2 : 1;
+  constexpr int NCH = CPL / RS;
+  static_assert(!Epi::kPairRows || (!Epi::kRowNorm && !Epi::kCols && !Epi::kWriteback),
+                "paired rows: row pass only");
+  float aux[2][NCH][NAUX];
   const int rl = lane >> 3, ql = lane & 7;      // row-chunk lane coordinates
-  auto issue_pre = [&](int sb, float (&ax)[CPL][NAUX]) {
+  auto issue_pre = [&](int sb, float (&ax)[NCH][NAUX]) {
     const int grow = m0 + wm * WM + (sb / NSN) * SB, gcol = n0 + wn * WN + (sb % NSN) * SB;
 #pragma unroll
-    for (int b = 0; b < CPL; ++b) {
-      const int row = grow + rl + 8 * b, col = gcol + 8 * ql;
-      if (row < P.M && col < P.N) G.epi.pre8(pi, layer, row, col, P.M, P.N, ax[b]);
+    for (int b = 0; b < NCH; ++b) {
+      const int row = grow + RS * (rl + 8 * b), col = gcol + 8 * ql;
+      if (row + RS - 1 < P.M && col < P.N) G.epi.pre8(pi, layer, row, col, P.M, P.N, ax[b]);
     }
   };
   if constexpr (Epi::kPre) issue_pre(0, aux[0]);
@@ -510,8 +516,8 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       if (sb + 1 < NSB) issue_pre(sb + 1, aux[(sb + 1) & 1]);
     }
 #pragma unroll
-    for (int b = 0; b < CPL; ++b) {
-      const int r = rl + 8 * b, c = 8 * ql;
+    for (int b = 0; b < NCH; ++b) {
+      const int r = RS * (rl + 8 * b), c = 8 * ql;
       float* s0 = stw + sidx(r, c);
       float* s1 = stw + sidx(r, c + 4);
       float v[8];
@@ -519,23 +525,32 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       const float4 x1 = *reinterpret_cast<const float4*>(s1);
       v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
       v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
-      const bool ok = grow + r < P.M && gcol + c < P.N;
+      const bool ok = grow + r + RS - 1 < P.M && gcol + c < P.N;
       float val = 0.0f;
-      if (ok) {
+      if constexpr (Epi::kPairRows) {
+        // the partner row r + 1 (r is even: sub-blocks start at even rows)
+        const float4 y0 = *reinterpret_cast<const float4*>(stw + sidx(r + 1, c));
+        const float4 y1 = *reinterpret_cast<const float4*>(stw + sidx(r + 1, c + 4));
+        const float w[8] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
+        if (ok) val = G.epi.rows8p(pi, layer, grow + r, gcol + c, P.M, P.N, v, w, aux[sb & 1][b]);
+        partial += val;
+      } else if (ok) {
         val = G.epi.rows8(pi, layer, grow + r, gcol + c, P.M, P.N, v, aux[sb & 1][b]);
         if constexpr (Epi::kWriteback) {
           *reinterpret_cast<float4*>(s0) = make_float4(v[0], v[1], v[2], v[3]);
           *reinterpret_cast<float4*>(s1) = make_float4(v[4], v[5], v[6], v[7]);
         }
       }
-      if constexpr (Epi::kRowNorm) {
-        // the 8 lanes of a row segment are lanes 8*rl .. 8*rl+7: a fixed-order tree sum
-        val += __shfl_xor(val, 1, 64);
-        val += __shfl_xor(val, 2, 64);
-        val += __shfl_xor(val, 4, 64);
-        if (ok && ql == 0) G.epi.row_partial(pi, layer, grow + r, gcol / SB, val);
-      } else {
-        partial += val;
+      if constexpr (!Epi::kPairRows) {
+        if constexpr (Epi::kRowNorm) {
+          // the 8 lanes of a row segment are lanes 8*rl .. 8*rl+7: a fixed-order tree sum
+          val += __shfl_xor(val, 1, 64);
+          val += __shfl_xor(val, 2, 64);
+          val += __shfl_xor(val, 4, 64);
+          if (ok && ql == 0) G.epi.row_partial(pi, layer, grow + r, gcol / SB, val);
+        } else {
+          partial += val;
+        }
       }
     }
     if constexpr (Epi::kCols) {
@@ -572,6 +587,8 @@ struct EpiBase {
   static constexpr int kAux = 8;       // floats pre8 reads per row chunk
   static constexpr bool kRowNorm = false;  // rows8 returns the chunk's sum of squares, which
                                            // is reduced per 64-column row segment
+  static constexpr bool kPairRows = false; // rows8p(v = row r, w = row r + 1) for even r
+                                           // replaces rows8 (row pass only)
   __device__ __forceinline__ void row_partial(int, int, int, int, float) const {}
   static constexpr bool kCols = false;
   static constexpr bool kWriteback = false;
@@ -1196,4 +1213,5 @@ __global__ __launch_bounds__(256) void memory_attention_kernel(
   }
 }
 
+}  // namespace
 }  // namespace mone

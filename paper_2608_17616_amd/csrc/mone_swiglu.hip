@@ -1,0 +1,442 @@
+// Host side of the paper-form memory (SwiGLU per fast-weight head): argument validation,
+// workspace layout and the per-stage launches of a segment step.  The C ABI is declared in
+// include/mone_swiglu.h.
+//
+// Data layout in HBM (row-major; B = L * H head operands, b = l * H + e; Tp = seg_len rounded
+// up to 256; d_hp = d_h rounded up to 64, padding columns zero):
+//   caller state   W_in, W_gate, W_out [L][H][d_h][d_h] fp32; P [L][2d][d] act; s, b [L][d]
+//   workspace      raw  [L][Tp][2d] fp32   raw key and value projections
+//                  K    [B][Tp][d_hp]      preprocessed keys (B operand of FWD)
+//                  K^T  [B][d_h][Tp]       (B operand of the W_in / W_gate gradients)
+//                  dY0  [B][Tp][d_hp]      -v / n (B operand of DA)
+//                  dY^T [B][d_h][Tp]       -eta v / n (B operand of the W_out gradient)
+//                  dA0^T [B][d_h][Tp]      DA's output, read by FWD's epilogue
+//                  A^T  [B][d_h][Tp]       (A operand of the W_out gradient)
+//                  [dZ|dG]^T [B][2 d_h][Tp] interleaved rows (A operand of the W_in/W_gate
+//                                          gradients)
+//                  W_ig [B][2 d_h][d_hp], W_out copy [B][d_h][d_hp]  MFMA copies
+//                  RoPE table [Tp][d_h/2] (cos, sin); loss partials; loss [L]
+//                  paper optimiser (fp32): rates [L][Tp], decay block sums, decay [L],
+//                  initial row norms, row-segment sums of squares
+// A segment step, each stage one launch grouped over all layers (PROJ) or all B heads:
+//   [RATE]  per-token rates and momentum decay (paper optimiser)
+//   PROJ    [raw K | raw V] = X [P_k ; P_v]^T
+//   PREP    keys: affine, SiLU, L2, RoPE -> K, K^T; values: SiLU -> dY0, dY^T
+//   DA      dA0^T = W_out dY0^T
+//   FWD     [Z | G]^T = W_ig K^T     epilogue: A^T, [dZ | dG]^T, loss partials
+//   UPD     A^T dY and [dZ | dG]^T K  (2 problems)  epilogue: update of the masters + copies
+//   [RENORM] rows back to their initial norms, copies (paper optimiser)
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <new>
+
+#include "../../include/mone_swiglu.h"
+#include "host_common.hpp"
+#include "swiglu_kernels.hpp"
+
+using namespace mone;
+
+namespace {
+
+struct SwLayout {
+  int Tp, dhp, nseg, parts_max;
+  size_t raw, kh, kt, dy, dyt, dat, at, dzgt, wig, woc, rope, loss_part, loss_out;
+  size_t rate, vpart, beta, n_ig, n_out, ss_ig, ss_out;  // paper optimiser
+  size_t total;
+};
+
+int check_sw_config(const mone_swiglu_config* c) {
+  if (!c) return fail(MONE_EINVAL, "config is NULL");
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_heads < 1 || c->d_head < 1 || c->seg_len < 1)
+    return fail(MONE_EINVAL, "config sizes must be >= 1 (L=%d d=%d H=%d d_h=%d T=%d)",
+                c->n_layers, c->d_model, c->n_heads, c->d_head, c->seg_len);
+  if ((long long)c->n_heads * c->d_head != c->d_model)
+    return fail(MONE_EINVAL, "d_model %d is not n_heads %d x d_head %d", c->d_model, c->n_heads,
+                c->d_head);
+  if (c->d_head % 2) return fail(MONE_EINVAL, "d_head %d is odd (RoPE pairs channels)", c->d_head);
+  if (c->act_dtype != MONE_F32 && c->act_dtype != MONE_BF16)
+    return fail(MONE_EINVAL, "act_dtype %d is not MONE_F32 or MONE_BF16", c->act_dtype);
+  if (c->optimizer != MONE_OPT_SGD && c->optimizer != MONE_OPT_PAPER)
+    return fail(MONE_EINVAL, "optimizer %d is not a mone_optimizer", c->optimizer);
+  if (!std::isfinite(c->lr)) return fail(MONE_EINVAL, "lr is not finite");
+  if (!std::isfinite(c->rope_base) || !(c->rope_base > 0.0f))
+    return fail(MONE_EINVAL, "rope_base must be finite and positive");
+  if (c->d_model % 64) return fail(MONE_EUNSUPPORTED, "d_model must be a multiple of 64");
+  if (c->d_head % 8 || c->d_head > 256)
+    return fail(MONE_EUNSUPPORTED, "d_head must be a multiple of 8 in [8, 256]");
+  if (c->seg_len > 65536) return fail(MONE_EUNSUPPORTED, "seg_len above 65536");
+  const long long Tp = round_up(c->seg_len, 256), d = c->d_model;
+  const long long E = c->act_dtype == MONE_BF16 ? 2 : 4;
+  // per-layer and per-head operand slices are addressed with 32-bit byte offsets
+  if (Tp * 2 * d * 4 >= (1LL << 31) || 2 * d * d * E >= (1LL << 31))
+    return fail(MONE_EUNSUPPORTED, "a per-layer matrix exceeds 2^31 bytes");
+  return MONE_OK;
+}
+
+SwLayout make_sw_layout(const mone_swiglu_config* c) {
+  SwLayout L{};
+  const size_t E = c->act_dtype == MONE_BF16 ? 2 : 4;
+  const size_t nl = (size_t)c->n_layers, d = c->d_model, dh = c->d_head;
+  const size_t B = nl * (size_t)c->n_heads;
+  L.Tp = (int)round_up(c->seg_len, 256);
+  L.dhp = (int)round_up(c->d_head, 64);
+  L.nseg = (c->d_head + 63) / 64;
+  // 4 wave partials per FWD tile; no tile shape is smaller than 64 in either direction
+  L.parts_max = 4 * ((2 * c->d_head + 63) / 64) * (L.Tp / 64);
+  const size_t Tp = L.Tp, dhp = L.dhp;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, kAlign);
+    return o;
+  };
+  L.raw = take(nl * Tp * 2 * d * 4);
+  L.kh = take(B * Tp * dhp * E);
+  L.kt = take(B * dh * Tp * E);
+  L.dy = take(B * Tp * dhp * E);
+  L.dyt = take(B * dh * Tp * E);
+  L.dat = take(B * dh * Tp * E);
+  L.at = take(B * dh * Tp * E);
+  L.dzgt = take(B * 2 * dh * Tp * E);
+  L.wig = take(B * 2 * dh * dhp * E);
+  L.woc = take(B * dh * dhp * E);
+  L.rope = take(Tp * (dh / 2) * 8);
+  L.loss_part = take(B * (size_t)L.parts_max * 4);
+  L.loss_out = take(nl * 4);
+  if (c->optimizer == MONE_OPT_PAPER) {
+    L.rate = take(nl * Tp * 4);
+    L.vpart = take(nl * (Tp / 64) * 4);
+    L.beta = take(nl * 4);
+    L.n_ig = take(B * 2 * dh * 4);
+    L.n_out = take(B * dh * 4);
+    L.ss_ig = take(B * 2 * dh * (size_t)L.nseg * 4);
+    L.ss_out = take(B * dh * (size_t)L.nseg * 4);
+  }
+  L.total = off;
+  return L;
+}
+
+// Tile shape of the per-head GEMMs: their K extent (d_hp or a segment's tokens) is short, and
+// 128 x 128 tiles give several workgroups per CU even for a few layers.
+constexpr TileShape kHeadTile = TILE_128x128;
+
+template <typename E, class Epi>
+hipError_t launch_head_gemm(const Spec* specs, int nspec, int heads, const Epi& epi,
+                            hipStream_t s) {
+  return launch_tiled<E, 128, 128, 2>(specs, nspec, heads, epi, s, nullptr);
+}
+
+}  // namespace
+
+struct mone_swiglu {
+  mone_swiglu_config cfg;
+  SwLayout lay;
+  mone_swiglu_frozen fz;
+  mone_swiglu_weights w;
+  mone_swiglu_optimizer opt;  // MONE_OPT_PAPER only
+  unsigned char* ws;
+  int last_n;      // tokens of the last non-empty segment (0: none yet)
+  int last_parts;  // loss partials per head written by that segment
+  StageTimer timer;
+
+  template <typename T>
+  T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+};
+
+namespace {
+
+template <typename E, bool PAPER>
+int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
+  const mone_swiglu_config& c = H->cfg;
+  const SwLayout& Ly = H->lay;
+  const int L = c.n_layers, d = c.d_model, NH = c.n_heads, dh = c.d_head, B = L * NH;
+  const int Tp = Ly.Tp, dhp = Ly.dhp;
+  constexpr int BK = 8 * (16 / (int)sizeof(E));
+  const int nz = (int)round_up(n, 64);   // token extent PREP writes
+  const int kt = (int)round_up(n, BK);   // token extent of the UPD contractions
+  E* kh = H->at<E>(Ly.kh);
+  E* ktr = H->at<E>(Ly.kt);
+  E* dy = H->at<E>(Ly.dy);
+  E* dyt = H->at<E>(Ly.dyt);
+  E* dat = H->at<E>(Ly.dat);
+  E* At = H->at<E>(Ly.at);
+  E* dzgt = H->at<E>(Ly.dzgt);
+  E* wig = H->at<E>(Ly.wig);
+  E* woc = H->at<E>(Ly.woc);
+  float* rate = PAPER ? H->at<float>(Ly.rate) : nullptr;
+  const long long lsx = (long long)n * d, lhT = (long long)dh * Tp, lhP = (long long)Tp * dhp;
+  hipError_t e;
+
+  if constexpr (PAPER) {
+    H->timer.begin(s);
+    rate_kernel<E><<<dim3(Tp / 64, L), dim3(256), 0, s>>>(
+        reinterpret_cast<const E*>(x), lsx, d, n, H->opt.rate_w, H->opt.rate_b, H->opt.decay_w,
+        c.lr, rate, Tp, H->at<float>(Ly.vpart));
+    decay_kernel<<<dim3((L + 63) / 64), dim3(64), 0, s>>>(H->at<float>(Ly.vpart), Tp / 64, n,
+                                                          H->opt.decay_b, H->at<float>(Ly.beta), L);
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch RATE");
+    H->timer.end(MONE_SW_STAGE_RATE, s);
+  }
+  // PROJ: [raw K | raw V] = X [P_k ; P_v]^T, fp32
+  {
+    Spec sp{};
+    sp.part[0].a = opnd(x, lsx, d, n);
+    sp.part[0].b = opnd(H->fz.proj, 2LL * d * d, d, 2 * d);
+    sp.part[0].k_len = d;
+    sp.nparts = 1;
+    sp.m_extent = n;
+    sp.n = 2 * d;
+    sp.m_store = -1;
+    sp.n_store = 2 * d;
+    EpiSwProj epi;
+    epi.raw = H->at<float>(Ly.raw); epi.ls = (long long)Tp * 2 * d; epi.ld = 2 * d;
+    H->timer.begin(s);
+    if ((e = launch_gemm<E>(pick_tile(n, 2 * d, L), &sp, 1, L, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch PROJ");
+    H->timer.end(MONE_SW_STAGE_PROJ, s);
+  }
+  // PREP
+  {
+    const int TB = (64 * (dh + 1) + 64) * 4 <= 65536 ? 64 : 32;
+    const size_t shmem = (size_t)(TB * (dh + 1) + TB) * 4;
+    H->timer.begin(s);
+    sw_prep_kernel<E><<<dim3(nz / TB, NH, L), dim3(256), shmem, s>>>(
+        H->at<float>(Ly.raw), (long long)Tp * 2 * d, d, n, NH, dh, dhp, Tp, TB, H->fz.k_scale,
+        H->fz.k_shift, H->at<float2>(Ly.rope), rate, c.lr, 1.0f / (float)n, kh, ktr, dy, dyt);
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch PREP");
+    H->timer.end(MONE_SW_STAGE_PREP, s);
+  }
+  // DA: dA0^T = W_out dY0^T (A operand W_out [d_h][d_hp], B operand dY0 [tokens][d_hp])
+  {
+    Spec sp{};
+    sp.part[0].a = opnd(woc, (long long)dh * dhp, dhp, dh);
+    sp.part[0].b = opnd(dy, lhP, dhp, n);
+    sp.part[0].k_len = dhp;
+    sp.nparts = 1;
+    sp.m_extent = dh;
+    sp.n = n;
+    sp.m_store = dh;
+    sp.n_store = -1;
+    EpiSwDa<E> epi;
+    epi.dat = dat; epi.ls = lhT; epi.Tp = Tp;
+    H->timer.begin(s);
+    if ((e = launch_head_gemm<E>(&sp, 1, B, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch DA");
+    H->timer.end(MONE_SW_STAGE_DA, s);
+  }
+  // FWD: [Z | G]^T = W_ig K^T (A operand W_ig [2 d_h][d_hp], B operand K [tokens][d_hp])
+  {
+    Spec sp{};
+    sp.part[0].a = opnd(wig, 2LL * dh * dhp, dhp, 2 * dh);
+    sp.part[0].b = opnd(kh, lhP, dhp, n);
+    sp.part[0].k_len = dhp;
+    sp.nparts = 1;
+    sp.m_extent = 2 * dh;
+    sp.n = n;
+    sp.m_store = 2 * dh;
+    sp.n_store = -1;
+    EpiSwFwd<E> epi;
+    epi.dat = dat; epi.rate = rate; epi.at = At; epi.dzgt = dzgt;
+    epi.loss_part = H->at<float>(Ly.loss_part); epi.ls = lhT; epi.Tp = Tp; epi.n = n; epi.H = NH;
+    epi.parts = 4 * tiles_for(kHeadTile, 2 * dh, n);
+    epi.lr = c.lr;
+    H->timer.begin(s);
+    if ((e = launch_head_gemm<E>(&sp, 1, B, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch FWD");
+    H->timer.end(MONE_SW_STAGE_FWD, s);
+    H->last_parts = epi.parts;
+  }
+  // UPD: problem 0 = A^T dY (W_out's gradient), problem 1 = [dZ | dG]^T K (W_in's and W_gate's)
+  {
+    Spec sp[2] = {};
+    sp[0].part[0].a = opnd(At, lhT, Tp, dh);
+    sp[0].part[0].b = opnd(dyt, lhT, Tp, dh);
+    sp[0].part[0].k_len = kt;
+    sp[0].nparts = 1;
+    sp[0].m_extent = dh;
+    sp[0].n = dh;
+    sp[0].m_store = dh;
+    sp[0].n_store = dh;
+    sp[1].part[0].a = opnd(dzgt, 2 * lhT, Tp, 2 * dh);
+    sp[1].part[0].b = opnd(ktr, lhT, Tp, dh);
+    sp[1].part[0].k_len = kt;
+    sp[1].nparts = 1;
+    sp[1].m_extent = 2 * dh;
+    sp[1].n = dh;
+    sp[1].m_store = 2 * dh;
+    sp[1].n_store = dh;
+    EpiSwUpd<E, PAPER> epi;
+    epi.w_in = H->w.w_in; epi.w_gate = H->w.w_gate; epi.w_out = H->w.w_out;
+    epi.m_in = PAPER ? H->opt.mom_in : nullptr;
+    epi.m_gate = PAPER ? H->opt.mom_gate : nullptr;
+    epi.m_out = PAPER ? H->opt.mom_out : nullptr;
+    epi.wig = wig; epi.woc = woc;
+    epi.beta = PAPER ? H->at<float>(Ly.beta) : nullptr;
+    epi.ss_ig = PAPER ? H->at<float>(Ly.ss_ig) : nullptr;
+    epi.ss_out = PAPER ? H->at<float>(Ly.ss_out) : nullptr;
+    epi.lsw = (long long)dh * dh; epi.dh = dh; epi.dhp = dhp; epi.H = NH; epi.nseg = Ly.nseg;
+    H->timer.begin(s);
+    if ((e = launch_head_gemm<E>(sp, 2, B, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch UPD");
+    H->timer.end(MONE_SW_STAGE_UPD, s);
+  }
+  if constexpr (PAPER) {
+    H->timer.begin(s);
+    sw_renorm_kernel<E><<<dim3((3 * dh + 3) / 4, B), dim3(256), 0, s>>>(
+        H->w.w_in, H->w.w_gate, H->w.w_out, dh, dhp, Ly.nseg, H->at<float>(Ly.ss_ig),
+        H->at<float>(Ly.ss_out), H->at<float>(Ly.n_ig), H->at<float>(Ly.n_out), wig, woc);
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch RENORM");
+    H->timer.end(MONE_SW_STAGE_RENORM, s);
+  }
+  H->last_n = n;
+  return MONE_OK;
+}
+
+template <typename E>
+hipError_t build_copies(mone_swiglu* H, hipStream_t s) {
+  const mone_swiglu_config& c = H->cfg;
+  const SwLayout& Ly = H->lay;
+  const int dh = c.d_head, B = c.n_layers * c.n_heads;
+  const long long per = 3LL * dh * Ly.dhp;
+  sw_pack_kernel<E><<<dim3((unsigned)((per + 255) / 256), B), dim3(256), 0, s>>>(
+      H->w.w_in, H->w.w_gate, H->w.w_out, dh, Ly.dhp, H->at<E>(Ly.wig), H->at<E>(Ly.woc));
+  return hipGetLastError();
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t mone_swiglu_workspace_bytes(const mone_swiglu_config* cfg) {
+  g_err[0] = 0;
+  if (check_sw_config(cfg) != MONE_OK) return 0;
+  return make_sw_layout(cfg).total;
+}
+
+int mone_swiglu_init(mone_swiglu** out, const mone_swiglu_config* cfg,
+                     const mone_swiglu_frozen* frozen, const mone_swiglu_weights* weights,
+                     const mone_swiglu_optimizer* opt, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  g_err[0] = 0;
+  if (!out) return fail(MONE_EINVAL, "out is NULL");
+  *out = nullptr;
+  int rc = check_sw_config(cfg);
+  if (rc != MONE_OK) return rc;
+  if (!frozen || !weights) return fail(MONE_EINVAL, "frozen and weights must be non-NULL");
+  if (!frozen->proj || !frozen->k_scale || !frozen->k_shift || !weights->w_in ||
+      !weights->w_gate || !weights->w_out || !workspace)
+    return fail(MONE_EINVAL, "every frozen and weight pointer and the workspace must be non-NULL");
+  if (!aligned16(frozen->proj) || !aligned16(frozen->k_scale) || !aligned16(frozen->k_shift) ||
+      !aligned16(weights->w_in) || !aligned16(weights->w_gate) || !aligned16(weights->w_out))
+    return fail(MONE_EINVAL, "frozen and weight pointers must be 16-byte aligned");
+  const bool paper = cfg->optimizer == MONE_OPT_PAPER;
+  if (paper != (opt != nullptr))
+    return fail(MONE_EINVAL, paper ? "MONE_OPT_PAPER needs the optimiser state (opt)"
+                                   : "opt must be NULL for MONE_OPT_SGD");
+  if (paper) {
+    if (!opt->rate_w || !opt->rate_b || !opt->decay_w || !opt->decay_b || !opt->mom_in ||
+        !opt->mom_gate || !opt->mom_out)
+      return fail(MONE_EINVAL, "every pointer of the optimiser state must be non-NULL");
+    if (!aligned16(opt->rate_w) || !aligned16(opt->decay_w) || !aligned16(opt->mom_in) ||
+        !aligned16(opt->mom_gate) || !aligned16(opt->mom_out))
+      return fail(MONE_EINVAL, "rate_w, decay_w and the momenta must be 16-byte aligned");
+  }
+  if (((uintptr_t)workspace & (kAlign - 1)) != 0)
+    return fail(MONE_EINVAL, "workspace must be 256-byte aligned");
+  const SwLayout Ly = make_sw_layout(cfg);
+  if (workspace_bytes < Ly.total)
+    return fail(MONE_EINVAL, "workspace has %zu bytes, %zu needed", workspace_bytes, Ly.total);
+
+  mone_swiglu* H = new (std::nothrow) mone_swiglu();
+  if (!H) return fail(MONE_EINVAL, "host allocation failed");
+  H->cfg = *cfg;
+  H->lay = Ly;
+  H->fz = *frozen;
+  H->w = *weights;
+  if (opt) H->opt = *opt;
+  H->ws = reinterpret_cast<unsigned char*>(workspace);
+  H->last_n = 0;
+  H->last_parts = 0;
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = hipMemsetAsync(workspace, 0, Ly.total, s);
+  if (e == hipSuccess)
+    e = cfg->act_dtype == MONE_BF16 ? build_copies<bf16_t>(H, s) : build_copies<float>(H, s);
+  if (e == hipSuccess) {
+    const long long nt = (long long)Ly.Tp * (cfg->d_head / 2);
+    sw_rope_table_kernel<<<dim3((unsigned)((nt + 255) / 256)), dim3(256), 0, s>>>(
+        H->at<float2>(Ly.rope), Ly.Tp, cfg->d_head, (double)cfg->rope_base);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess && paper) {
+    const int B = cfg->n_layers * cfg->n_heads, dh = cfg->d_head;
+    sw_row_norm_kernel<<<dim3((3 * dh + 3) / 4, B), dim3(256), 0, s>>>(
+        weights->w_in, weights->w_gate, weights->w_out, dh, H->at<float>(Ly.n_ig),
+        H->at<float>(Ly.n_out));
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) {
+    delete H;
+    return hip_fail(e, "building the handle's copies");
+  }
+  *out = H;
+  return MONE_OK;
+}
+
+int mone_swiglu_segment(mone_swiglu* H, const void* x, int32_t n_tokens, void* stream) {
+  g_err[0] = 0;
+  if (!H) return fail(MONE_EINVAL, "handle is NULL");
+  if (n_tokens < 0 || n_tokens > H->cfg.seg_len)
+    return fail(MONE_EINVAL, "n_tokens %d outside [0, seg_len=%d]", n_tokens, H->cfg.seg_len);
+  if (n_tokens == 0) return MONE_OK;
+  if (!x) return fail(MONE_EINVAL, "x is NULL");
+  if (!aligned16(x)) return fail(MONE_EINVAL, "x must be 16-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const bool paper = H->cfg.optimizer == MONE_OPT_PAPER;
+  if (H->cfg.act_dtype == MONE_BF16)
+    return paper ? run_sw_segment<bf16_t, true>(H, x, n_tokens, s)
+                 : run_sw_segment<bf16_t, false>(H, x, n_tokens, s);
+  return paper ? run_sw_segment<float, true>(H, x, n_tokens, s)
+               : run_sw_segment<float, false>(H, x, n_tokens, s);
+}
+
+int mone_swiglu_loss(mone_swiglu* H, float* out_host, void* stream) {
+  g_err[0] = 0;
+  if (!H || !out_host) return fail(MONE_EINVAL, "handle and out_host must be non-NULL");
+  if (H->last_n == 0) return fail(MONE_ESTATE, "no non-empty segment has been processed");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int L = H->cfg.n_layers, per = H->cfg.n_heads * H->last_parts;
+  float* dev_out = H->at<float>(H->lay.loss_out);
+  loss_finalize_kernel<<<dim3(L), dim3(256), 0, s>>>(H->at<float>(H->lay.loss_part), per, per,
+                                                      1.0f, dev_out);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "launch loss");
+  if ((e = hipMemcpyAsync(out_host, dev_out, sizeof(float) * L, hipMemcpyDeviceToHost, s)) !=
+      hipSuccess)
+    return hip_fail(e, "copy loss");
+  if ((e = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(e, "synchronise");
+  return MONE_OK;
+}
+
+int mone_swiglu_destroy(mone_swiglu* H) {
+  g_err[0] = 0;
+  if (!H) return MONE_OK;
+  H->timer.destroy();
+  delete H;
+  return MONE_OK;
+}
+
+int mone_swiglu_set_stage_timing(mone_swiglu* H, int32_t max_records) {
+  g_err[0] = 0;
+  if (!H) return fail(MONE_EINVAL, "handle is NULL");
+  return H->timer.enable(max_records);
+}
+
+int mone_swiglu_stage_times(mone_swiglu* H, double* ms_sum, int32_t* count) {
+  g_err[0] = 0;
+  if (!H || !ms_sum || !count) return fail(MONE_EINVAL, "NULL argument");
+  return H->timer.report(ms_sum, count, MONE_SW_N_STAGES);
+}
+
+}  // extern "C"

@@ -36,38 +36,19 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
-#include <cstdarg>
-#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <new>
 #include <vector>
 
 #include "../../include/mone_ttl.h"
-#include "kernels.hpp"
+#include "host_common.hpp"
+
+thread_local char g_err[512] = "";
 
 using namespace mone;
 
 namespace {
-
-thread_local char g_err[512] = "";
-
-int fail(int code, const char* fmt, ...) {
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(g_err, sizeof g_err, fmt, ap);
-  va_end(ap);
-  return code;
-}
-
-int hip_fail(hipError_t e, const char* what) {
-  return fail(MONE_EHIP, "%s: %s", what, hipGetErrorString(e));
-}
-
-constexpr size_t kAlign = 256;
-
-size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
-long long round_up(long long v, long long a) { return (v + a - 1) / a * a; }
 
 struct Layout {
   int Tp;
@@ -149,86 +130,6 @@ Layout make_layout(const mone_ttl_config* c) {
   return L;
 }
 
-bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
-
-enum TileShape { TILE_256x256 = 0, TILE_128x128 = 1, TILE_64x256 = 2, TILE_256x64 = 3 };
-
-constexpr int kNumCUs = 256;
-
-// 64-row tiles for short row extents (short segments, query batches), 64-column tiles for
-// short column extents (the token axis of the transposed backward); 256 x 256 when the grouped
-// problem still has at least one such tile per CU; 128 x 128 otherwise.
-TileShape pick_tile(int m, int n, int layers) {
-  if (m <= 64) return TILE_64x256;
-  if (n <= 64) return TILE_256x64;
-  const long long big = (long long)((m + 255) / 256) * ((n + 255) / 256) * layers;
-  if (m >= 256 && n >= 256 && big >= kNumCUs) return TILE_256x256;
-  return TILE_128x128;
-}
-
-// Host description of one grouped problem before the tile shape fixes its tiling.
-struct Spec {
-  Part part[2];
-  int nparts;
-  int m_extent;   // rows that are computed (tiles cover them)
-  int n;          // columns that are computed
-  int m_store;    // rows stored by the epilogue; -1 = every computed tile row
-  int n_store;    // columns stored by the epilogue; -1 = every computed tile column
-};
-
-Opnd opnd(const void* p, long long lstride, int ld, int rows) {
-  Opnd o;
-  o.p = p;
-  o.lstride = lstride;
-  o.ld = ld;
-  o.rows = rows;
-  return o;
-}
-
-template <typename E, int BM, int BN, int WAVES_M, class Epi>
-hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi,
-                        hipStream_t s, int* tiles_per_layer) {
-  GemmLaunch<Epi> G;
-  std::memset(&G, 0, sizeof G);
-  int begin = 0;
-  for (int i = 0; i < nspec; ++i) {
-    // the kernel reads as many operand parts as the epilogue type declares
-    if (specs[i].nparts < 1 || specs[i].nparts > Epi::kParts) return hipErrorInvalidValue;
-    Problem& P = G.prob[i];
-    P.part[0] = specs[i].part[0];
-    P.part[1] = specs[i].part[1];
-    P.nparts = specs[i].nparts;
-    P.tiles_m = (specs[i].m_extent + BM - 1) / BM;
-    P.tiles_n = (specs[i].n + BN - 1) / BN;
-    P.M = specs[i].m_store >= 0 ? specs[i].m_store : P.tiles_m * BM;
-    P.N = specs[i].n_store >= 0 ? specs[i].n_store : P.tiles_n * BN;
-    P.tile_begin = begin;
-    begin += P.tiles_m * P.tiles_n * layers;
-  }
-  G.nprob = nspec;
-  G.epi = epi;
-  if (tiles_per_layer)  // tiles per layer of each problem
-    for (int i = 0; i < nspec; ++i) tiles_per_layer[i] = G.prob[i].tiles_m * G.prob[i].tiles_n;
-  if (begin == 0) return hipSuccess;
-  gemm_nt_kernel<E, BM, BN, WAVES_M, Epi><<<dim3(begin), dim3(256), 0, s>>>(G);
-  return hipGetLastError();
-}
-
-template <typename E, class Epi>
-hipError_t launch_gemm(TileShape t, const Spec* specs, int nspec, int layers, const Epi& epi,
-                       hipStream_t s, int* tiles_per_layer = nullptr) {
-  switch (t) {
-    case TILE_256x256:
-      return launch_tiled<E, 256, 256, 2>(specs, nspec, layers, epi, s, tiles_per_layer);
-    case TILE_128x128:
-      return launch_tiled<E, 128, 128, 2>(specs, nspec, layers, epi, s, tiles_per_layer);
-    case TILE_256x64:
-      return launch_tiled<E, 256, 64, 4>(specs, nspec, layers, epi, s, tiles_per_layer);
-    default:
-      return launch_tiled<E, 64, 256, 1>(specs, nspec, layers, epi, s, tiles_per_layer);
-  }
-}
-
 }  // namespace
 
 struct mone_ttl {
@@ -242,31 +143,13 @@ struct mone_ttl {
   int last_n;           // tokens of the last non-empty segment (0: none yet)
   int w2t_cur;          // which copy of the W2^T ping-pong pair holds the current weights
   int last_loss_count;  // loss partials per layer written by that segment
-  // stage timing
-  std::vector<hipEvent_t> ev;
-  std::vector<int> ev_stage;
-  int ev_cap = 0, ev_used = 0;
+  StageTimer timer;
 
   template <typename T>
   T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
 
-  void timing_begin(int stage, hipStream_t s) {
-    if (ev_used < ev_cap) (void)hipEventRecord(ev[2 * ev_used], s);
-    (void)stage;
-  }
-  void timing_end(int stage, hipStream_t s) {
-    if (ev_used < ev_cap) {
-      (void)hipEventRecord(ev[2 * ev_used + 1], s);
-      ev_stage[ev_used] = stage;
-      ++ev_used;
-    }
-  }
-  void destroy_events() {
-    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
-    ev.clear();
-    ev_stage.clear();
-    ev_cap = ev_used = 0;
-  }
+  void timing_begin(int, hipStream_t s) { timer.begin(s); }
+  void timing_end(int stage, hipStream_t s) { timer.end(stage, s); }
 };
 
 namespace {
@@ -716,7 +599,7 @@ int mone_ttl_loss(mone_ttl* H, float* out_host, void* stream) {
 int mone_ttl_destroy(mone_ttl* H) {
   g_err[0] = 0;
   if (!H) return MONE_OK;
-  H->destroy_events();
+  H->timer.destroy();
   delete H;
   return MONE_OK;
 }
@@ -726,42 +609,13 @@ const char* mone_ttl_last_error(void) { return g_err; }
 int mone_ttl_set_stage_timing(mone_ttl* H, int32_t max_records) {
   g_err[0] = 0;
   if (!H) return fail(MONE_EINVAL, "handle is NULL");
-  if (max_records < 0) return fail(MONE_EINVAL, "max_records is negative");
-  H->destroy_events();
-  if (max_records == 0) return MONE_OK;
-  H->ev.assign(2 * (size_t)max_records, nullptr);
-  H->ev_stage.assign((size_t)max_records, 0);
-  for (size_t i = 0; i < H->ev.size(); ++i) {
-    hipError_t e = hipEventCreate(&H->ev[i]);
-    if (e != hipSuccess) {
-      H->ev.resize(i);
-      H->destroy_events();
-      return hip_fail(e, "hipEventCreate");
-    }
-  }
-  H->ev_cap = max_records;
-  H->ev_used = 0;
-  return MONE_OK;
+  return H->timer.enable(max_records);
 }
 
 int mone_ttl_stage_times(mone_ttl* H, double* ms_sum, int32_t* count) {
   g_err[0] = 0;
   if (!H || !ms_sum || !count) return fail(MONE_EINVAL, "NULL argument");
-  for (int i = 0; i < MONE_N_STAGES; ++i) {
-    ms_sum[i] = 0.0;
-    count[i] = 0;
-  }
-  for (int i = 0; i < H->ev_used; ++i) {
-    hipError_t e = hipEventSynchronize(H->ev[2 * i + 1]);
-    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
-    float ms = 0.0f;
-    if ((e = hipEventElapsedTime(&ms, H->ev[2 * i], H->ev[2 * i + 1])) != hipSuccess)
-      return hip_fail(e, "hipEventElapsedTime");
-    ms_sum[H->ev_stage[i]] += ms;
-    count[H->ev_stage[i]] += 1;
-  }
-  H->ev_used = 0;
-  return MONE_OK;
+  return H->timer.report(ms_sum, count, MONE_N_STAGES);
 }
 
 }  // extern "C"

@@ -15,6 +15,10 @@ Distributions (the workloads' stated defaults):
   W_k, W_v ~ N(0, 1/d)   stacked as W_kv = [W_k; W_v], shape [2*d_kv, d]
   W1 ~ N(0, 1/d)         shape [h, d]      (variance 1/fan_in)
   W2 ~ N(0, 1/h)         shape [2*d_kv, h] (variance 1/fan_in)
+Paper-form (SwiGLU per head) memory, per layer:
+  P_k, P_v ~ N(0, 1/d)   key and value projections, stacked as [P_k; P_v], shape [2d, d]
+  s = 1 + 0.1 N(0, 1), b = 0.1 N(0, 1)    the keys' per-channel affine step, shape [d] each
+  W_in, W_gate, W_out ~ N(0, 1/d_h)       fast weights, shape [H, d_h, d_h] each
 Meta-parameters of the paper's optimiser (trained offline in the paper; synthetic here):
   u, v ~ N(0, 1/d)       rate and decay projections, shape [d] each
   b_u = log(e - 1)       so that softplus(b_u) = 1: rates average about lr
@@ -25,6 +29,7 @@ from __future__ import annotations
 import numpy as np
 
 KIND_WK, KIND_WV, KIND_W1, KIND_W2, KIND_X, KIND_XQ, KIND_U, KIND_V = range(8)
+KIND_PK, KIND_PV, KIND_KSCALE, KIND_KSHIFT, KIND_WIN, KIND_WGATE, KIND_WOUT = range(8, 15)
 B_U = float(np.log(np.e - 1.0))
 B_V = 0.0
 
@@ -84,6 +89,29 @@ def layer_meta(cfg, layer: int):
     u = normal(cfg.seed, KIND_U, layer, 0, (d,), 1.0 / np.sqrt(d))
     v = normal(cfg.seed, KIND_V, layer, 0, (d,), 1.0 / np.sqrt(d))
     return u, np.float32(B_U), v, np.float32(B_V)
+
+
+def sw_layer_proj(cfg, layer: int) -> np.ndarray:
+    """Frozen [P_k; P_v] of one layer of the paper-form memory, [2d, d], float32."""
+    d = cfg.d_model
+    pk = normal(cfg.seed, KIND_PK, layer, 0, (d, d), 1.0 / np.sqrt(d))
+    pv = normal(cfg.seed, KIND_PV, layer, 0, (d, d), 1.0 / np.sqrt(d))
+    return act_round(np.concatenate([pk, pv], axis=0), cfg.act_dtype)
+
+
+def sw_layer_affine(cfg, layer: int):
+    """The keys' per-channel scale and shift of one layer, [d] float32 each."""
+    d = cfg.d_model
+    scale = (1.0 + normal(cfg.seed, KIND_KSCALE, layer, 0, (d,), 0.1)).astype(np.float32)
+    shift = normal(cfg.seed, KIND_KSHIFT, layer, 0, (d,), 0.1)
+    return scale, shift
+
+
+def sw_layer_fast(cfg, layer: int):
+    """Initial (W_in, W_gate, W_out) of one layer, [H, d_h, d_h] float32 each."""
+    shape, std = (cfg.n_heads, cfg.d_head, cfg.d_head), 1.0 / np.sqrt(cfg.d_head)
+    return tuple(normal(cfg.seed, k, layer, 0, shape, std)
+                 for k in (KIND_WIN, KIND_WGATE, KIND_WOUT))
 
 
 def segment_x(cfg, layer: int, s: int, n_tokens: int | None = None) -> np.ndarray:

@@ -1,4 +1,4 @@
-"""Python binding of libmone_ttl.so (the C ABI in include/mone_ttl.h).
+"""Python binding of libmone_ttl.so (the C ABI in include/mone_ttl.h and include/mone_swiglu.h).
 
 Argument marshalling only: every function forwards to the C call of the same name.  Device
 buffers are passed as torch tensors (their data_ptr()) or as raw integer addresses, streams as
@@ -23,11 +23,17 @@ MONE_OPT_SGD, MONE_OPT_PAPER = 0, 1
 STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2", "rate", "renorm", "attn")
 MONE_N_STAGES = len(STAGES)
 
-# every symbol include/mone_ttl.h declares
+SW_STAGES = ("rate", "proj", "prep", "da", "fwd", "upd", "renorm")
+MONE_SW_N_STAGES = len(SW_STAGES)
+
+# every symbol include/mone_ttl.h and include/mone_swiglu.h declare
 EXPORTS = ("mone_ttl_workspace_bytes", "mone_ttl_init", "mone_ttl_init_paper",
            "mone_ttl_segment", "mone_memory_kv", "mone_memory_attention",
            "mone_ttl_loss", "mone_ttl_destroy", "mone_ttl_last_error",
-           "mone_ttl_set_stage_timing", "mone_ttl_stage_times")
+           "mone_ttl_set_stage_timing", "mone_ttl_stage_times",
+           "mone_swiglu_workspace_bytes", "mone_swiglu_init", "mone_swiglu_segment",
+           "mone_swiglu_loss", "mone_swiglu_destroy", "mone_swiglu_set_stage_timing",
+           "mone_swiglu_stage_times")
 
 
 class MoneError(RuntimeError):
@@ -48,6 +54,31 @@ class mone_paper_optimizer(ctypes.Structure):
     _fields_ = [("rate_w", ctypes.c_void_p), ("rate_b", ctypes.c_void_p),
                 ("decay_w", ctypes.c_void_p), ("decay_b", ctypes.c_void_p),
                 ("mom1", ctypes.c_void_p), ("mom2", ctypes.c_void_p)]
+
+
+class mone_swiglu_config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("d_head", ctypes.c_int32),
+                ("seg_len", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
+                ("optimizer", ctypes.c_int32), ("lr", ctypes.c_float),
+                ("rope_base", ctypes.c_float)]
+
+
+class mone_swiglu_frozen(ctypes.Structure):
+    _fields_ = [("proj", ctypes.c_void_p), ("k_scale", ctypes.c_void_p),
+                ("k_shift", ctypes.c_void_p)]
+
+
+class mone_swiglu_weights(ctypes.Structure):
+    _fields_ = [("w_in", ctypes.c_void_p), ("w_gate", ctypes.c_void_p),
+                ("w_out", ctypes.c_void_p)]
+
+
+class mone_swiglu_optimizer(ctypes.Structure):
+    _fields_ = [("rate_w", ctypes.c_void_p), ("rate_b", ctypes.c_void_p),
+                ("decay_w", ctypes.c_void_p), ("decay_b", ctypes.c_void_p),
+                ("mom_in", ctypes.c_void_p), ("mom_gate", ctypes.c_void_p),
+                ("mom_out", ctypes.c_void_p)]
 
 
 _lib = None
@@ -78,8 +109,23 @@ def lib() -> ctypes.CDLL:
         L.mone_ttl_set_stage_timing.argtypes = [vp, i32]
         L.mone_ttl_stage_times.argtypes = [vp, ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_int32)]
+        swp = ctypes.POINTER(mone_swiglu_config)
+        L.mone_swiglu_workspace_bytes.argtypes = [swp]
+        L.mone_swiglu_workspace_bytes.restype = ctypes.c_size_t
+        L.mone_swiglu_init.argtypes = [ctypes.POINTER(vp), swp,
+                                       ctypes.POINTER(mone_swiglu_frozen),
+                                       ctypes.POINTER(mone_swiglu_weights),
+                                       ctypes.POINTER(mone_swiglu_optimizer), vp, ctypes.c_size_t,
+                                       vp]
+        L.mone_swiglu_segment.argtypes = [vp, vp, i32, vp]
+        L.mone_swiglu_loss.argtypes = [vp, ctypes.POINTER(ctypes.c_float), vp]
+        L.mone_swiglu_destroy.argtypes = [vp]
+        L.mone_swiglu_set_stage_timing.argtypes = [vp, i32]
+        L.mone_swiglu_stage_times.argtypes = [vp, ctypes.POINTER(ctypes.c_double),
+                                              ctypes.POINTER(ctypes.c_int32)]
         for name in EXPORTS:
-            if name not in ("mone_ttl_workspace_bytes", "mone_ttl_last_error"):
+            if name not in ("mone_ttl_workspace_bytes", "mone_ttl_last_error",
+                            "mone_swiglu_workspace_bytes"):
                 getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -234,6 +280,107 @@ class TtlSession:
     def close(self):
         if self.handle:
             mone_ttl_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ---------------------------------------------------------------- paper-form (SwiGLU) memory
+
+def make_swiglu_config(n_layers, d_model, n_heads, d_head, seg_len, act_dtype, optimizer, lr,
+                       rope_base=10000.0) -> mone_swiglu_config:
+    dt = {"f32": MONE_F32, "bf16": MONE_BF16}.get(act_dtype, act_dtype)
+    op = {"sgd": MONE_OPT_SGD, "paper": MONE_OPT_PAPER}.get(optimizer, optimizer)
+    return mone_swiglu_config(int(n_layers), int(d_model), int(n_heads), int(d_head),
+                              int(seg_len), int(dt), int(op), float(lr), float(rope_base))
+
+
+def swiglu_config_from(cfg) -> mone_swiglu_config:
+    """C config of a configs.SwigluConfig."""
+    return make_swiglu_config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.d_head, cfg.seg_len,
+                              cfg.act_dtype, cfg.optimizer, cfg.lr, cfg.rope_base)
+
+
+def mone_swiglu_workspace_bytes(cfg: mone_swiglu_config) -> int:
+    n = lib().mone_swiglu_workspace_bytes(ctypes.byref(cfg))
+    if n == 0:
+        raise MoneError(MONE_EINVAL, mone_ttl_last_error())
+    return n
+
+
+def mone_swiglu_init(cfg: mone_swiglu_config, frozen: mone_swiglu_frozen,
+                     weights: mone_swiglu_weights, opt, workspace, workspace_bytes: int,
+                     stream=None) -> int:
+    h = ctypes.c_void_p()
+    _check(lib().mone_swiglu_init(ctypes.byref(h), ctypes.byref(cfg),
+                                  ctypes.byref(frozen) if frozen is not None else None,
+                                  ctypes.byref(weights) if weights is not None else None,
+                                  ctypes.byref(opt) if opt is not None else None,
+                                  _ptr(workspace), int(workspace_bytes), _stream(stream)))
+    return h.value
+
+
+def mone_swiglu_segment(handle: int, x, n_tokens: int, stream=None) -> None:
+    _check(lib().mone_swiglu_segment(handle, _ptr(x), int(n_tokens), _stream(stream)))
+
+
+def mone_swiglu_loss(handle: int, n_layers: int, stream=None) -> list[float]:
+    out = (ctypes.c_float * n_layers)()
+    _check(lib().mone_swiglu_loss(handle, out, _stream(stream)))
+    return list(out)
+
+
+def mone_swiglu_destroy(handle: int) -> None:
+    _check(lib().mone_swiglu_destroy(handle))
+
+
+def mone_swiglu_set_stage_timing(handle: int, max_records: int) -> None:
+    _check(lib().mone_swiglu_set_stage_timing(handle, int(max_records)))
+
+
+def mone_swiglu_stage_times(handle: int) -> dict:
+    ms = (ctypes.c_double * MONE_SW_N_STAGES)()
+    cnt = (ctypes.c_int32 * MONE_SW_N_STAGES)()
+    _check(lib().mone_swiglu_stage_times(handle, ms, cnt))
+    return {name: (ms[i], cnt[i]) for i, name in enumerate(SW_STAGES)}
+
+
+class SwigluSession:
+    """Device state of one paper-form TTL run.
+
+    proj [L, 2d, d] (activation dtype), k_scale and k_shift [L, d] fp32, and the fast weights
+    w_in, w_gate, w_out [L, H, d_h, d_h] fp32 are torch tensors on the GPU; opt, for
+    cfg.optimizer == "paper", is (rate_w [L, d], rate_b [L], decay_w [L, d], decay_b [L],
+    mom_in, mom_gate, mom_out), all fp32.  The workspace is allocated here with torch.
+    """
+
+    def __init__(self, cfg, proj, k_scale, k_shift, w_in, w_gate, w_out, opt=None, stream=None):
+        import torch
+        self.cfg = cfg
+        self.ccfg = swiglu_config_from(cfg)
+        self.keep = (proj, k_scale, k_shift, w_in, w_gate, w_out, opt)
+        self.frozen = mone_swiglu_frozen(_ptr(proj), _ptr(k_scale), _ptr(k_shift))
+        self.weights = mone_swiglu_weights(_ptr(w_in), _ptr(w_gate), _ptr(w_out))
+        self.copt = mone_swiglu_optimizer(*(_ptr(t) for t in opt)) if opt is not None else None
+        self.ws_bytes = mone_swiglu_workspace_bytes(self.ccfg)
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=w_in.device)
+        self.handle = mone_swiglu_init(self.ccfg, self.frozen, self.weights, self.copt,
+                                       self.workspace, self.ws_bytes, stream)
+
+    def segment(self, x, n_tokens=None, stream=None):
+        n = x.shape[1] if n_tokens is None else n_tokens
+        mone_swiglu_segment(self.handle, x, n, stream)
+
+    def loss(self, stream=None):
+        return mone_swiglu_loss(self.handle, self.cfg.n_layers, stream)
+
+    def close(self):
+        if self.handle:
+            mone_swiglu_destroy(self.handle)
             self.handle = None
 
     def __del__(self):
