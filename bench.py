@@ -131,6 +131,183 @@ def cpu_baseline(cfg, w1, w2, wkv, xs, budget_s, meta=None):
                       f"({t:.1f} s, float64 NumPy), scaled to {cfg.n_layers} layers"}
 
 
+def sw_stage_work(cfg):
+    """Algorithmic FLOPs and bytes of one launch of each stage of the paper-form memory (all
+    layers and heads; B = L H head problems of d_h x d_h; T tokens)."""
+    L, d, H, dh, T = cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.d_head, cfg.seg_len
+    E = 2 if cfg.act_dtype == "bf16" else 4
+    B = L * H
+    paper = cfg.optimizer == "paper"
+    # the three masters are read and written in fp32 and their MFMA copies written (+ the
+    # momentum's read and write with the paper's optimiser, whose row renormalisation happens
+    # in the same epilogue)
+    upd_w = 3 * dh * dh * (8 + E + (8 if paper else 0))
+    return {
+        "rate": (L * 4 * T * d, L * (T * d * E + 2 * d * 4 + T * 4)),
+        # the projections with the elementwise preprocessing fused: X and P in; K', dY0 and
+        # dY^T out
+        "proj": (L * 2 * T * 2 * d * d, L * (4 * T * d + 2 * d * d) * E),
+        # K' in; K and K^T out
+        "keys": (0, 3 * L * T * d * E),
+        "da": (B * 2 * T * dh * dh, B * (dh * dh + 2 * T * dh) * E),
+        "fwd": (B * 2 * T * 2 * dh * dh, B * (2 * dh * dh + 5 * T * dh) * E + L * T * 4),
+        "upd": (B * 2 * T * 3 * dh * dh, B * (5 * dh * T * E + upd_w)),
+    }
+
+
+def sw_cpu_baseline(cfg, host, xs, budget_s, meta):
+    import numpy as np
+
+    import oracle.swiglu_memory as sw
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()
+                     if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    proj, scale, shift, fast = host
+    d = cfg.d_model
+    frozen = dict(p_k=proj[:d], p_v=proj[d:], scale=scale, shift=shift)
+    fast = tuple(np.asarray(w, np.float64) for w in fast)
+    if meta is not None:
+        norms0 = sw.initial_norms(fast)
+        mom = tuple(np.zeros_like(w) for w in fast)
+    done, t0 = 0, time.perf_counter()
+    while True:
+        x = xs[done % len(xs)]
+        if meta is None:
+            fast, _ = sw.sgd_step(x, fast, frozen, cfg.lr, cfg.n_heads, cfg.rope_base)
+        else:
+            fast, mom, _, _ = sw.paper_step(x, fast, mom, frozen, meta, norms0, cfg.lr,
+                                            cfg.n_heads, cfg.rope_base)
+        done += 1
+        if time.perf_counter() - t0 >= budget_s or done >= 256:
+            break
+    t = time.perf_counter() - t0
+    return {"value": done * cfg.seg_len / t / cfg.n_layers, "unit": "tokens/s",
+            "cores": int(cores), "kind": "oracle",
+            "sample": f"layer 0, {done} consecutive segments of T={cfg.seg_len} tokens "
+                      f"({t:.1f} s, float64 NumPy), scaled to {cfg.n_layers} layers"}
+
+
+def run_swiglu(args):
+    """The paper-form memory (SwiGLU per fast-weight head) at the paper's shape: one step is
+    every segment of the context through mone_swiglu_segment (all layers and heads)."""
+    import numpy as np
+    import torch
+
+    from paper_2608_17616_amd import configs, inputs, mone
+
+    cfg = configs.SW_CONFIGS[args.config if args.config in configs.SW_CONFIGS
+                             else "sw_qwen0.5b"].with_(optimizer=args.optimizer)
+    L, d, H, dh, T = cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.d_head, cfg.seg_len
+    S = args.segments or cfg.n_segments
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    act = torch.bfloat16 if cfg.act_dtype == "bf16" else torch.float32
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfg.seed)
+    f32 = torch.float32
+    proj = inputs.device_normal_(torch.empty(L, 2 * d, d, dtype=act, device=dev),
+                                 1 / np.sqrt(d), gen)
+    k_scale = inputs.device_normal_(torch.empty(L, d, dtype=f32, device=dev), 0.1, gen) + 1.0
+    k_shift = inputs.device_normal_(torch.empty(L, d, dtype=f32, device=dev), 0.1, gen)
+    w = [inputs.device_normal_(torch.empty(L, H, dh, dh, dtype=f32, device=dev),
+                               1 / np.sqrt(dh), gen) for _ in range(3)]
+    ctx = torch.empty(S, L, T, d, dtype=act, device=dev)
+    for s in range(S):
+        inputs.device_normal_(ctx[s], 1.0, gen)
+    opt = None
+    if cfg.optimizer == "paper":
+        opt = (inputs.device_normal_(torch.empty(L, d, dtype=f32, device=dev), 1 / np.sqrt(d),
+                                     gen),
+               torch.full((L,), inputs.B_U, dtype=f32, device=dev),
+               inputs.device_normal_(torch.empty(L, d, dtype=f32, device=dev), 1 / np.sqrt(d),
+                                     gen),
+               torch.full((L,), inputs.B_V, dtype=f32, device=dev),
+               *(torch.zeros_like(t) for t in w))
+    n_cpu = 0 if args.no_cpu_baseline else min(S, 4)
+    cpu_in = None
+    if n_cpu:
+        host = (proj[0].double().cpu().numpy(), k_scale[0].double().cpu().numpy(),
+                k_shift[0].double().cpu().numpy(), tuple(t[0].double().cpu().numpy() for t in w))
+        cpu_in = (host, [ctx[s, 0].double().cpu().numpy() for s in range(n_cpu)])
+
+    stream = torch.cuda.current_stream(dev)
+    sess = mone.SwigluSession(cfg, proj, k_scale, k_shift, *w, opt=opt, stream=stream)
+    Hd = sess.handle
+    sptr = stream.cuda_stream
+
+    def step():
+        for s in range(S):
+            mone.mone_swiglu_segment(Hd, ctx[s], T, sptr)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    mone.mone_swiglu_set_stage_timing(Hd, args.steps * S * 6)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stimes = mone.mone_swiglu_stage_times(Hd)
+    finite = all(bool(torch.isfinite(t).all().item()) for t in w)
+    sess.close()
+
+    tokens = args.steps * S * T
+    value = tokens / elapsed
+    flop_tok = cfg.flops_per_token()
+    peak = PEAK_BF16_TFLOPS if cfg.act_dtype == "bf16" else PEAK_F32_TFLOPS
+    work = sw_stage_work(cfg)
+    stages = {}
+    for name, (ms, cnt) in stimes.items():
+        if cnt == 0:
+            continue
+        fl, by = work[name]
+        avg_s = ms / cnt / 1e3
+        stages[name] = {"launches": cnt, "avg_ms": round(ms / cnt, 4),
+                        "tflops": round(fl / avg_s / 1e12, 1),
+                        "gbs": round(by / avg_s / 1e9, 1)}
+    dom = max(stages, key=lambda k: stimes[k][0])
+    dfl, dby = work[dom]
+    davg = stimes[dom][0] / stimes[dom][1] / 1e3
+    if dfl > 0:
+        roof = {"kernel": f"gemm_nt_kernel ({dom})", "bound": "mfma",
+                "achieved": round(dfl / davg / 1e12, 1), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(dfl / davg / 1e12 / peak, 4), "traffic": None}
+    else:
+        roof = {"kernel": {"keys": "sw_keys_kernel", "rate": "rate_kernel"}[dom],
+                "bound": "hbm",
+                "achieved": round(dby / davg / 1e9, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(dby / davg / 1e9 / PEAK_HBM_GBS, 4), "traffic": None}
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.act_dtype, "data": "synthetic",
+        "config": {"workload": f"paper-form SwiGLU memory TTL ({cfg.name}): L={L} d={d} "
+                               f"H={H} d_h={dh} T={T} N={S * T} ({S} segments), "
+                               f"{'paper optimiser' if cfg.optimizer == 'paper' else 'SGD'}",
+                   "n_layers": L, "d_model": d, "n_heads": H, "d_head": dh, "seg_len": T,
+                   "n_context": S * T, "lr": cfg.lr, "optimizer": cfg.optimizer,
+                   "loss": "nip"},
+        "mfma_pct": round(100.0 * value * flop_tok / (peak * 1e12), 2),
+        "flop_per_token": flop_tok,
+        "roofline": roof,
+        "stages": stages,
+        "finite": finite,
+    }
+    if cpu_in is not None:
+        meta = None
+        if opt is not None:
+            meta = (opt[0][0].double().cpu().numpy(), float(opt[1][0]),
+                    opt[2][0].double().cpu().numpy(), float(opt[3][0]))
+        out["cpu_baseline"] = sw_cpu_baseline(cfg, *cpu_in, args.cpu_seconds, meta)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -146,15 +323,26 @@ def main():
     ap.add_argument("--loss", default=None, choices=("mse_sum", "mse_mean", "nip"),
                     help="override the configuration's loss (nip: the paper's negative inner "
                          "product, whose step skips the output layer's forward)")
-    ap.add_argument("--optimizer", default="sgd", choices=("sgd", "paper"),
-                    help="the configuration's SGD, or the paper's optimiser (per-token rates, "
-                         "momentum, row renormalisation)")
+    ap.add_argument("--optimizer", default=None, choices=("sgd", "paper"),
+                    help="SGD or the paper's optimiser (per-token rates, momentum, row "
+                         "renormalisation); default: SGD for the configurations' memory, the "
+                         "paper's optimiser for the paper-form memory (whose negative inner "
+                         "product loss is unbounded below: plain SGD lets the weights grow "
+                         "without limit over a long context)")
+    ap.add_argument("--memory", default="config", choices=("config", "swiglu"),
+                    help="config: the configurations' 2-layer memory (default); swiglu: the "
+                         "paper-form SwiGLU memory per fast-weight head at the paper's shape")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: this build measures one GPU "
               "(the path would shard by layers with no communication during TTL).",
               file=sys.stderr, flush=True)
         sys.exit(2)
+    if args.memory == "swiglu":
+        args.optimizer = args.optimizer or "paper"
+        run_swiglu(args)
+        return
+    args.optimizer = args.optimizer or "sgd"
 
     import numpy as np
     import torch

@@ -113,14 +113,15 @@ int mone_swiglu_destroy(mone_swiglu* h);
 
 /* ---- measurement hooks (as mone_ttl_set_stage_timing / mone_ttl_stage_times) ------------ */
 #define MONE_SW_STAGE_RATE 0   /* MONE_OPT_PAPER: per-token rates and the momentum decay */
-#define MONE_SW_STAGE_PROJ 1   /* [P_k x ; P_v x] for every token (one grouped GEMM) */
-#define MONE_SW_STAGE_PREP 2   /* keys: affine, SiLU, L2, RoPE; values: SiLU; operand copies */
+#define MONE_SW_STAGE_PROJ 1   /* [P_k x ; P_v x] for every token (one grouped GEMM) with the
+                                  keys' affine step and SiLU and the values' SiLU fused */
+#define MONE_SW_STAGE_KEYS 2   /* keys: per-token L2 norm per head and RoPE; K and K^T */
 #define MONE_SW_STAGE_DA 3     /* dA^T = W_out dY^T per head: the hidden activations' gradient */
 #define MONE_SW_STAGE_FWD 4    /* [Z | G]^T = [W_in ; W_gate] K^T per head; epilogue: A^T,
                                   dZ^T, dG^T and the loss partials */
-#define MONE_SW_STAGE_UPD 5    /* the three weight gradients and the update (one launch) */
-#define MONE_SW_STAGE_RENORM 6 /* MONE_OPT_PAPER: row renormalisation and the copies */
-#define MONE_SW_N_STAGES 7
+#define MONE_SW_STAGE_UPD 5    /* the three weight gradients and the update (one launch; with
+                                  MONE_OPT_PAPER also the momentum and the row renormalisation) */
+#define MONE_SW_N_STAGES 6
 
 int mone_swiglu_set_stage_timing(mone_swiglu* h, int32_t max_records);
 int mone_swiglu_stage_times(mone_swiglu* h, double* ms_sum, int32_t* count);

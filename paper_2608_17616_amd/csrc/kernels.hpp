@@ -37,14 +37,21 @@
 #include <utility>
 
 namespace mone {
-// Internal linkage: every library source file that includes this header has its own copies.
-namespace {
 
 typedef uint16_t bf16_t;  // raw bf16 storage (same bits as torch.bfloat16)
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer load of size bytes per lane straight into LDS (no VGPR staging): lane l's data lands
+// at M0 + 16*l for 16-byte loads; offsets at or beyond the descriptor's byte count read 0.
+__device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t* lds,
+                                    int size, int voffset, int soffset, int offset,
+                                    int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+
+// Internal linkage: every library source file that includes this header has its own copies.
+namespace {
 
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(bf16_t v) { return __uint_as_float((uint32_t)v << 16); }
@@ -133,11 +140,6 @@ struct GemmLaunch {
 // ------------------------------------------------------------------------------------------
 // The grouped GEMM kernel
 
-// Buffer load of size bytes per lane straight into LDS (no VGPR staging): lane l's data lands
-// at M0 + 16*l for 16-byte loads; offsets at or beyond the descriptor's byte count read 0.
-__device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t* lds,
-                                    int size, int voffset, int soffset, int offset,
-                                    int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
 
 // Raw buffer descriptor over [p, p + bytes): stride 0, range-checked by byte offset.
 __device__ __forceinline__ i32x4 make_rsrc(const void* p, uint32_t bytes) {
@@ -471,6 +473,11 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   constexpr int CPL = SB * SB / 8 / 64;         // row (and column) chunks per lane: 8
   static_assert(WM % SB == 0 && WN % SB == 0, "wave tile");
   float* stw = reinterpret_cast<float*>(smem) + wave * (SB * SB);
+  // kRowScale: per-wave partial sums of squares of the tile's rows, after the 4 staging areas
+  float* rss = reinterpret_cast<float*>(smem) + 4 * SB * SB;
+  static_assert(!Epi::kRowScale || (NSB == 1 && WAVES_M == 1 &&
+                                    TC::SMEM >= (4 * SB * SB + 4 * SB) * 4),
+                "row scale: one 64 x 64 sub-block per wave, the 4 waves side by side");
   auto sidx = [](int r, int c) { return r * SB + (c ^ (((r ^ (r >> 3)) & 7) << 2)); };
   auto wave_sync = [] {  // this wave's LDS writes are visible to all its lanes
     __builtin_amdgcn_s_waitcnt((63 & 15) | ((63 >> 4) << 14) | (7 << 4));  // lgkmcnt(0)
@@ -483,8 +490,11 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   // Row chunks per lane: 8, or 4 pairs of rows (2i, 2i + 1) when the epilogue pairs rows.
   constexpr int RS = Epi::kPairRows ? 2 : 1;
   constexpr int NCH = CPL / RS;
-  static_assert(!Epi::kPairRows || (!Epi::kRowNorm && !Epi::kCols && !Epi::kWriteback),
+  static_assert(!Epi::kPairRows || (!Epi::kRowNorm && !Epi::kCols && !Epi::kWriteback &&
+                                     !Epi::kRowScale),
                 "paired rows: row pass only");
+  static_assert(!Epi::kRowScale || (Epi::kWriteback && !Epi::kRowNorm && !Epi::kCols),
+                "row scale: row pass with write-back, then the scale pass");
   float aux[2][NCH][NAUX];
   const int rl = lane >> 3, ql = lane & 7;      // row-chunk lane coordinates
   auto issue_pre = [&](int sb, float (&ax)[NCH][NAUX]) {
@@ -541,7 +551,13 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
           *reinterpret_cast<float4*>(s1) = make_float4(v[4], v[5], v[6], v[7]);
         }
       }
-      if constexpr (!Epi::kPairRows) {
+      if constexpr (Epi::kRowScale) {
+        // this wave's 64-column part of the row's sum of squares, for the scale pass
+        val += __shfl_xor(val, 1, 64);
+        val += __shfl_xor(val, 2, 64);
+        val += __shfl_xor(val, 4, 64);
+        if (ql == 0) rss[wave * SB + r] = val;
+      } else if constexpr (!Epi::kPairRows) {
         if constexpr (Epi::kRowNorm) {
           // the 8 lanes of a row segment are lanes 8*rl .. 8*rl+7: a fixed-order tree sum
           val += __shfl_xor(val, 1, 64);
@@ -569,6 +585,23 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       }
     }
   }
+  if constexpr (Epi::kRowScale) {
+    // Scale pass: every row of the tile is whole in this workgroup (4 waves x 64 columns); its
+    // sum of squares is the 4 waves' parts in a fixed order.  The row pass left the unscaled
+    // values in each wave's staging.
+    __syncthreads();
+    const int grow = m0, gcol = n0 + wave * SB;
+#pragma unroll
+    for (int b = 0; b < CPL; ++b) {
+      const int r = rl + 8 * b, c = 8 * ql;
+      if (grow + r >= P.M || gcol + c >= P.N) continue;
+      const float tot = ((rss[r] + rss[SB + r]) + rss[2 * SB + r]) + rss[3 * SB + r];
+      const float4 x0 = *reinterpret_cast<const float4*>(stw + sidx(r, c));
+      const float4 x1 = *reinterpret_cast<const float4*>(stw + sidx(r, c + 4));
+      const float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+      G.epi.scale8(pi, layer, grow + r, gcol + c, tot, v);
+    }
+  }
   G.epi.finish(pi, layer, t, wave, lane, partial);
 }
 
@@ -589,6 +622,10 @@ struct EpiBase {
                                            // is reduced per 64-column row segment
   static constexpr bool kPairRows = false; // rows8p(v = row r, w = row r + 1) for even r
                                            // replaces rows8 (row pass only)
+  static constexpr bool kRowScale = false; // rows8 writes its results back and returns their
+                                           // sum of squares; after a workgroup barrier
+                                           // scale8 gets each whole row's sum (64 x 256 tiles)
+  __device__ __forceinline__ void scale8(int, int, int, int, float, const float (&)[8]) const {}
   __device__ __forceinline__ void row_partial(int, int, int, int, float) const {}
   static constexpr bool kCols = false;
   static constexpr bool kWriteback = false;
@@ -1025,8 +1062,10 @@ __device__ __forceinline__ void wave_dot2(const E* __restrict__ row, const float
 }
 
 // Per-token rates rate[l][j] = lr * softplus(u_l . x_j + b_u[l]) for j < n (0 for n <= j < Tp),
-// and per-block sums of v_l . x_j over the block's tokens (64 tokens per block, summed in token
-// order), from which decay_kernel forms the momentum decay.  Grid (Tp / 64, L), 256 threads.
+// and per-block sums of v_l . x_j over the block's kRateTokens tokens (summed in token order),
+// from which decay_kernel forms the momentum decay.  Grid (Tp / kRateTokens, L), 256 threads:
+// each wave takes kRateTokens / 4 consecutive tokens.
+constexpr int kRateTokens = 16;
 template <typename E>
 __global__ __launch_bounds__(256) void rate_kernel(const E* __restrict__ x, long long x_ls, int d,
                                                    int n, const float* __restrict__ u,
@@ -1034,11 +1073,13 @@ __global__ __launch_bounds__(256) void rate_kernel(const E* __restrict__ x, long
                                                    const float* __restrict__ v, float lr,
                                                    float* __restrict__ rate, int Tp,
                                                    float* __restrict__ vpart) {
-  const int l = blockIdx.y, j0 = blockIdx.x * 64, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  constexpr int TW = kRateTokens / 4;
+  const int l = blockIdx.y, j0 = blockIdx.x * kRateTokens, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
   __shared__ float wsum[4];
   float acc = 0.0f;
-  for (int t = 0; t < 16; ++t) {
-    const int j = j0 + wave * 16 + t;
+  for (int t = 0; t < TW; ++t) {
+    const int j = j0 + wave * TW + t;
     float pu = 0.0f, pv = 0.0f;
     if (j < n)
       wave_dot2(x + (long long)l * x_ls + (long long)j * d, u + (long long)l * d,
@@ -1051,7 +1092,8 @@ __global__ __launch_bounds__(256) void rate_kernel(const E* __restrict__ x, long
   if (lane == 0) wsum[wave] = acc;
   __syncthreads();
   if (threadIdx.x == 0)
-    vpart[(long long)l * (Tp / 64) + blockIdx.x] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+    vpart[(long long)l * (Tp / kRateTokens) + blockIdx.x] =
+        ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
 }
 
 // beta[l] = sigmoid(mean_j (v_l . x_j) + b_v[l]) = sigmoid(v_l . xbar + b_v[l]).

@@ -5,7 +5,7 @@
 // Data layout in HBM (row-major; B = L * H head operands, b = l * H + e; Tp = seg_len rounded
 // up to 256; d_hp = d_h rounded up to 64, padding columns zero):
 //   caller state   W_in, W_gate, W_out [L][H][d_h][d_h] fp32; P [L][2d][d] act; s, b [L][d]
-//   workspace      raw  [L][Tp][2d] fp32   raw key and value projections
+//   workspace      K'   [L][Tp][d] act     keys after the affine step and SiLU
 //                  K    [B][Tp][d_hp]      preprocessed keys (B operand of FWD)
 //                  K^T  [B][d_h][Tp]       (B operand of the W_in / W_gate gradients)
 //                  dY0  [B][Tp][d_hp]      -v / n (B operand of DA)
@@ -17,15 +17,17 @@
 //                  W_ig [B][2 d_h][d_hp], W_out copy [B][d_h][d_hp]  MFMA copies
 //                  RoPE table [Tp][d_h/2] (cos, sin); loss partials; loss [L]
 //                  paper optimiser (fp32): rates [L][Tp], decay block sums, decay [L],
-//                  initial row norms, row-segment sums of squares
+//                  initial row norms
 // A segment step, each stage one launch grouped over all layers (PROJ) or all B heads:
 //   [RATE]  per-token rates and momentum decay (paper optimiser)
-//   PROJ    [raw K | raw V] = X [P_k ; P_v]^T
-//   PREP    keys: affine, SiLU, L2, RoPE -> K, K^T; values: SiLU -> dY0, dY^T
+//   PROJ    [raw K | raw V] = X [P_k ; P_v]^T   epilogue: keys: affine, SiLU -> K';
+//                                               values: SiLU -> dY0, dY^T
+//   KEYS    K': per-token L2 norm per head, RoPE -> K, K^T
 //   DA      dA0^T = W_out dY0^T
 //   FWD     [Z | G]^T = W_ig K^T     epilogue: A^T, [dZ | dG]^T, loss partials
 //   UPD     A^T dY and [dZ | dG]^T K  (2 problems)  epilogue: update of the masters + copies
-//   [RENORM] rows back to their initial norms, copies (paper optimiser)
+//           (paper optimiser: momentum, and each row rescaled to its initial norm in the same
+//           epilogue, 64 x 256 tiles holding whole rows)
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -40,9 +42,9 @@ using namespace mone;
 namespace {
 
 struct SwLayout {
-  int Tp, dhp, nseg, parts_max;
-  size_t raw, kh, kt, dy, dyt, dat, at, dzgt, wig, woc, rope, loss_part, loss_out;
-  size_t rate, vpart, beta, n_ig, n_out, ss_ig, ss_out;  // paper optimiser
+  int Tp, dhp, parts_max;
+  size_t kpre, kh, kt, dy, dyt, dat, at, dzgt, wig, woc, rope, loss_part, loss_out;
+  size_t rate, vpart, beta, n_ig, n_out;  // paper optimiser
   size_t total;
 };
 
@@ -69,7 +71,7 @@ int check_sw_config(const mone_swiglu_config* c) {
   const long long Tp = round_up(c->seg_len, 256), d = c->d_model;
   const long long E = c->act_dtype == MONE_BF16 ? 2 : 4;
   // per-layer and per-head operand slices are addressed with 32-bit byte offsets
-  if (Tp * 2 * d * 4 >= (1LL << 31) || 2 * d * d * E >= (1LL << 31))
+  if (Tp * d * E >= (1LL << 31) || 2 * d * d * E >= (1LL << 31))
     return fail(MONE_EUNSUPPORTED, "a per-layer matrix exceeds 2^31 bytes");
   return MONE_OK;
 }
@@ -81,7 +83,6 @@ SwLayout make_sw_layout(const mone_swiglu_config* c) {
   const size_t B = nl * (size_t)c->n_heads;
   L.Tp = (int)round_up(c->seg_len, 256);
   L.dhp = (int)round_up(c->d_head, 64);
-  L.nseg = (c->d_head + 63) / 64;
   // 4 wave partials per FWD tile; no tile shape is smaller than 64 in either direction
   L.parts_max = 4 * ((2 * c->d_head + 63) / 64) * (L.Tp / 64);
   const size_t Tp = L.Tp, dhp = L.dhp;
@@ -91,7 +92,7 @@ SwLayout make_sw_layout(const mone_swiglu_config* c) {
     off = align_up(off + bytes, kAlign);
     return o;
   };
-  L.raw = take(nl * Tp * 2 * d * 4);
+  L.kpre = take(nl * Tp * d * E);
   L.kh = take(B * Tp * dhp * E);
   L.kt = take(B * dh * Tp * E);
   L.dy = take(B * Tp * dhp * E);
@@ -106,12 +107,10 @@ SwLayout make_sw_layout(const mone_swiglu_config* c) {
   L.loss_out = take(nl * 4);
   if (c->optimizer == MONE_OPT_PAPER) {
     L.rate = take(nl * Tp * 4);
-    L.vpart = take(nl * (Tp / 64) * 4);
+    L.vpart = take(nl * (Tp / kRateTokens) * 4);
     L.beta = take(nl * 4);
     L.n_ig = take(B * 2 * dh * 4);
     L.n_out = take(B * dh * 4);
-    L.ss_ig = take(B * 2 * dh * (size_t)L.nseg * 4);
-    L.ss_out = take(B * dh * (size_t)L.nseg * 4);
   }
   L.total = off;
   return L;
@@ -153,7 +152,7 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
   const int L = c.n_layers, d = c.d_model, NH = c.n_heads, dh = c.d_head, B = L * NH;
   const int Tp = Ly.Tp, dhp = Ly.dhp;
   constexpr int BK = 8 * (16 / (int)sizeof(E));
-  const int nz = (int)round_up(n, 64);   // token extent PREP writes
+  const int nz = (int)round_up(n, 64);   // token extent KEYS writes
   const int kt = (int)round_up(n, BK);   // token extent of the UPD contractions
   E* kh = H->at<E>(Ly.kh);
   E* ktr = H->at<E>(Ly.kt);
@@ -170,15 +169,16 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
 
   if constexpr (PAPER) {
     H->timer.begin(s);
-    rate_kernel<E><<<dim3(Tp / 64, L), dim3(256), 0, s>>>(
+    rate_kernel<E><<<dim3(Tp / kRateTokens, L), dim3(256), 0, s>>>(
         reinterpret_cast<const E*>(x), lsx, d, n, H->opt.rate_w, H->opt.rate_b, H->opt.decay_w,
         c.lr, rate, Tp, H->at<float>(Ly.vpart));
-    decay_kernel<<<dim3((L + 63) / 64), dim3(64), 0, s>>>(H->at<float>(Ly.vpart), Tp / 64, n,
+    decay_kernel<<<dim3((L + 63) / 64), dim3(64), 0, s>>>(H->at<float>(Ly.vpart),
+                                                          Tp / kRateTokens, n,
                                                           H->opt.decay_b, H->at<float>(Ly.beta), L);
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch RATE");
     H->timer.end(MONE_SW_STAGE_RATE, s);
   }
-  // PROJ: [raw K | raw V] = X [P_k ; P_v]^T, fp32
+  // PROJ: [raw K | raw V] = X [P_k ; P_v]^T; epilogue: K', dY0, dY^T
   {
     Spec sp{};
     sp.part[0].a = opnd(x, lsx, d, n);
@@ -189,23 +189,26 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
     sp.n = 2 * d;
     sp.m_store = -1;
     sp.n_store = 2 * d;
-    EpiSwProj epi;
-    epi.raw = H->at<float>(Ly.raw); epi.ls = (long long)Tp * 2 * d; epi.ld = 2 * d;
+    EpiSwProj<E> epi;
+    epi.kpre = H->at<E>(Ly.kpre); epi.dy = dy; epi.dyt = dyt;
+    epi.kscale = H->fz.k_scale; epi.kshift = H->fz.k_shift; epi.rate = rate;
+    epi.lr = c.lr; epi.inv_n = 1.0f / (float)n;
+    epi.d = d; epi.dh = dh; epi.dhp = dhp; epi.H = NH; epi.Tp = Tp; epi.n = n;
     H->timer.begin(s);
-    if ((e = launch_gemm<E>(pick_tile(n, 2 * d, L), &sp, 1, L, epi, s)) != hipSuccess)
+    // 128 x 128 tiles (measured faster here than 256 x 256, which leave most CUs idle in
+    // their second round); 64-row tiles for short segments
+    const TileShape tp = n <= 64 ? TILE_64x256 : TILE_128x128;
+    if ((e = launch_gemm<E>(tp, &sp, 1, L, epi, s)) != hipSuccess)
       return hip_fail(e, "launch PROJ");
     H->timer.end(MONE_SW_STAGE_PROJ, s);
   }
-  // PREP
+  // KEYS: per-token L2 norm per head and RoPE -> K, K^T
   {
-    const int TB = (64 * (dh + 1) + 64) * 4 <= 65536 ? 64 : 32;
-    const size_t shmem = (size_t)(TB * (dh + 1) + TB) * 4;
     H->timer.begin(s);
-    sw_prep_kernel<E><<<dim3(nz / TB, NH, L), dim3(256), shmem, s>>>(
-        H->at<float>(Ly.raw), (long long)Tp * 2 * d, d, n, NH, dh, dhp, Tp, TB, H->fz.k_scale,
-        H->fz.k_shift, H->at<float2>(Ly.rope), rate, c.lr, 1.0f / (float)n, kh, ktr, dy, dyt);
-    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch PREP");
-    H->timer.end(MONE_SW_STAGE_PREP, s);
+    sw_keys_kernel<E><<<dim3(nz / 64, NH, L), dim3(256), 0, s>>>(
+        H->at<E>(Ly.kpre), d, NH, dh, dhp, Tp, H->at<float2>(Ly.rope), kh, ktr);
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch KEYS");
+    H->timer.end(MONE_SW_STAGE_KEYS, s);
   }
   // DA: dA0^T = W_out dY0^T (A operand W_out [d_h][d_hp], B operand dY0 [tokens][d_hp])
   {
@@ -273,21 +276,18 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
     epi.m_out = PAPER ? H->opt.mom_out : nullptr;
     epi.wig = wig; epi.woc = woc;
     epi.beta = PAPER ? H->at<float>(Ly.beta) : nullptr;
-    epi.ss_ig = PAPER ? H->at<float>(Ly.ss_ig) : nullptr;
-    epi.ss_out = PAPER ? H->at<float>(Ly.ss_out) : nullptr;
-    epi.lsw = (long long)dh * dh; epi.dh = dh; epi.dhp = dhp; epi.H = NH; epi.nseg = Ly.nseg;
+    epi.n_ig = PAPER ? H->at<float>(Ly.n_ig) : nullptr;
+    epi.n_out = PAPER ? H->at<float>(Ly.n_out) : nullptr;
+    epi.lsw = (long long)dh * dh; epi.dh = dh; epi.dhp = dhp; epi.H = NH;
     H->timer.begin(s);
-    if ((e = launch_head_gemm<E>(sp, 2, B, epi, s)) != hipSuccess)
-      return hip_fail(e, "launch UPD");
+    // the paper's optimiser renormalises whole rows in the epilogue: 64 x 256 tiles, one
+    // workgroup per 64 rows of a head's matrix (d_h <= 256 columns)
+    if constexpr (PAPER)
+      e = launch_tiled<E, 64, 256, 1>(sp, 2, B, epi, s, nullptr);
+    else
+      e = launch_head_gemm<E>(sp, 2, B, epi, s);
+    if (e != hipSuccess) return hip_fail(e, "launch UPD");
     H->timer.end(MONE_SW_STAGE_UPD, s);
-  }
-  if constexpr (PAPER) {
-    H->timer.begin(s);
-    sw_renorm_kernel<E><<<dim3((3 * dh + 3) / 4, B), dim3(256), 0, s>>>(
-        H->w.w_in, H->w.w_gate, H->w.w_out, dh, dhp, Ly.nseg, H->at<float>(Ly.ss_ig),
-        H->at<float>(Ly.ss_out), H->at<float>(Ly.n_ig), H->at<float>(Ly.n_out), wig, woc);
-    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch RENORM");
-    H->timer.end(MONE_SW_STAGE_RENORM, s);
   }
   H->last_n = n;
   return MONE_OK;

@@ -117,7 +117,7 @@ Layout make_layout(const mone_ttl_config* c) {
   L.loss_out = take(nl * 4);
   if (c->optimizer == MONE_OPT_PAPER) {
     L.rate = take(nl * Tp * 4);
-    L.vpart = take(nl * (Tp / 64) * 4);
+    L.vpart = take(nl * (Tp / kRateTokens) * 4);
     L.beta = take(nl * 4);
     L.norm1 = take(nl * h * 4);
     L.norm2 = take(nl * D * 4);
@@ -188,10 +188,11 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
   // RATE (paper optimiser): per-token rates and the momentum decay of this segment
   if constexpr (PAPER) {
     H->timing_begin(MONE_STAGE_RATE, s);
-    rate_kernel<E><<<dim3(Tp / 64, Lc), dim3(256), 0, s>>>(
+    rate_kernel<E><<<dim3(Tp / kRateTokens, Lc), dim3(256), 0, s>>>(
         reinterpret_cast<const E*>(x), lsx, d, n, H->opt.rate_w, H->opt.rate_b, H->opt.decay_w,
         c.lr, H->at<float>(Ly.rate), Tp, H->at<float>(Ly.vpart));
-    decay_kernel<<<dim3((Lc + 63) / 64), dim3(64), 0, s>>>(H->at<float>(Ly.vpart), Tp / 64, n,
+    decay_kernel<<<dim3((Lc + 63) / 64), dim3(64), 0, s>>>(H->at<float>(Ly.vpart),
+                                                           Tp / kRateTokens, n,
                                                            H->opt.decay_b, H->at<float>(Ly.beta), Lc);
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch RATE");
     H->timing_end(MONE_STAGE_RATE, s);

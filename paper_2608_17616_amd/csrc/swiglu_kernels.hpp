@@ -13,15 +13,59 @@
 namespace mone {
 namespace {
 
-// PROJ: tile of X [P_k ; P_v]^T = [raw keys | raw values] [tokens][2d], stored in fp32.
+// PROJ: tile of X [P_k ; P_v]^T = [raw keys | raw values] [tokens][2d], with the elementwise
+// part of the preprocessing fused:
+//   key columns    SiLU(s r + b) per channel  -> K' [L][Tp][d] (normalised and rotated by the
+//                  KEYS kernel)
+//   value columns  v = SiLU(r)                -> dY0 = -v / n [B][Tp][d_hp] (row pass) and
+//                  dY^T = -eta v / n [B][d_h][Tp] (column pass, from v left in the staging)
+// Tokens >= n are stored as 0.  d and d_h are multiples of 8, so a chunk never straddles the
+// key/value boundary or a head.
+template <typename E>
 struct EpiSwProj : EpiBase {
-  float* raw;
-  long long ls;  // Tp * 2d
-  int ld;        // 2d
-  __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
-                                         float (&v)[8], const float (&)[8]) const {
-    store8(raw + (long long)layer * ls + (long long)row * ld + col, v);
+  static constexpr bool kCols = true;
+  static constexpr bool kWriteback = true;
+  E* kpre; E* dy; E* dyt;
+  const float* kscale; const float* kshift;  // [L][d]
+  const float* rate;                          // [L][Tp] per-token rates, or null (lr)
+  float lr, inv_n;
+  int d, dh, dhp, H, Tp, n;
+  __device__ __forceinline__ bool has_cols(int) const { return true; }
+  __device__ __forceinline__ float rows8(int, int l, int row, int col, int, int, float (&v)[8],
+                                         const float (&)[8]) const {
+    float o[8];
+    if (col < d) {
+      const float* sc = kscale + (long long)l * d + col;
+      const float* sh = kshift + (long long)l * d + col;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float u = sc[e] * v[e] + sh[e];
+        o[e] = row < n ? u * sigmoidf_(u) : 0.0f;
+      }
+      store8(kpre + ((long long)l * Tp + row) * d + col, o);
+    } else {
+      const int c = col - d, e = c / dh, ch = c - e * dh;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float sv = row < n ? v[i] * sigmoidf_(v[i]) : 0.0f;
+        v[i] = sv;
+        o[i] = -sv * inv_n;
+      }
+      store8(dy + (((long long)l * H + e) * Tp + row) * dhp + ch, o);
+    }
     return 0.0f;
+  }
+  __device__ __forceinline__ void cols8(int, int l, int row, int col, int, int,
+                                        const float (&v)[8]) const {
+    if (col < d) return;
+    const int c = col - d, e = c / dh, ch = c - e * dh;
+    float o[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float eta = rate ? rate[(long long)l * Tp + row + i] : lr;
+      o[i] = -eta * v[i] * inv_n;
+    }
+    store8(dyt + (((long long)l * H + e) * dh + ch) * Tp + row, o);
   }
 };
 
@@ -100,22 +144,26 @@ struct EpiSwFwd : EpiBase {
 // UPD: problem 0 is the tile of A^T dY [d_h][d_h] (the gradient of W_out, rows = hidden
 // units), problem 1 the tile of [dZ | dG]^T K [2 d_h][d_h] (the gradients of W_in and W_gate,
 // rows interleaved as in FWD).  The rates are already inside dY and dZ, dG, so the SGD update is
-// W - acc.  fp32 read-modify-write of the masters, then the MFMA copies the next segment reads:
-// W_ig (interleaved rows) and W_out, d_hp columns each.  With the paper's optimiser (PAPER):
-// mu = beta mu + acc, W - mu, and each row chunk's sum of squares for the renormalisation,
-// which writes the copies afterwards.
+// W - acc: fp32 read-modify-write of the masters, then the MFMA copies the next segment reads
+// (W_ig with interleaved rows, and W_out; d_hp columns each).
+// With the paper's optimiser (PAPER) the launch uses 64 x 256 tiles, so each workgroup holds
+// whole rows (d_h <= 256): the row pass updates the momentum, mu = beta mu + acc, and leaves
+// W - mu in the staging; after the workgroup has summed each row's squares, the scale pass
+// rescales the row to its initial norm (norm0 / norm; 1 for a row of norm 0) and stores the
+// master and its copy.
 template <typename E, bool PAPER>
 struct EpiSwUpd : EpiBase {
   static constexpr bool kPre = true;
   static constexpr int kAux = PAPER ? 16 : 8;
-  static constexpr bool kRowNorm = PAPER;
+  static constexpr bool kWriteback = PAPER;
+  static constexpr bool kRowScale = PAPER;
   float* w_in; float* w_gate; float* w_out;   // masters [B][d_h][d_h]
   float* m_in; float* m_gate; float* m_out;   // PAPER: momenta, same layout
   E* wig; E* woc;                             // copies [B][2 d_h][d_hp], [B][d_h][d_hp]
   const float* beta;                          // PAPER: [L]
-  float* ss_ig; float* ss_out;                // PAPER: [B][2 d_h][nseg], [B][d_h][nseg]
+  const float* n_ig; const float* n_out;      // PAPER: initial row norms [B][2 d_h], [B][d_h]
   long long lsw;                              // d_h * d_h
-  int dh, dhp, H, nseg;
+  int dh, dhp, H;
   __device__ __forceinline__ long long off(int pi, int b, int row, int col) const {
     return (long long)b * lsw + (long long)(pi ? row >> 1 : row) * dh + col;
   }
@@ -124,6 +172,10 @@ struct EpiSwUpd : EpiBase {
   }
   __device__ __forceinline__ float* mom(int pi, int row) const {
     return pi == 0 ? m_out : (row & 1) ? m_gate : m_in;
+  }
+  __device__ __forceinline__ E* copy(int pi, int b, int row, int col) const {
+    return pi == 0 ? woc + ((long long)b * dh + row) * dhp + col
+                   : wig + ((long long)b * 2 * dh + row) * dhp + col;
   }
   __device__ __forceinline__ void pre8(int pi, int b, int row, int col, int, int,
                                        float (&w)[kAux]) const {
@@ -134,36 +186,35 @@ struct EpiSwUpd : EpiBase {
   __device__ __forceinline__ float rows8(int pi, int b, int row, int col, int, int,
                                          float (&v)[8], const float (&w)[kAux]) const {
     const long long o = off(pi, b, row, col);
-    float nw[8];
     if constexpr (PAPER) {
       const float bt = beta[b / H];
       float m[8], ss = 0.0f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         m[e] = bt * w[8 + e] + v[e];
-        nw[e] = w[e] - m[e];
-        ss += nw[e] * nw[e];
+        v[e] = w[e] - m[e];
+        ss += v[e] * v[e];
       }
       store8(mom(pi, row) + o, m);
-      store8(master(pi, row) + o, nw);
       return ss;
     } else {
+      float nw[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) nw[e] = w[e] - v[e];
       store8(master(pi, row) + o, nw);
-      E* cp = pi == 0 ? woc + ((long long)b * dh + row) * dhp + col
-                      : wig + ((long long)b * 2 * dh + row) * dhp + col;
-      store8(cp, nw);
+      store8(copy(pi, b, row, col), nw);
       return 0.0f;
     }
   }
-  __device__ __forceinline__ void row_partial(int pi, int b, int row, int cb, float ss) const {
-    if (PAPER) {
-      if (pi == 0)
-        ss_out[((long long)b * dh + row) * nseg + cb] = ss;
-      else
-        ss_ig[((long long)b * 2 * dh + row) * nseg + cb] = ss;
-    }
+  __device__ __forceinline__ void scale8(int pi, int b, int row, int col, float ss,
+                                         const float (&v)[8]) const {
+    const float n0 = pi == 0 ? n_out[(long long)b * dh + row] : n_ig[(long long)b * 2 * dh + row];
+    const float sc = ss > 0.0f ? n0 * rsqrtf(ss) : 1.0f;
+    float nw[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) nw[e] = v[e] * sc;
+    store8(master(pi, row) + off(pi, b, row, col), nw);
+    store8(copy(pi, b, row, col), nw);
   }
 };
 
@@ -180,99 +231,64 @@ __global__ void sw_rope_table_kernel(float2* __restrict__ tab, int Tp, int dh, d
   tab[i] = make_float2((float)cs, (float)sn);
 }
 
-// PREP: one workgroup per (TB tokens, head e, layer l).  From the fp32 raw projections:
-//   keys   SiLU(s r + b) per channel, divided by max(norm, 1e-12) per token, then rotated by
-//          RoPE at the token's position; written as K [B][Tp][d_hp] (zero padding columns) and
-//          K^T [B][d_h][Tp];
-//   values SiLU(r); written as dY0 = -v / n [B][Tp][d_hp] (unit rates, zero padding) and
-//          dY^T = -eta v / n [B][d_h][Tp] (eta the token's rate, or lr).
-// Tokens n <= j < j0 + TB are written as 0.  Dynamic LDS: TB * (d_h + 1) + TB floats.
+// KEYS: one workgroup per (64 tokens, head e, layer l); one wave per token at a time.  From the
+// post-SiLU keys K' of the head, each token's keys are divided by max(norm, 1e-12) and rotated
+// by RoPE at the token's position (the table holds cos and sin per position and channel pair);
+// written as K [B][Tp][d_hp] (zero padding columns) and, through LDS, K^T [B][d_h][Tp].
+// Lane l holds channels 4l .. 4l + 3; the partner of channel c < d_h/2 is c + d_h/2, held by
+// lane l + d_h/8 (d_h is a multiple of 8).  Tokens >= n hold zeros in K' and stay zero.
 template <typename E>
-__global__ __launch_bounds__(256) void sw_prep_kernel(
-    const float* __restrict__ raw, long long raw_ls, int d, int n, int H, int dh, int dhp,
-    int Tp, int TB, const float* __restrict__ kscale, const float* __restrict__ kshift,
-    const float2* __restrict__ rope, const float* __restrict__ rate, float lr, float inv_n,
-    E* __restrict__ kh, E* __restrict__ kt, E* __restrict__ dy, E* __restrict__ dyt) {
-  extern __shared__ float sm[];
-  const int LD = dh + 1;
-  float* sk = sm;
-  float* sinv = sm + TB * LD;
-  const int j0 = blockIdx.x * TB, e = blockIdx.y, l = blockIdx.z, b = l * H + e;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int d2 = 2 * d, half = dh / 2;
-  const float* rk = raw + (long long)l * raw_ls + (long long)e * dh;
-  const float* sc = kscale + (long long)l * d + (long long)e * dh;
-  const float* sh = kshift + (long long)l * d + (long long)e * dh;
-  const long long okh = (long long)b * Tp * dhp, okt = (long long)b * dh * Tp;
-
-  // keys: affine, SiLU
-  for (int i = tid; i < TB * dh; i += 256) {
-    const int t = i / dh, c = i - t * dh, j = j0 + t;
-    float kv = 0.0f;
-    if (j < n) {
-      const float u = sc[c] * rk[(long long)j * d2 + c] + sh[c];
-      kv = u * sigmoidf_(u);
+__global__ __launch_bounds__(256) void sw_keys_kernel(const E* __restrict__ kpre, int d, int H,
+                                                      int dh, int dhp, int Tp,
+                                                      const float2* __restrict__ rope,
+                                                      E* __restrict__ kh, E* __restrict__ kt) {
+  __shared__ float tile[64][257];  // [token][channel], d_h <= 256
+  const int j0 = blockIdx.x * 64, e = blockIdx.y, l = blockIdx.z, b = l * H + e;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = dh / 2, q = dh / 8, c = 4 * lane;
+  const bool act = c < dh;
+  const bool lo = c < half;
+  const int src = act ? (lo ? lane + q : lane - q) : lane;
+  for (int t = wave; t < 64; t += 4) {
+    const int j = j0 + t;
+    float x[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (act) {
+      const E* p = kpre + ((long long)l * Tp + j) * d + (long long)e * dh + c;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[i] = to_f32(p[i]);
     }
-    sk[t * LD + c] = kv;
-  }
-  __syncthreads();
-  // per-token inverse norms (one wave per token, fixed-order reduction)
-  for (int t = wave; t < TB; t += 4) {
-    float ss = 0.0f;
-    for (int c = lane; c < dh; c += 64) {
-      const float x = sk[t * LD + c];
-      ss += x * x;
-    }
+    float ss = x[0] * x[0] + x[1] * x[1] + x[2] * x[2] + x[3] * x[3];
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
-    if (lane == 0) sinv[t] = 1.0f / fmaxf(sqrtf(ss), 1e-12f);
-  }
-  __syncthreads();
-  // normalise and rotate in place; row-major copy with zero padding
-  for (int i = tid; i < TB * half; i += 256) {
-    const int t = i / half, c = i - t * half, j = j0 + t;
-    const float inv = sinv[t];
-    const float x1 = sk[t * LD + c] * inv, x2 = sk[t * LD + c + half] * inv;
-    const float2 cs = rope[(long long)j * half + c];
-    const float o1 = x1 * cs.x - x2 * cs.y, o2 = x1 * cs.y + x2 * cs.x;
-    sk[t * LD + c] = o1;
-    sk[t * LD + c + half] = o2;
-    E* kr = kh + okh + (long long)j * dhp;
-    kr[c] = from_f32<E>(o1);
-    kr[c + half] = from_f32<E>(o2);
-  }
-  const int pad = dhp - dh;
-  for (int i = tid; i < TB * pad; i += 256) {
-    const int t = i / pad, c = dh + i - t * pad;
-    kh[okh + (long long)(j0 + t) * dhp + c] = from_f32<E>(0.0f);
-  }
-  __syncthreads();
-  for (int i = tid; i < dh * TB; i += 256) {
-    const int c = i / TB, t = i - c * TB;
-    kt[okt + (long long)c * Tp + j0 + t] = from_f32<E>(sk[t * LD + c]);
-  }
-  __syncthreads();
-  // values: SiLU
-  const float* rv = rk + d;
-  for (int i = tid; i < TB * dh; i += 256) {
-    const int t = i / dh, c = i - t * dh, j = j0 + t;
-    float vv = 0.0f;
-    if (j < n) {
-      const float r = rv[(long long)j * d2 + c];
-      vv = r * sigmoidf_(r);
+    const float inv = 1.0f / fmaxf(sqrtf(ss), 1e-12f);
+    float y[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) y[i] = __shfl(x[i], src, 64);
+    float o[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (act) {
+      const float2* cs = rope + (long long)j * half + (lo ? c : c - half);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float2 r = cs[i];
+        // c < d_h/2: x cos - partner sin; c >= d_h/2: partner sin + x cos
+        o[i] = (lo ? x[i] * r.x - y[i] * r.y : y[i] * r.y + x[i] * r.x) * inv;
+        tile[t][c + i] = o[i];
+      }
     }
-    sk[t * LD + c] = vv;
+    if (c < dhp) {
+      E* kr = kh + ((long long)b * Tp + j) * dhp + c;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) kr[i] = from_f32<E>(o[i]);
+    }
   }
   __syncthreads();
-  for (int i = tid; i < TB * dhp; i += 256) {
-    const int t = i / dhp, c = i - t * dhp;
-    const float val = c < dh ? -sk[t * LD + c] * inv_n : 0.0f;
-    dy[okh + (long long)(j0 + t) * dhp + c] = from_f32<E>(val);
-  }
-  for (int i = tid; i < dh * TB; i += 256) {
-    const int c = i / TB, t = i - c * TB, j = j0 + t;
-    const float eta = rate ? rate[(long long)l * Tp + j] : lr;
-    dyt[okt + (long long)c * Tp + j] = from_f32<E>(-eta * sk[t * LD + c] * inv_n);
+  // K^T: 8 threads per channel row, 8 tokens (one vector) each
+  for (int i = threadIdx.x; i < dh * 8; i += 256) {
+    const int ch = i >> 3, t0 = (i & 7) * 8;
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = tile[t0 + k][ch];
+    store8(kt + ((long long)b * dh + ch) * Tp + j0 + t0, v);
   }
 }
 
@@ -326,33 +342,6 @@ __global__ __launch_bounds__(256) void sw_row_norm_kernel(float* w_in, float* w_
       n_ig[(long long)b * 2 * dh + r] = sqrtf(s);
     else
       n_out[(long long)b * dh + r - 2 * dh] = sqrtf(s);
-  }
-}
-
-// Renormalisation of the paper's optimiser: every master row is rescaled to its initial norm,
-// scale = norm0 / sqrt(sum of the row's nseg segment sums of squares, fixed order), 1 for a row
-// of norm 0; the MFMA copy of the row is written from the rescaled values.
-// One wave per row; grid (ceil(3 d_h / 4), B).
-template <typename E>
-__global__ __launch_bounds__(256) void sw_renorm_kernel(
-    float* w_in, float* w_gate, float* w_out, int dh, int dhp, int nseg,
-    const float* __restrict__ ss_ig, const float* __restrict__ ss_out,
-    const float* __restrict__ n_ig, const float* __restrict__ n_out, E* __restrict__ wig,
-    E* __restrict__ woc) {
-  const int b = blockIdx.y, r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (r >= 3 * dh) return;
-  float* row = sw_row(w_in, w_gate, w_out, b, r, dh);
-  const bool ig = r < 2 * dh;
-  const long long ri = ig ? (long long)b * 2 * dh + r : (long long)b * dh + r - 2 * dh;
-  const float* ss = (ig ? ss_ig : ss_out) + ri * nseg;
-  float s = 0.0f;
-  for (int k = 0; k < nseg; ++k) s += ss[k];
-  const float scale = s > 0.0f ? (ig ? n_ig : n_out)[ri] * rsqrtf(s) : 1.0f;
-  E* cp = (ig ? wig : woc) + ri * dhp;
-  for (int c = lane; c < dh; c += 64) {
-    const float v = row[c] * scale;
-    row[c] = v;
-    cp[c] = from_f32<E>(v);
   }
 }
 

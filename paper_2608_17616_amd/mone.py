@@ -23,7 +23,7 @@ MONE_OPT_SGD, MONE_OPT_PAPER = 0, 1
 STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2", "rate", "renorm", "attn")
 MONE_N_STAGES = len(STAGES)
 
-SW_STAGES = ("rate", "proj", "prep", "da", "fwd", "upd", "renorm")
+SW_STAGES = ("rate", "proj", "keys", "da", "fwd", "upd")
 MONE_SW_N_STAGES = len(SW_STAGES)
 
 # every symbol include/mone_ttl.h and include/mone_swiglu.h declare

@@ -115,7 +115,7 @@ def test_paper_optimizer_workspace_adds_only_its_small_buffers():
     p = _cfg(optimizer="paper")
     n, n_p = mone.mone_ttl_workspace_bytes(c), mone.mone_ttl_workspace_bytes(p)
     L, d, h, D, Tp = 2, 128, 192, 128, 256
-    extra = 4 * L * (Tp + Tp // 64 + 1 + h + D + h * (d // 64) + D * (h // 64) + h + D)
+    extra = 4 * L * (Tp + Tp // 16 + 1 + h + D + h * (d // 64) + D * (h // 64) + h + D)
     assert extra <= n_p - n <= extra + 9 * 256
 
 
@@ -172,7 +172,7 @@ def test_swiglu_workspace_formula():
                                          + 3 * dh * dhp) + Tp * (dh // 2) * 8)
     assert act <= n <= act + 64 * 1024
     p = mone.mone_swiglu_workspace_bytes(_swcfg(optimizer="paper"))
-    extra = 4 * (L * Tp + L * (Tp // 64) + L + 3 * B * dh + 3 * B * dh * 2)
+    extra = 4 * (L * Tp + L * (Tp // 16) + L + 3 * B * dh + 3 * B * dh * 2)
     assert extra <= p - n <= extra + 8 * 256
     # the context length is not a parameter of any call
     for cfg in configs.SW_CONFIGS.values():
