@@ -31,6 +31,18 @@ Readings (the paper leaves these open):
     (W_in, W_gate: one hidden unit's input weights; W_out: the output pattern one hidden unit
     writes).
 
+At read time (Eq. read, Eq. attn) the query tokens' hidden states x_q go through the query
+projection P_q and the keys' preprocessing (with the query's own affine step; RoPE at positions
+0..Q-1, Sec. 3.3), the memory reads them per head, and the output o_e of each head is
+RMS-normalised and gated (Sec. 3.2, App. A.2):
+    h_{j,e} = RMSNorm(o_{j,e}) * w_rms_e * SiLU(a_e . x_j + c_e),
+    RMSNorm(o) = o / sqrt(mean(o^2) + 1e-6);
+the memory tokens h are then projected by the backbone's frozen key and value maps, [h W_k^T |
+h W_v^T], and join the query tokens' attention (memory_attention).
+Readings of the read path: the gate is a learned per-head vector a_e (and bias c_e) on the
+query token's hidden state, passed through SiLU (per head, Sec. 3.2; SiLU-gated, App. A.2);
+the RMSNorm has a learned per-channel weight w_rms.
+
 Float64 NumPy; plain loops over heads; matmul is the library primitive.
 Pins: tests/test_oracle_swiglu_memory.py.
 """
@@ -224,6 +236,43 @@ def swiglu_run(segments, fast, frozen, lr, n_heads: int, optimizer: str = "sgd",
     return fast, mom, losses
 
 
+# ------------------------------------------------------------------ the read
+
+RMS_EPS = 1e-6
+
+
+def rms_normalise(o):
+    """Rows of o divided by sqrt(mean(row^2) + 1e-6)."""
+    o = _f64(o)
+    return o / np.sqrt(np.mean(o * o, axis=1, keepdims=True) + RMS_EPS)
+
+
+def memory_tokens(xq, fast, reader, n_heads: int, base: float = ROPE_BASE):
+    """Memory tokens h [Q, H*d_h] of query hidden states xq [Q, d_in] at the fast weights fast.
+
+    reader = dict(p_q [d, d_in], q_scale [d], q_shift [d], rms_w [d], gate_w [H, d_in],
+    gate_b [H])."""
+    xq = _f64(xq)
+    q = preprocess_keys(xq @ _f64(reader["p_q"]).T, reader["q_scale"], reader["q_shift"],
+                        n_heads, np.arange(xq.shape[0]), base)
+    o = memory_read(q, fast)
+    dh = o.shape[1] // n_heads
+    gate = silu(xq @ _f64(reader["gate_w"]).T + _f64(reader["gate_b"])[None, :])  # [Q, H]
+    h = np.empty_like(o)
+    w = _f64(reader["rms_w"])
+    for e in range(n_heads):
+        cols = slice(e * dh, (e + 1) * dh)
+        h[:, cols] = rms_normalise(o[:, cols]) * w[None, cols] * gate[:, e:e + 1]
+    return h
+
+
+def memory_kv(h, w_kv):
+    """The memory tokens in the backbone's key/value space: [h W_k^T | h W_v^T], with
+    w_kv = [W_k ; W_v] of shape [2 d_kv, d]."""
+    return _f64(h) @ _f64(w_kv).T
+
+
 __all__ = ["rope", "l2_normalise", "preprocess_keys", "preprocess_values", "layer_keys_values",
            "swiglu_forward", "memory_read", "nip_loss", "weighted_grad", "sgd_step",
-           "initial_norms", "paper_step", "swiglu_run", "sigmoid", "ROPE_BASE"]
+           "initial_norms", "paper_step", "swiglu_run", "sigmoid", "ROPE_BASE", "rms_normalise",
+           "memory_tokens", "memory_kv"]

@@ -305,3 +305,73 @@ def test_paper_momentum_carries_with_beta_and_norms_stay_fixed():
         np.testing.assert_allclose(np.linalg.norm(end[m], axis=2), np.linalg.norm(fast[m], axis=2),
                                    rtol=1e-13)
     assert np.linalg.norm(end[0] - fast[0]) > 1e-3 and len(losses) == 5
+
+
+# ---------------------------------------------------------------- the read
+
+def _reader(rng, d_in, H, dh, d_kv):
+    d = H * dh
+    return dict(p_q=rng.standard_normal((d, d_in)) / math.sqrt(d_in),
+                q_scale=1.0 + 0.3 * rng.standard_normal(d), q_shift=0.2 * rng.standard_normal(d),
+                rms_w=1.0 + 0.2 * rng.standard_normal(d),
+                gate_w=rng.standard_normal((H, d_in)) / math.sqrt(d_in),
+                gate_b=0.3 * rng.standard_normal(H),
+                w_kv=rng.standard_normal((2 * d_kv, d)) / math.sqrt(d))
+
+
+def test_memory_tokens_brute_force():
+    rng = np.random.default_rng(20)
+    H, dh, d_in, Q = 2, 4, 6, 3
+    fast, rd = _fast(rng, H, dh), _reader(rng, d_in, H, dh, 4)
+    xq = rng.standard_normal((Q, d_in))
+    got = sw.memory_tokens(xq, fast, rd, H, base=50.0)
+    q = _keys_brute(xq @ rd["p_q"].T, rd["q_scale"], rd["q_shift"], H, list(range(Q)), 50.0)
+    for j in range(Q):
+        for e in range(H):
+            ke = q[j, e * dh:(e + 1) * dh]
+            a = []
+            for i in range(dh):
+                z = sum(fast[0][e, i, c] * ke[c] for c in range(dh))
+                g = sum(fast[1][e, i, c] * ke[c] for c in range(dh))
+                a.append(z / (1.0 + math.exp(-z)) * g)
+            o = [sum(fast[2][e, i, c] * a[i] for i in range(dh)) for c in range(dh)]
+            rms = math.sqrt(sum(t * t for t in o) / dh + 1e-6)
+            gl = sum(rd["gate_w"][e, k] * xq[j, k] for k in range(d_in)) + rd["gate_b"][e]
+            gate = gl / (1.0 + math.exp(-gl))
+            for c in range(dh):
+                want = o[c] / rms * rd["rms_w"][e * dh + c] * gate
+                assert got[j, e * dh + c] == pytest.approx(want, rel=1e-11, abs=1e-14)
+
+
+def test_memory_tokens_are_scale_free_in_w_out_and_have_unit_rms():
+    """RMSNorm per head: scaling one head's W_out leaves its tokens unchanged (up to the 1e-6
+    in the norm, negligible once mean(o^2) is large: W_out is scaled up first), and with unit
+    norm weights and a gate of SiLU(z) the RMS of a head's token is SiLU(z)."""
+    rng = np.random.default_rng(21)
+    H, dh, d_in, Q = 3, 8, 5, 4
+    fast, rd = _fast(rng, H, dh), _reader(rng, d_in, H, dh, 4)
+    fast = (fast[0], fast[1], 1e4 * fast[2])
+    xq = rng.standard_normal((Q, d_in))
+    h = sw.memory_tokens(xq, fast, rd, H)
+    w_out = fast[2].copy()
+    w_out[1] *= 7.0
+    h2 = sw.memory_tokens(xq, (fast[0], fast[1], w_out), rd, H)
+    np.testing.assert_allclose(h2, h, rtol=1e-8)
+    rd1 = dict(rd, rms_w=np.ones(H * dh), gate_w=np.zeros((H, d_in)),
+               gate_b=np.array([0.5, 1.0, 2.0]))
+    h1 = sw.memory_tokens(xq, fast, rd1, H).reshape(Q, H, dh)
+    rms = np.sqrt(np.mean(h1 * h1, axis=2))
+    want = np.array([0.5, 1.0, 2.0]) / (1.0 + np.exp(-np.array([0.5, 1.0, 2.0])))
+    for j in range(Q):
+        np.testing.assert_allclose(rms[j], want, rtol=1e-8)
+
+
+def test_memory_kv_is_the_backbone_projection():
+    rng = np.random.default_rng(22)
+    h = rng.standard_normal((3, 8))
+    w_kv = rng.standard_normal((6, 8))
+    got = sw.memory_kv(h, w_kv)
+    for j in range(3):
+        for o in range(6):
+            assert got[j, o] == pytest.approx(sum(h[j, c] * w_kv[o, c] for c in range(8)),
+                                               rel=1e-13)
