@@ -108,6 +108,42 @@ int mone_swiglu_segment(mone_swiglu* h, const void* x, int32_t n_tokens, void* s
  * MONE_ESTATE before the first non-empty segment. */
 int mone_swiglu_loss(mone_swiglu* h, float* out_host, void* stream);
 
+/* Frozen parameters of the read (borrowed for the duration of a call, read only). */
+typedef struct {
+  const void* proj_q;    /* [L][d][d] act_dtype: the query projection P_q */
+  const float* q_scale;  /* [L][d] fp32: per-channel scale of the queries' affine step */
+  const float* q_shift;  /* [L][d] fp32: per-channel shift */
+  const float* rms_w;    /* [L][d] fp32: per-channel weight of the memory tokens' RMSNorm */
+  const float* gate_w;   /* [L][H][d] fp32: per-head gate vectors a_e */
+  const float* gate_b;   /* [L][H] fp32: per-head gate biases c_e */
+  const void* w_kv;      /* [L][2 d_kv][d] act_dtype: the backbone's [W_k ; W_v] */
+  int32_t d_kv;          /* width of K and of V (a multiple of 64) */
+} mone_swiglu_reader;
+
+/* Read of the current fast weights on query-side inputs, without any update (Eq. read, with the
+ * per-head RMSNorm and gate of Sec. 3.2 and the projection of Eq. attn), per layer and query
+ * token j (positions j = 0 .. q-1):
+ *   q_j   = RoPE_j( L2( SiLU( s_q * (P_q x_j) + b_q ) ) )        per head, as the keys
+ *   o_j,e = M_e(q_j,e)                                              the memory, head e
+ *   h_j,e = o_j,e / sqrt(mean(o_j,e^2) + 1e-6) * w_rms,e * SiLU(a_e . x_j + c_e)
+ *   kv_j  = [ h_j W_k^T | h_j W_v^T ]                               the memory token's K and V
+ *   xq       [L][q][d] act_dtype.
+ *   q        0 <= q <= seg_len rounded up to a multiple of 256; q = 0 is a no-op.
+ *   kv       [L][q][2 d_kv] of kv_dtype (MONE_F32 or MONE_BF16): K columns [0, d_kv), V after.
+ * The fast weights are not modified.  The call uses the handle's scratch space, so it must not
+ * overlap with another call on the same handle. */
+int mone_swiglu_read(mone_swiglu* h, const mone_swiglu_reader* rd, const void* xq, int32_t q,
+                     void* kv, int32_t kv_dtype, void* stream);
+
+/* Memory injection into attention for the paper-form memory: exactly mone_memory_attention
+ * (Eq. attn, Eq. std_attn; grouped heads, causal over the query keys and the memory rows) with
+ * the memory rows kv_mem of mone_swiglu_read, for the handle's L layers and activation dtype and
+ * the given d_kv. */
+int mone_swiglu_attention(mone_swiglu* h, int32_t d_kv, const void* qh, const void* kh,
+                          const void* vh, const void* kv_mem, int32_t kv_dtype, int32_t q,
+                          int32_t n_heads, int32_t n_kv_heads, void* out, int32_t out_dtype,
+                          void* stream);
+
 /* Destroy a handle (host memory only).  NULL is accepted. */
 int mone_swiglu_destroy(mone_swiglu* h);
 
@@ -121,7 +157,13 @@ int mone_swiglu_destroy(mone_swiglu* h);
                                   dZ^T, dG^T and the loss partials */
 #define MONE_SW_STAGE_UPD 5    /* the three weight gradients and the update (one launch; with
                                   MONE_OPT_PAPER also the momentum and the row renormalisation) */
-#define MONE_SW_N_STAGES 6
+#define MONE_SW_STAGE_QPROJ 6  /* read: P_q x_q with the affine step and SiLU; the gates */
+#define MONE_SW_STAGE_QKEYS 7  /* read: L2 norm and RoPE of the queries */
+#define MONE_SW_STAGE_QFWD 8   /* read: A = SiLU(Z) * G per head */
+#define MONE_SW_STAGE_QOUT 9   /* read: O = A W_out per head, RMSNorm and gate -> h */
+#define MONE_SW_STAGE_QKV 10   /* read: [h W_k^T | h W_v^T] */
+#define MONE_SW_STAGE_ATTN 11  /* mone_swiglu_attention */
+#define MONE_SW_N_STAGES 12
 
 int mone_swiglu_set_stage_timing(mone_swiglu* h, int32_t max_records);
 int mone_swiglu_stage_times(mone_swiglu* h, double* ms_sum, int32_t* count);

@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -120,6 +121,48 @@ hipError_t launch_gemm(TileShape t, const Spec* specs, int nspec, int layers, co
     default:
       return launch_tiled<E, 64, 256, 1>(specs, nspec, layers, epi, s, tiles_per_layer);
   }
+}
+
+// Memory injection into attention (Eq. attn with Eq. std_attn): validation and the launch of
+// memory_attention_kernel for L layers of K/V width d_kv; one query row per wavefront.  With
+// q = 0 nothing is launched.
+inline int launch_attention(int L, int d_kv, bool act_bf16, const void* qh, const void* kh,
+                            const void* vh, const void* kv_mem, int kv_dtype, int q, int n_heads,
+                            int n_kv_heads, void* out, int out_dtype, hipStream_t s) {
+  if (q < 0) return fail(MONE_EINVAL, "q = %d is negative", q);
+  if ((kv_dtype != MONE_F32 && kv_dtype != MONE_BF16) ||
+      (out_dtype != MONE_F32 && out_dtype != MONE_BF16))
+    return fail(MONE_EINVAL, "kv_dtype and out_dtype must be MONE_F32 or MONE_BF16");
+  if (n_heads < 1 || n_kv_heads < 1 || n_heads % n_kv_heads || d_kv % n_kv_heads)
+    return fail(MONE_EINVAL, "heads: n_heads=%d must be a multiple of n_kv_heads=%d, which "
+                "must divide d_kv=%d", n_heads, n_kv_heads, d_kv);
+  const int dh = d_kv / n_kv_heads;
+  if (dh > 256) return fail(MONE_EUNSUPPORTED, "head width %d above 256", dh);
+  if (q == 0) return MONE_OK;
+  if (!qh || !kh || !vh || !kv_mem || !out)
+    return fail(MONE_EINVAL, "qh, kh, vh, kv_mem and out must be non-NULL");
+  if (!aligned16(qh) || !aligned16(kh) || !aligned16(vh) || !aligned16(kv_mem) || !aligned16(out))
+    return fail(MONE_EINVAL, "qh, kh, vh, kv_mem and out must be 16-byte aligned");
+  const dim3 grid((q + 3) / 4, n_heads, L), block(256);
+  const float scale = 1.0f / std::sqrt((float)dh);
+  const bool kbf = kv_dtype == MONE_BF16, obf = out_dtype == MONE_BF16;
+  // the eight dtype combinations of (activations, memory K/V, output)
+#define MONE_ATTN(EA, EK, EO)                                                                   \
+  memory_attention_kernel<EA, EK, EO><<<grid, block, 0, s>>>(                                  \
+      reinterpret_cast<const EA*>(qh), reinterpret_cast<const EA*>(kh),                         \
+      reinterpret_cast<const EA*>(vh), reinterpret_cast<const EK*>(kv_mem),                     \
+      reinterpret_cast<EO*>(out), q, n_heads, n_kv_heads, dh, d_kv, scale)
+  if (act_bf16) {
+    if (kbf) { if (obf) MONE_ATTN(bf16_t, bf16_t, bf16_t); else MONE_ATTN(bf16_t, bf16_t, float); }
+    else { if (obf) MONE_ATTN(bf16_t, float, bf16_t); else MONE_ATTN(bf16_t, float, float); }
+  } else {
+    if (kbf) { if (obf) MONE_ATTN(float, bf16_t, bf16_t); else MONE_ATTN(float, bf16_t, float); }
+    else { if (obf) MONE_ATTN(float, float, bf16_t); else MONE_ATTN(float, float, float); }
+  }
+#undef MONE_ATTN
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "launch ATTN");
+  return MONE_OK;
 }
 
 // Per-stage timing: each timed launch is bracketed by two HIP events on the launch's stream.

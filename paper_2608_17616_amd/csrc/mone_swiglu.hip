@@ -15,7 +15,11 @@
 //                  [dZ|dG]^T [B][2 d_h][Tp] interleaved rows (A operand of the W_in/W_gate
 //                                          gradients)
 //                  W_ig [B][2 d_h][d_hp], W_out copy [B][d_h][d_hp]  MFMA copies
-//                  RoPE table [Tp][d_h/2] (cos, sin); loss partials; loss [L]
+//                  RoPE table [Tp][d_h/2] (cos, sin); read gates [L][Tp][H]; loss partials;
+//                  loss [L]
+// The read reuses the step's scratch: K' holds the pre-normalisation queries and then the memory
+// tokens h, K the queries, dY0 the hidden activations A (row-major, zero padding) and dA0^T's
+// space the transposed W_out copy.
 //                  paper optimiser (fp32): rates [L][Tp], decay block sums, decay [L],
 //                  initial row norms
 // A segment step, each stage one launch grouped over all layers (PROJ) or all B heads:
@@ -43,7 +47,7 @@ namespace {
 
 struct SwLayout {
   int Tp, dhp, parts_max;
-  size_t kpre, kh, kt, dy, dyt, dat, at, dzgt, wig, woc, rope, loss_part, loss_out;
+  size_t kpre, kh, kt, dy, dyt, dat, at, dzgt, wig, woc, rope, gate, loss_part, loss_out;
   size_t rate, vpart, beta, n_ig, n_out;  // paper optimiser
   size_t total;
 };
@@ -103,6 +107,7 @@ SwLayout make_sw_layout(const mone_swiglu_config* c) {
   L.wig = take(B * 2 * dh * dhp * E);
   L.woc = take(B * dh * dhp * E);
   L.rope = take(Tp * (dh / 2) * 8);
+  L.gate = take(nl * Tp * (size_t)c->n_heads * 4);
   L.loss_part = take(B * (size_t)L.parts_max * 4);
   L.loss_out = take(nl * 4);
   if (c->optimizer == MONE_OPT_PAPER) {
@@ -294,6 +299,110 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
 }
 
 template <typename E>
+int run_sw_read(mone_swiglu* H, const mone_swiglu_reader* rd, const void* xq, int q, void* kv,
+                int kv_bf16, hipStream_t s) {
+  const mone_swiglu_config& c = H->cfg;
+  const SwLayout& Ly = H->lay;
+  const int L = c.n_layers, d = c.d_model, NH = c.n_heads, dh = c.d_head, B = L * NH;
+  const int Tp = Ly.Tp, dhp = Ly.dhp, D = 2 * rd->d_kv;
+  const int qz = (int)round_up(q, 64);
+  E* qpre = H->at<E>(Ly.kpre);  // the queries before normalisation, then the memory tokens h
+  E* kq = H->at<E>(Ly.kh);
+  E* abuf = H->at<E>(Ly.dy);    // A [B][Tp][d_hp]; its padding columns are always zero
+  E* wot = H->at<E>(Ly.dat);    // W_out^T [B][d_h][d_hp]
+  float* gate = H->at<float>(Ly.gate);
+  const TileShape tq = q <= 64 ? TILE_64x256 : TILE_128x128;
+  hipError_t e;
+  // QPROJ: Q' = SiLU(s_q (X_q P_q^T) + b_q); the gates
+  {
+    Spec sp{};
+    sp.part[0].a = opnd(xq, (long long)q * d, d, q);
+    sp.part[0].b = opnd(rd->proj_q, (long long)d * d, d, d);
+    sp.part[0].k_len = d;
+    sp.nparts = 1;
+    sp.m_extent = q;
+    sp.n = d;
+    sp.m_store = -1;
+    sp.n_store = d;
+    EpiSwQproj<E> epi;
+    epi.qpre = qpre; epi.scale = rd->q_scale; epi.shift = rd->q_shift;
+    epi.d = d; epi.Tp = Tp; epi.q = q;
+    H->timer.begin(s);
+    if ((e = launch_gemm<E>(tq, &sp, 1, L, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch QPROJ");
+    sw_gate_kernel<E><<<dim3((q + 3) / 4, L), dim3(256), 0, s>>>(
+        reinterpret_cast<const E*>(xq), q, d, NH, rd->gate_w, rd->gate_b, Tp, gate);
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch gates");
+    H->timer.end(MONE_SW_STAGE_QPROJ, s);
+  }
+  // QKEYS: per-head L2 norm and RoPE at positions 0 .. q-1
+  H->timer.begin(s);
+  sw_keys_kernel<E><<<dim3(qz / 64, NH, L), dim3(256), 0, s>>>(
+      qpre, d, NH, dh, dhp, Tp, H->at<float2>(Ly.rope), kq, H->at<E>(Ly.kt));
+  if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch QKEYS");
+  H->timer.end(MONE_SW_STAGE_QKEYS, s);
+  // QFWD: A = SiLU(Z) * G with [Z | G] = K_q W_ig^T; and the W_out^T copy for QOUT
+  {
+    transpose_kernel<float, E><<<dim3((dh + 63) / 64, (dhp + 63) / 64, B), dim3(256), 0, s>>>(
+        H->w.w_out, (long long)dh * dh, dh, dh, dh, wot, (long long)dh * dhp, dhp, dhp);
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch W_out^T");
+    Spec sp{};
+    sp.part[0].a = opnd(kq, (long long)Tp * dhp, dhp, q);
+    sp.part[0].b = opnd(H->at<E>(Ly.wig), 2LL * dh * dhp, dhp, 2 * dh);
+    sp.part[0].k_len = dhp;
+    sp.nparts = 1;
+    sp.m_extent = q;
+    sp.n = 2 * dh;
+    sp.m_store = -1;
+    sp.n_store = 2 * dh;
+    EpiSwQfwd<E> epi;
+    epi.a = abuf; epi.ls = (long long)Tp * dhp; epi.dhp = dhp;
+    H->timer.begin(s);
+    if ((e = launch_gemm<E>(tq, &sp, 1, B, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch QFWD");
+    H->timer.end(MONE_SW_STAGE_QFWD, s);
+  }
+  // QOUT: O = A W_out per head (64 x 256 tiles: whole rows), RMSNorm and gate -> h
+  {
+    Spec sp{};
+    sp.part[0].a = opnd(abuf, (long long)Tp * dhp, dhp, q);
+    sp.part[0].b = opnd(wot, (long long)dh * dhp, dhp, dh);
+    sp.part[0].k_len = dhp;
+    sp.nparts = 1;
+    sp.m_extent = q;
+    sp.n = dh;
+    sp.m_store = q;
+    sp.n_store = dh;
+    EpiSwQout<E> epi;
+    epi.hout = qpre; epi.rms_w = rd->rms_w; epi.gate = gate;
+    epi.d = d; epi.dh = dh; epi.H = NH; epi.Tp = Tp;
+    H->timer.begin(s);
+    if ((e = launch_tiled<E, 64, 256, 1>(&sp, 1, B, epi, s, nullptr)) != hipSuccess)
+      return hip_fail(e, "launch QOUT");
+    H->timer.end(MONE_SW_STAGE_QOUT, s);
+  }
+  // QKV: [h W_k^T | h W_v^T] into the caller's buffer
+  {
+    Spec sp{};
+    sp.part[0].a = opnd(qpre, (long long)Tp * d, d, q);
+    sp.part[0].b = opnd(rd->w_kv, (long long)D * d, d, D);
+    sp.part[0].k_len = d;
+    sp.nparts = 1;
+    sp.m_extent = q;
+    sp.n = D;
+    sp.m_store = q;
+    sp.n_store = D;
+    EpiSwKv epi;
+    epi.kv = kv; epi.ls = (long long)q * D; epi.D = D; epi.bf16_out = kv_bf16;
+    H->timer.begin(s);
+    if ((e = launch_gemm<E>(tq, &sp, 1, L, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch QKV");
+    H->timer.end(MONE_SW_STAGE_QKV, s);
+  }
+  return MONE_OK;
+}
+
+template <typename E>
 hipError_t build_copies(mone_swiglu* H, hipStream_t s) {
   const mone_swiglu_config& c = H->cfg;
   const SwLayout& Ly = H->lay;
@@ -417,6 +526,52 @@ int mone_swiglu_loss(mone_swiglu* H, float* out_host, void* stream) {
     return hip_fail(e, "copy loss");
   if ((e = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(e, "synchronise");
   return MONE_OK;
+}
+
+int mone_swiglu_read(mone_swiglu* H, const mone_swiglu_reader* rd, const void* xq, int32_t q,
+                     void* kv, int32_t kv_dtype, void* stream) {
+  g_err[0] = 0;
+  if (!H) return fail(MONE_EINVAL, "handle is NULL");
+  if (!rd) return fail(MONE_EINVAL, "reader is NULL");
+  if (q < 0) return fail(MONE_EINVAL, "q = %d is negative", q);
+  if (kv_dtype != MONE_F32 && kv_dtype != MONE_BF16)
+    return fail(MONE_EINVAL, "kv_dtype %d is not MONE_F32 or MONE_BF16", kv_dtype);
+  if (rd->d_kv < 1) return fail(MONE_EINVAL, "d_kv = %d must be >= 1", rd->d_kv);
+  if (rd->d_kv % 64) return fail(MONE_EUNSUPPORTED, "d_kv must be a multiple of 64");
+  if (2LL * rd->d_kv * H->cfg.d_model * (H->cfg.act_dtype == MONE_BF16 ? 2 : 4) >= (1LL << 31))
+    return fail(MONE_EUNSUPPORTED, "a per-layer matrix exceeds 2^31 bytes");
+  if (q > H->lay.Tp)
+    return fail(MONE_EUNSUPPORTED, "q = %d above %d (seg_len rounded up to 256)", q, H->lay.Tp);
+  if (!rd->proj_q || !rd->q_scale || !rd->q_shift || !rd->rms_w || !rd->gate_w || !rd->gate_b ||
+      !rd->w_kv)
+    return fail(MONE_EINVAL, "every pointer of the reader must be non-NULL");
+  if (!aligned16(rd->proj_q) || !aligned16(rd->q_scale) || !aligned16(rd->q_shift) ||
+      !aligned16(rd->rms_w) || !aligned16(rd->gate_w) || !aligned16(rd->w_kv))
+    return fail(MONE_EINVAL, "proj_q, q_scale, q_shift, rms_w, gate_w and w_kv must be "
+                "16-byte aligned");
+  if (q == 0) return MONE_OK;
+  if (!xq || !kv) return fail(MONE_EINVAL, "xq and kv must be non-NULL");
+  if (!aligned16(xq) || !aligned16(kv)) return fail(MONE_EINVAL, "xq and kv must be 16-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int kvb = kv_dtype == MONE_BF16 ? 1 : 0;
+  return H->cfg.act_dtype == MONE_BF16 ? run_sw_read<bf16_t>(H, rd, xq, q, kv, kvb, s)
+                                       : run_sw_read<float>(H, rd, xq, q, kv, kvb, s);
+}
+
+int mone_swiglu_attention(mone_swiglu* H, int32_t d_kv, const void* qh, const void* kh,
+                          const void* vh, const void* kv_mem, int32_t kv_dtype, int32_t q,
+                          int32_t n_heads, int32_t n_kv_heads, void* out, int32_t out_dtype,
+                          void* stream) {
+  g_err[0] = 0;
+  if (!H) return fail(MONE_EINVAL, "handle is NULL");
+  if (d_kv < 1) return fail(MONE_EINVAL, "d_kv = %d must be >= 1", d_kv);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const bool timed = q > 0;
+  if (timed) H->timer.begin(s);
+  const int rc = launch_attention(H->cfg.n_layers, d_kv, H->cfg.act_dtype == MONE_BF16, qh, kh,
+                                  vh, kv_mem, kv_dtype, q, n_heads, n_kv_heads, out, out_dtype, s);
+  if (rc == MONE_OK && timed) H->timer.end(MONE_SW_STAGE_ATTN, s);
+  return rc;
 }
 
 int mone_swiglu_destroy(mone_swiglu* H) {

@@ -529,45 +529,14 @@ int mone_memory_attention(mone_ttl* H, const void* qh, const void* kh, const voi
                           int32_t n_kv_heads, void* out, int32_t out_dtype, void* stream) {
   g_err[0] = 0;
   if (!H) return fail(MONE_EINVAL, "handle is NULL");
-  if (q < 0) return fail(MONE_EINVAL, "q = %d is negative", q);
-  if ((kv_dtype != MONE_F32 && kv_dtype != MONE_BF16) ||
-      (out_dtype != MONE_F32 && out_dtype != MONE_BF16))
-    return fail(MONE_EINVAL, "kv_dtype and out_dtype must be MONE_F32 or MONE_BF16");
-  const int d_kv = H->cfg.d_kv;
-  if (n_heads < 1 || n_kv_heads < 1 || n_heads % n_kv_heads || d_kv % n_kv_heads)
-    return fail(MONE_EINVAL, "heads: n_heads=%d must be a multiple of n_kv_heads=%d, which "
-                "must divide d_kv=%d", n_heads, n_kv_heads, d_kv);
-  const int dh = d_kv / n_kv_heads;
-  if (dh > 256) return fail(MONE_EUNSUPPORTED, "head width %d above 256", dh);
-  if (q == 0) return MONE_OK;
-  if (!qh || !kh || !vh || !kv_mem || !out)
-    return fail(MONE_EINVAL, "qh, kh, vh, kv_mem and out must be non-NULL");
-  if (!aligned16(qh) || !aligned16(kh) || !aligned16(vh) || !aligned16(kv_mem) || !aligned16(out))
-    return fail(MONE_EINVAL, "qh, kh, vh, kv_mem and out must be 16-byte aligned");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const dim3 grid((q + 3) / 4, n_heads, H->cfg.n_layers), block(256);
-  const float scale = 1.0f / std::sqrt((float)dh);
-  const bool abf = H->cfg.act_dtype == MONE_BF16;
-  const bool kbf = kv_dtype == MONE_BF16, obf = out_dtype == MONE_BF16;
-  H->timing_begin(MONE_STAGE_ATTN, s);
-  // the eight dtype combinations of (activations, memory K/V, output)
-#define MONE_ATTN(EA, EK, EO)                                                                   \
-  memory_attention_kernel<EA, EK, EO><<<grid, block, 0, s>>>(                                  \
-      reinterpret_cast<const EA*>(qh), reinterpret_cast<const EA*>(kh),                         \
-      reinterpret_cast<const EA*>(vh), reinterpret_cast<const EK*>(kv_mem),                     \
-      reinterpret_cast<EO*>(out), q, n_heads, n_kv_heads, dh, d_kv, scale)
-  if (abf) {
-    if (kbf) { if (obf) MONE_ATTN(bf16_t, bf16_t, bf16_t); else MONE_ATTN(bf16_t, bf16_t, float); }
-    else { if (obf) MONE_ATTN(bf16_t, float, bf16_t); else MONE_ATTN(bf16_t, float, float); }
-  } else {
-    if (kbf) { if (obf) MONE_ATTN(float, bf16_t, bf16_t); else MONE_ATTN(float, bf16_t, float); }
-    else { if (obf) MONE_ATTN(float, float, bf16_t); else MONE_ATTN(float, float, float); }
-  }
-#undef MONE_ATTN
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return hip_fail(e, "launch ATTN");
-  H->timing_end(MONE_STAGE_ATTN, s);
-  return MONE_OK;
+  const bool timed = q > 0;
+  if (timed) H->timing_begin(MONE_STAGE_ATTN, s);
+  const int rc = launch_attention(H->cfg.n_layers, H->cfg.d_kv, H->cfg.act_dtype == MONE_BF16,
+                                  qh, kh, vh, kv_mem, kv_dtype, q, n_heads, n_kv_heads, out,
+                                  out_dtype, s);
+  if (rc == MONE_OK && timed) H->timing_end(MONE_STAGE_ATTN, s);
+  return rc;
 }
 
 int mone_ttl_loss(mone_ttl* H, float* out_host, void* stream) {

@@ -218,6 +218,139 @@ struct EpiSwUpd : EpiBase {
   }
 };
 
+// ---- the read (Eq. read, Eq. attn) --------------------------------------------------------
+
+// Four consecutive elements (p 8-byte aligned for bf16, 16-byte for fp32).
+__device__ __forceinline__ void store4(float* p, const float (&v)[4]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void store4(bf16_t* p, const float (&v)[4]) {
+  uint2 w;
+  w.x = pack_bf16(v[0], v[1]);
+  w.y = pack_bf16(v[2], v[3]);
+  *reinterpret_cast<uint2*>(p) = w;
+}
+
+// QPROJ: tile of X_q P_q^T [q][d]: SiLU(s_q r + b_q) per channel -> Q' [L][Tp][d] (rows >= q
+// stored as 0), which the KEYS kernel normalises and rotates like the keys.
+template <typename E>
+struct EpiSwQproj : EpiBase {
+  E* qpre;
+  const float* scale; const float* shift;  // [L][d]
+  int d, Tp, q;
+  __device__ __forceinline__ float rows8(int, int l, int row, int col, int, int, float (&v)[8],
+                                         const float (&)[8]) const {
+    const float* sc = scale + (long long)l * d + col;
+    const float* sh = shift + (long long)l * d + col;
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float u = sc[e] * v[e] + sh[e];
+      o[e] = row < q ? u * sigmoidf_(u) : 0.0f;
+    }
+    store8(qpre + ((long long)l * Tp + row) * d + col, o);
+    return 0.0f;
+  }
+};
+
+// QFWD: tile of [Z | G] = K_q W_ig^T [q][2 d_h] for one head; z_i and g_i are adjacent columns
+// (W_ig interleaves the rows of W_in and W_gate), so a row chunk holds 4 hidden units:
+// A = SiLU(z) g -> A [B][Tp][d_hp] (columns < d_h).
+template <typename E>
+struct EpiSwQfwd : EpiBase {
+  E* a;
+  long long ls;  // Tp * d_hp
+  int dhp;
+  __device__ __forceinline__ float rows8(int, int b, int row, int col, int, int, float (&v)[8],
+                                         const float (&)[8]) const {
+    float av[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) av[p] = v[2 * p] * sigmoidf_(v[2 * p]) * v[2 * p + 1];
+    store4(a + (long long)b * ls + (long long)row * dhp + col / 2, av);
+    return 0.0f;
+  }
+};
+
+// QOUT: tile of Y = A W_out [q][d_h] for one head, on 64 x 256 tiles so that a workgroup holds
+// whole rows: the scale pass forms the memory token h = y / sqrt(mean(y^2) + 1e-6) * w_rms *
+// gate -> H [L][Tp][d] at the head's columns.
+template <typename E>
+struct EpiSwQout : EpiBase {
+  static constexpr bool kWriteback = true;
+  static constexpr bool kRowScale = true;
+  E* hout;
+  const float* rms_w;  // [L][d]
+  const float* gate;   // [L][Tp][H]
+  int d, dh, H, Tp;
+  __device__ __forceinline__ float rows8(int, int, int, int, int, int, float (&v)[8],
+                                         const float (&)[8]) const {
+    float ss = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += v[e] * v[e];
+    return ss;
+  }
+  __device__ __forceinline__ void scale8(int, int b, int row, int col, float ss,
+                                         const float (&v)[8]) const {
+    const int l = b / H, e = b - l * H;
+    const float r = rsqrtf(ss / (float)dh + 1e-6f);
+    const float g = gate[((long long)l * Tp + row) * H + e];
+    const float* w = rms_w + (long long)l * d + (long long)e * dh + col;
+    float o[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = v[i] * r * w[i] * g;
+    store8(hout + ((long long)l * Tp + row) * d + (long long)e * dh + col, o);
+  }
+};
+
+// QKV: tile of H [W_k ; W_v]^T [q][2 d_kv]: the memory tokens in the backbone's key/value space,
+// stored into the caller's [L][q][2 d_kv] (fp32 or bf16), rows < q.
+struct EpiSwKv : EpiBase {
+  void* kv;
+  long long ls;  // q * 2 d_kv
+  int D;
+  int bf16_out;
+  __device__ __forceinline__ float rows8(int, int l, int row, int col, int M, int,
+                                         float (&v)[8], const float (&)[8]) const {
+    if (row >= M) return 0.0f;
+    const long long o = (long long)l * ls + (long long)row * D + col;
+    if (bf16_out)
+      store8(reinterpret_cast<bf16_t*>(kv) + o, v);
+    else
+      store8(reinterpret_cast<float*>(kv) + o, v);
+    return 0.0f;
+  }
+};
+
+// Gates of the memory tokens: gate[l][j][e] = SiLU(a_{l,e} . x_j + c_{l,e}).  One wave per
+// token (fixed-order reduction); grid (ceil(q / 4), L), 256 threads.
+template <typename E>
+__global__ __launch_bounds__(256) void sw_gate_kernel(const E* __restrict__ xq, int q, int d,
+                                                      int H, const float* __restrict__ gw,
+                                                      const float* __restrict__ gb, int Tp,
+                                                      float* __restrict__ gate) {
+  const int l = blockIdx.y, j = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (j >= q) return;
+  const E* row = xq + ((long long)l * q + j) * d;
+  for (int e = 0; e < H; ++e) {
+    const float* w = gw + ((long long)l * H + e) * d;
+    float s = 0.0f;
+    for (int c = lane * 8; c < d; c += 64 * 8) {
+      float x[8], u[8];
+      load8(row + c, x);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) u[i] = w[c + i];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += x[i] * u[i];
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    if (lane == 0) {
+      const float z = s + gb[(long long)l * H + e];
+      gate[((long long)l * Tp + j) * H + e] = z * sigmoidf_(z);
+    }
+  }
+}
+
 // RoPE table: tab[p][c] = (cos, sin) of p * base^(-2c/d_h) for positions p < Tp and channel
 // pairs c < d_h / 2, evaluated in double precision.
 __global__ void sw_rope_table_kernel(float2* __restrict__ tab, int Tp, int dh, double base) {

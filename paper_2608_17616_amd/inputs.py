@@ -19,6 +19,12 @@ Paper-form (SwiGLU per head) memory, per layer:
   P_k, P_v ~ N(0, 1/d)   key and value projections, stacked as [P_k; P_v], shape [2d, d]
   s = 1 + 0.1 N(0, 1), b = 0.1 N(0, 1)    the keys' per-channel affine step, shape [d] each
   W_in, W_gate, W_out ~ N(0, 1/d_h)       fast weights, shape [H, d_h, d_h] each
+Read of the paper-form memory, per layer:
+  P_q ~ N(0, 1/d)                          query projection, shape [d, d]
+  s_q = 1 + 0.1 N(0, 1), b_q = 0.1 N(0, 1) the queries' affine step, shape [d] each
+  w_rms = 1 + 0.1 N(0, 1)                  RMSNorm weight, shape [d]
+  a ~ N(0, 1/d), c = 0.1 N(0, 1)           gate vectors [H, d] and biases [H]
+  W_k, W_v ~ N(0, 1/d)                     the backbone's key/value maps, [2 d_kv, d]
 Meta-parameters of the paper's optimiser (trained offline in the paper; synthetic here):
   u, v ~ N(0, 1/d)       rate and decay projections, shape [d] each
   b_u = log(e - 1)       so that softplus(b_u) = 1: rates average about lr
@@ -30,6 +36,7 @@ import numpy as np
 
 KIND_WK, KIND_WV, KIND_W1, KIND_W2, KIND_X, KIND_XQ, KIND_U, KIND_V = range(8)
 KIND_PK, KIND_PV, KIND_KSCALE, KIND_KSHIFT, KIND_WIN, KIND_WGATE, KIND_WOUT = range(8, 15)
+KIND_PQ, KIND_QSCALE, KIND_QSHIFT, KIND_RMSW, KIND_GATEW, KIND_GATEB, KIND_BWK, KIND_BWV = range(15, 23)
 B_U = float(np.log(np.e - 1.0))
 B_V = 0.0
 
@@ -112,6 +119,20 @@ def sw_layer_fast(cfg, layer: int):
     shape, std = (cfg.n_heads, cfg.d_head, cfg.d_head), 1.0 / np.sqrt(cfg.d_head)
     return tuple(normal(cfg.seed, k, layer, 0, shape, std)
                  for k in (KIND_WIN, KIND_WGATE, KIND_WOUT))
+
+
+def sw_layer_reader(cfg, layer: int, d_kv: int) -> dict:
+    """The read's frozen parameters of one layer of the paper-form memory (float32; the
+    projections bf16-representable in bf16 mode)."""
+    d, H, sd = cfg.d_model, cfg.n_heads, 1.0 / np.sqrt(cfg.d_model)
+    r = lambda kind, shape, std: normal(cfg.seed, kind, layer, 0, shape, std)  # noqa: E731
+    wk, wv = r(KIND_BWK, (d_kv, d), sd), r(KIND_BWV, (d_kv, d), sd)
+    return dict(p_q=act_round(r(KIND_PQ, (d, d), sd), cfg.act_dtype),
+                q_scale=(1.0 + r(KIND_QSCALE, (d,), 0.1)).astype(np.float32),
+                q_shift=r(KIND_QSHIFT, (d,), 0.1),
+                rms_w=(1.0 + r(KIND_RMSW, (d,), 0.1)).astype(np.float32),
+                gate_w=r(KIND_GATEW, (H, d), sd), gate_b=r(KIND_GATEB, (H,), 0.1),
+                w_kv=act_round(np.concatenate([wk, wv], axis=0), cfg.act_dtype))
 
 
 def segment_x(cfg, layer: int, s: int, n_tokens: int | None = None) -> np.ndarray:

@@ -23,7 +23,8 @@ MONE_OPT_SGD, MONE_OPT_PAPER = 0, 1
 STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2", "rate", "renorm", "attn")
 MONE_N_STAGES = len(STAGES)
 
-SW_STAGES = ("rate", "proj", "keys", "da", "fwd", "upd")
+SW_STAGES = ("rate", "proj", "keys", "da", "fwd", "upd", "qproj", "qkeys", "qfwd", "qout", "qkv",
+             "attn")
 MONE_SW_N_STAGES = len(SW_STAGES)
 
 # every symbol include/mone_ttl.h and include/mone_swiglu.h declare
@@ -32,8 +33,8 @@ EXPORTS = ("mone_ttl_workspace_bytes", "mone_ttl_init", "mone_ttl_init_paper",
            "mone_ttl_loss", "mone_ttl_destroy", "mone_ttl_last_error",
            "mone_ttl_set_stage_timing", "mone_ttl_stage_times",
            "mone_swiglu_workspace_bytes", "mone_swiglu_init", "mone_swiglu_segment",
-           "mone_swiglu_loss", "mone_swiglu_destroy", "mone_swiglu_set_stage_timing",
-           "mone_swiglu_stage_times")
+           "mone_swiglu_loss", "mone_swiglu_read", "mone_swiglu_attention",
+           "mone_swiglu_destroy", "mone_swiglu_set_stage_timing", "mone_swiglu_stage_times")
 
 
 class MoneError(RuntimeError):
@@ -81,6 +82,13 @@ class mone_swiglu_optimizer(ctypes.Structure):
                 ("mom_out", ctypes.c_void_p)]
 
 
+class mone_swiglu_reader(ctypes.Structure):
+    _fields_ = [("proj_q", ctypes.c_void_p), ("q_scale", ctypes.c_void_p),
+                ("q_shift", ctypes.c_void_p), ("rms_w", ctypes.c_void_p),
+                ("gate_w", ctypes.c_void_p), ("gate_b", ctypes.c_void_p),
+                ("w_kv", ctypes.c_void_p), ("d_kv", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -119,6 +127,10 @@ def lib() -> ctypes.CDLL:
                                        vp]
         L.mone_swiglu_segment.argtypes = [vp, vp, i32, vp]
         L.mone_swiglu_loss.argtypes = [vp, ctypes.POINTER(ctypes.c_float), vp]
+        L.mone_swiglu_read.argtypes = [vp, ctypes.POINTER(mone_swiglu_reader), vp, i32, vp, i32,
+                                       vp]
+        L.mone_swiglu_attention.argtypes = [vp, i32, vp, vp, vp, vp, i32, i32, i32, i32, vp, i32,
+                                            vp]
         L.mone_swiglu_destroy.argtypes = [vp]
         L.mone_swiglu_set_stage_timing.argtypes = [vp, i32]
         L.mone_swiglu_stage_times.argtypes = [vp, ctypes.POINTER(ctypes.c_double),
@@ -334,6 +346,28 @@ def mone_swiglu_loss(handle: int, n_layers: int, stream=None) -> list[float]:
     return list(out)
 
 
+def swiglu_reader(proj_q, q_scale, q_shift, rms_w, gate_w, gate_b, w_kv,
+                  d_kv: int) -> mone_swiglu_reader:
+    """C struct of the read's frozen parameters (device tensors or raw addresses)."""
+    return mone_swiglu_reader(*(_ptr(t) for t in (proj_q, q_scale, q_shift, rms_w, gate_w,
+                                                   gate_b, w_kv)), int(d_kv))
+
+
+def mone_swiglu_read(handle: int, reader: mone_swiglu_reader, xq, q: int, kv, kv_dtype: int,
+                     stream=None) -> None:
+    _check(lib().mone_swiglu_read(handle, ctypes.byref(reader) if reader is not None else None,
+                                  _ptr(xq), int(q), _ptr(kv), int(kv_dtype), _stream(stream)))
+
+
+def mone_swiglu_attention(handle: int, d_kv: int, qh, kh, vh, kv_mem, kv_dtype: int, q: int,
+                          n_heads: int, n_kv_heads: int, out, out_dtype: int,
+                          stream=None) -> None:
+    _check(lib().mone_swiglu_attention(handle, int(d_kv), _ptr(qh), _ptr(kh), _ptr(vh),
+                                       _ptr(kv_mem), int(kv_dtype), int(q), int(n_heads),
+                                       int(n_kv_heads), _ptr(out), int(out_dtype),
+                                       _stream(stream)))
+
+
 def mone_swiglu_destroy(handle: int) -> None:
     _check(lib().mone_swiglu_destroy(handle))
 
@@ -377,6 +411,13 @@ class SwigluSession:
 
     def loss(self, stream=None):
         return mone_swiglu_loss(self.handle, self.cfg.n_layers, stream)
+
+    def read(self, reader: mone_swiglu_reader, xq, kv, stream=None):
+        """Memory K/V rows kv [L, q, 2 d_kv] (fp32 or bf16 tensor) of query inputs xq."""
+        import torch
+        dt = MONE_BF16 if kv.dtype == torch.bfloat16 else MONE_F32
+        mone_swiglu_read(self.handle, reader, xq, xq.shape[1], kv, dt, stream)
+        return kv
 
     def close(self):
         if self.handle:

@@ -168,11 +168,11 @@ def test_swiglu_workspace_formula():
     n = mone.mone_swiglu_workspace_bytes(c)
     L, d, H, dh, dhp, Tp, E = 2, 192, 2, 96, 128, 512, 2
     B = L * H
-    act = (L * Tp * 2 * d * 4 + E * B * (2 * Tp * dhp + 4 * dh * Tp + 2 * dh * Tp
-                                         + 3 * dh * dhp) + Tp * (dh // 2) * 8)
+    act = (E * L * Tp * d + E * B * (2 * Tp * dhp + 4 * dh * Tp + 2 * dh * Tp + 3 * dh * dhp)
+           + Tp * (dh // 2) * 8 + 4 * L * Tp * H)
     assert act <= n <= act + 64 * 1024
     p = mone.mone_swiglu_workspace_bytes(_swcfg(optimizer="paper"))
-    extra = 4 * (L * Tp + L * (Tp // 16) + L + 3 * B * dh + 3 * B * dh * 2)
+    extra = 4 * (L * Tp + L * (Tp // 16) + L + 3 * B * dh)
     assert extra <= p - n <= extra + 8 * 256
     # the context length is not a parameter of any call
     for cfg in configs.SW_CONFIGS.values():
@@ -246,3 +246,7 @@ def test_swiglu_null_handle_calls_fail_cleanly():
     ms = (ctypes.c_double * mone.MONE_SW_N_STAGES)()
     cnt = (ctypes.c_int32 * mone.MONE_SW_N_STAGES)()
     assert L.mone_swiglu_stage_times(None, ms, cnt) == mone.MONE_EINVAL
+    rd = mone.mone_swiglu_reader(16, 16, 16, 16, 16, 16, 16, 64)
+    assert L.mone_swiglu_read(None, ctypes.byref(rd), 16, 1, 16, 0, None) == mone.MONE_EINVAL
+    assert L.mone_swiglu_attention(None, 64, 16, 16, 16, 16, 0, 4, 4, 2, 16, 0,
+                                   None) == mone.MONE_EINVAL

@@ -160,3 +160,86 @@ def test_empty_segment_is_a_no_op_and_loss_needs_a_segment():
     torch.cuda.synchronize()
     for w, w0 in zip(p.w, p.w0):
         assert torch.equal(w, w0)
+
+
+# ---------------------------------------------------------------- the read and attention
+
+def _reader(p, d_kv):
+    cfg = p.cfg
+    rds = [inputs.sw_layer_reader(cfg, l, d_kv) for l in range(cfg.n_layers)]
+    dev = {k: torch.from_numpy(np.stack([r[k] for r in rds])).to("cuda") for k in rds[0]}
+    dev["p_q"] = dev["p_q"].to(p.act)
+    dev["w_kv"] = dev["w_kv"].to(p.act)
+    c = mone.swiglu_reader(dev["p_q"], dev["q_scale"], dev["q_shift"], dev["rms_w"],
+                           dev["gate_w"], dev["gate_b"], dev["w_kv"], d_kv)
+    return rds, dev, c
+
+
+@pytest.mark.parametrize("case", ["f32_sgd", "bf16_paper", "paper_shape"])
+def test_read_and_attention(case):
+    """mone_swiglu_read at the GPU's current weights against the oracle's read on the same
+    weights (and, end to end, on the oracle's own weights), then mone_swiglu_attention with
+    those memory rows against the attention oracle."""
+    import oracle as orc
+    if case == "paper_shape":
+        cfg, d_kv, q, hq, hkv, layers = configs.SW_PAPER, 128, 64, 14, 2, [0, 23]
+    else:
+        cfg = configs.SW_TINY.with_(act_dtype="f32" if case == "f32_sgd" else "bf16",
+                                    optimizer="sgd" if case == "f32_sgd" else "paper")
+        d_kv, q, hq, hkv, layers = 64, 50, 4, 1, [0, 1]
+    tol = 1e-4 if cfg.act_dtype == "f32" else 2e-2
+    p = SwProblem(cfg)
+    for s in range(2):
+        p.segment(s, cfg.seg_len)
+    rds, dev, crd = _reader(p, d_kv)
+    L, d = cfg.n_layers, cfg.d_model
+    xq_h = [inputs.query_x(cfg, l, q) for l in range(L)]
+    xq = torch.from_numpy(np.stack(xq_h)).to("cuda", p.act)
+    kv = torch.empty(L, q, 2 * d_kv, dtype=torch.float32, device="cuda")
+    p.sess.read(crd, xq, kv)
+    rng = np.random.default_rng(5)
+    dh = d_kv // hkv
+    att = [rng.standard_normal((L, q, w)).astype(np.float32) for w in (hq * dh, hkv * dh,
+                                                                        hkv * dh)]
+    qh, kh, vh = (torch.from_numpy(a).to("cuda", p.act) for a in att)
+    out = torch.empty(L, q, hq * dh, dtype=torch.float32, device="cuda")
+    mone.mone_swiglu_attention(p.sess.handle, d_kv, qh, kh, vh, kv, mone.MONE_F32, q, hq, hkv,
+                               out, mone.MONE_F32)
+    torch.cuda.synchronize()
+    got_w = [w.cpu().numpy().astype(np.float64) for w in p.w]
+    kv_h = kv.cpu().numpy().astype(np.float64)
+    out_h = out.cpu().numpy().astype(np.float64)
+    att_h = [torch.from_numpy(a).to(p.act).float().numpy().astype(np.float64) for a in att]
+    errs = {}
+    for l in layers:
+        fast_gpu = tuple(w[l] for w in got_w)
+        h = sw.memory_tokens(xq_h[l], fast_gpu, rds[l], cfg.n_heads, cfg.rope_base)
+        want = sw.memory_kv(h, rds[l]["w_kv"])
+        errs[f"kv[{l}]"] = rel_l2(kv_h[l], want)
+        fast_orc, _, _ = p.oracle(l)
+        h2 = sw.memory_tokens(xq_h[l], fast_orc, rds[l], cfg.n_heads, cfg.rope_base)
+        errs[f"kv_end_to_end[{l}]"] = rel_l2(kv_h[l], sw.memory_kv(h2, rds[l]["w_kv"]))
+        want_out = orc.memory_attention(att_h[0][l], att_h[1][l], att_h[2][l], want, hq, hkv)
+        errs[f"attn[{l}]"] = rel_l2(out_h[l], want_out)
+    bad = {k: v for k, v in errs.items() if v > tol}
+    assert not bad, f"{bad} (all: {errs})"
+
+
+def test_read_argument_checks():
+    cfg = configs.SW_TINY
+    p = SwProblem(cfg)
+    _, _, crd = _reader(p, 64)
+    kv = torch.empty(cfg.n_layers, 4, 128, device="cuda")
+    xq = torch.zeros(cfg.n_layers, 4, cfg.d_model, device="cuda")
+    with pytest.raises(mone.MoneError) as ei:
+        mone.mone_swiglu_read(p.sess.handle, crd, xq, 257, kv, mone.MONE_F32)
+    assert ei.value.code == mone.MONE_EUNSUPPORTED  # above seg_len rounded up to 256
+    bad = mone.mone_swiglu_reader(crd.proj_q, crd.q_scale, crd.q_shift, crd.rms_w, crd.gate_w,
+                                  crd.gate_b, crd.w_kv, 96)
+    with pytest.raises(mone.MoneError) as ei:
+        mone.mone_swiglu_read(p.sess.handle, bad, xq, 4, kv, mone.MONE_F32)
+    assert ei.value.code == mone.MONE_EUNSUPPORTED
+    with pytest.raises(mone.MoneError) as ei:
+        mone.mone_swiglu_read(p.sess.handle, None, xq, 4, kv, mone.MONE_F32)
+    assert ei.value.code == mone.MONE_EINVAL
+    mone.mone_swiglu_read(p.sess.handle, crd, None, 0, None, mone.MONE_F32)  # q = 0: no-op
