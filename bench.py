@@ -11,8 +11,10 @@ The context is resident in HBM before timing starts (64 distinct segments, 32 Gi
 are seeded synthetic Gaussians: x ~ N(0, 1), W_k, W_v, W1 ~ N(0, 1/d), W2 ~ N(0, 1/h), drawn
 on the GPU with torch's generator.
 
-Prints one JSON line.  Per-stage kernel durations come from HIP events the library records on
-the launch stream around every stage during the timed steps.  The CPU baseline times the CPU
+Prints one JSON line.  Kernel durations come from HIP events the library records on the launch
+stream: around every stage during one untimed profiling step after the warmup ("stages"), and
+around the dominant stage only during the timed steps ("roofline"), so that event records between
+the other kernels do not slow the timed work.  The CPU baseline times the CPU
 oracle (float64 NumPy, as it stands) on one layer over as many segments as fit in about
 --cpu-seconds, scaled to all layers.
 """
@@ -78,11 +80,11 @@ def stage_work(cfg, q):
     }
 
 
-def counted_traffic(stage):
-    """Per-launch HBM bytes of `stage` from the committed counter summary, or None when the
-    kernel sources have changed since the counters were taken."""
+def counted_traffic(stage, record="hbm_traffic_8b.json"):
+    """Per-launch HBM bytes of `stage` from a committed counter summary under profiles/, or
+    None when the kernel sources have changed since the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "hbm_traffic_8b.json")
+    path = os.path.join(ROOT, "profiles", record)
     try:
         with open(path) as f:
             rec = json.load(f)
@@ -153,6 +155,71 @@ def sw_stage_work(cfg):
         "fwd": (B * 2 * T * 2 * dh * dh, B * (2 * dh * dh + 5 * T * dh) * E + L * T * 4),
         "upd": (B * 2 * T * 3 * dh * dh, B * (5 * dh * T * E + upd_w)),
     }
+
+
+def sw_read_work(cfg, q, d_kv, hq, hkv):
+    """Algorithmic FLOPs and bytes of the read's stages (all layers and heads; q query tokens;
+    attention with hq query heads and hkv key/value heads of width d_kv / hkv)."""
+    L, d, H, dh = cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.d_head
+    E = 2 if cfg.act_dtype == "bf16" else 4
+    B, D, ah = L * H, 2 * d_kv, d_kv // hkv
+    return {
+        "qproj": (L * 2 * q * d * (d + H), L * ((2 * q * d + d * d) * E + H * d * 4)),
+        "qkeys": (0, 3 * L * q * d * E),
+        "qfwd": (B * 2 * q * 2 * dh * dh, B * (2 * q * dh + 2 * dh * dh) * E),
+        "qout": (B * 2 * q * dh * dh, B * (2 * q * dh + dh * dh) * E + B * dh * dh * 4),
+        "qkv": (L * 2 * q * d * D, L * ((q * d + D * d) * E + q * D * 4)),
+        "attn": (L * hq * 2 * (q * (q + 1)) * 2 * ah,
+                 L * q * ((hq + 2 * hkv) * ah * E + D * 4 + hq * ah * 4)),
+    }
+
+
+def roofline(kernel, flops, nbytes, seconds, peak_tflops):
+    """Roofline entry of one launch: the bound is the resource nearest its peak (MFMA for a
+    contraction that keeps the matrix cores busy, HBM for one whose epilogue traffic dominates)."""
+    tf = flops / seconds / 1e12
+    gb = nbytes / seconds / 1e9
+    if flops > 0 and tf / peak_tflops >= gb / PEAK_HBM_GBS:
+        return {"kernel": kernel, "bound": "mfma", "achieved": round(tf, 1), "peak": peak_tflops,
+                "unit": "TFLOP/s", "frac": round(tf / peak_tflops, 4), "traffic": None}
+    return {"kernel": kernel, "bound": "hbm", "achieved": round(gb, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(gb / PEAK_HBM_GBS, 4), "traffic": None}
+
+
+def timed_steps(step, steps, set_timing, stage_times, names, records_per_step):
+    """Run one profiling step with every stage bracketed by HIP events (the per-stage breakdown
+    and the dominant stage), then time exactly `steps` steps with events around the dominant
+    stage only, so that event records between the other kernels do not slow the timed work.
+    Returns (elapsed seconds of the timed steps, per-stage (ms, launches) of the profiling step,
+    dominant stage, its (ms, launches) over the timed steps)."""
+    import torch
+    set_timing(records_per_step, 0xFFFFFFFF)
+    step()
+    torch.cuda.synchronize()
+    prof = stage_times()
+    dom = max((n for n in prof if prof[n][1]), key=lambda n: prof[n][0])
+    set_timing(steps * records_per_step, 1 << names.index(dom))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    return elapsed, prof, dom, stage_times()[dom]
+
+
+def stage_table(stimes, work):
+    """Per-stage average launch time and algorithmic rates."""
+    stages = {}
+    for name, (ms, cnt) in stimes.items():
+        if cnt == 0:
+            continue
+        fl, by = work[name]
+        avg_s = ms / cnt / 1e3
+        stages[name] = {"launches": cnt, "avg_ms": round(ms / cnt, 4),
+                        "tflops": round(fl / avg_s / 1e12, 1),
+                        "gbs": round(by / avg_s / 1e9, 1)}
+    return stages
 
 
 def sw_cpu_baseline(cfg, host, xs, budget_s, meta):
@@ -233,6 +300,31 @@ def run_swiglu(args):
                 k_shift[0].double().cpu().numpy(), tuple(t[0].double().cpu().numpy() for t in w))
         cpu_in = (host, [ctx[s, 0].double().cpu().numpy() for s in range(n_cpu)])
 
+    # the read: Q query tokens through the memory (Qwen2.5-0.5B's attention: 14 query heads and
+    # 2 key/value heads of 64, d_kv = 128), then the memory-injected attention
+    Q, d_kv, hq, hkv = cfg.n_query, 128, 14, 2
+    ah = d_kv // hkv
+    xq = inputs.device_normal_(torch.empty(L, Q, d, dtype=act, device=dev), 1.0, gen)
+    rd = dict(p_q=inputs.device_normal_(torch.empty(L, d, d, dtype=act, device=dev),
+                                        1 / np.sqrt(d), gen),
+              q_scale=inputs.device_normal_(torch.empty(L, d, dtype=f32, device=dev), 0.1,
+                                            gen) + 1.0,
+              q_shift=inputs.device_normal_(torch.empty(L, d, dtype=f32, device=dev), 0.1, gen),
+              rms_w=inputs.device_normal_(torch.empty(L, d, dtype=f32, device=dev), 0.1,
+                                          gen) + 1.0,
+              gate_w=inputs.device_normal_(torch.empty(L, H, d, dtype=f32, device=dev),
+                                           1 / np.sqrt(d), gen),
+              gate_b=inputs.device_normal_(torch.empty(L, H, dtype=f32, device=dev), 0.1, gen),
+              w_kv=inputs.device_normal_(torch.empty(L, 2 * d_kv, d, dtype=act, device=dev),
+                                         1 / np.sqrt(d), gen))
+    crd = mone.swiglu_reader(rd["p_q"], rd["q_scale"], rd["q_shift"], rd["rms_w"],
+                             rd["gate_w"], rd["gate_b"], rd["w_kv"], d_kv)
+    kv = torch.empty(L, Q, 2 * d_kv, dtype=f32, device=dev)
+    aq = inputs.device_normal_(torch.empty(L, Q, hq * ah, dtype=act, device=dev), 1.0, gen)
+    ak = inputs.device_normal_(torch.empty(L, Q, hkv * ah, dtype=act, device=dev), 1.0, gen)
+    av = inputs.device_normal_(torch.empty(L, Q, hkv * ah, dtype=act, device=dev), 1.0, gen)
+    aout = torch.empty(L, Q, hq * ah, dtype=f32, device=dev)
+
     stream = torch.cuda.current_stream(dev)
     sess = mone.SwigluSession(cfg, proj, k_scale, k_shift, *w, opt=opt, stream=stream)
     Hd = sess.handle
@@ -241,47 +333,41 @@ def run_swiglu(args):
     def step():
         for s in range(S):
             mone.mone_swiglu_segment(Hd, ctx[s], T, sptr)
+        mone.mone_swiglu_read(Hd, crd, xq, Q, kv, mone.MONE_F32, sptr)
+        mone.mone_swiglu_attention(Hd, d_kv, aq, ak, av, kv, mone.MONE_F32, Q, hq, hkv, aout,
+                                   mone.MONE_F32, sptr)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    mone.mone_swiglu_set_stage_timing(Hd, args.steps * S * 6)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    stimes = mone.mone_swiglu_stage_times(Hd)
-    finite = all(bool(torch.isfinite(t).all().item()) for t in w)
+    if args.calib_copy_mib:
+        src = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    elapsed, stimes, dom, (dms, dcnt) = timed_steps(
+        step, args.steps, lambda n, m: mone.mone_swiglu_set_stage_timing(Hd, n, m),
+        lambda: mone.mone_swiglu_stage_times(Hd), mone.SW_STAGES, S * 6 + 6)
+    finite = all(bool(torch.isfinite(t).all().item()) for t in w + [kv, aout])
     sess.close()
 
     tokens = args.steps * S * T
     value = tokens / elapsed
     flop_tok = cfg.flops_per_token()
     peak = PEAK_BF16_TFLOPS if cfg.act_dtype == "bf16" else PEAK_F32_TFLOPS
-    work = sw_stage_work(cfg)
-    stages = {}
-    for name, (ms, cnt) in stimes.items():
-        if cnt == 0:
-            continue
-        fl, by = work[name]
-        avg_s = ms / cnt / 1e3
-        stages[name] = {"launches": cnt, "avg_ms": round(ms / cnt, 4),
-                        "tflops": round(fl / avg_s / 1e12, 1),
-                        "gbs": round(by / avg_s / 1e9, 1)}
-    dom = max(stages, key=lambda k: stimes[k][0])
+    work = dict(sw_stage_work(cfg), **sw_read_work(cfg, Q, d_kv, hq, hkv))
+    stages = stage_table(stimes, work)
     dfl, dby = work[dom]
-    davg = stimes[dom][0] / stimes[dom][1] / 1e3
-    if dfl > 0:
-        roof = {"kernel": f"gemm_nt_kernel ({dom})", "bound": "mfma",
-                "achieved": round(dfl / davg / 1e12, 1), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(dfl / davg / 1e12 / peak, 4), "traffic": None}
-    else:
-        roof = {"kernel": {"keys": "sw_keys_kernel", "rate": "rate_kernel"}[dom],
-                "bound": "hbm",
-                "achieved": round(dby / davg / 1e9, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(dby / davg / 1e9 / PEAK_HBM_GBS, 4), "traffic": None}
+    davg = dms / dcnt / 1e3
+    kname = {"keys": "sw_keys_kernel", "rate": "rate_kernel"}.get(dom, f"gemm_nt_kernel ({dom})")
+    roof = roofline(kname, dfl, dby, davg, peak)
+    counted = (counted_traffic(dom, "hbm_traffic_sw_qwen0.5b.json")
+               if cfg.name == "sw_qwen0.5b" and cfg.optimizer == "paper" else None)
+    if counted:
+        roof["traffic"] = counted["read_bytes"] + counted["write_bytes"]
+        roof["traffic_detail"] = dict(counted, algorithmic_bytes=dby,
+                                      source="profiles/hbm_traffic_sw_qwen0.5b.json")
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup,
@@ -289,14 +375,17 @@ def run_swiglu(args):
         "scaling": "weak", "vs_baseline": None, "dtype": cfg.act_dtype, "data": "synthetic",
         "config": {"workload": f"paper-form SwiGLU memory TTL ({cfg.name}): L={L} d={d} "
                                f"H={H} d_h={dh} T={T} N={S * T} ({S} segments), "
-                               f"{'paper optimiser' if cfg.optimizer == 'paper' else 'SGD'}",
+                               f"{'paper optimiser' if cfg.optimizer == 'paper' else 'SGD'}"
+                               f" + read Q={Q} + attention ({hq}/{hkv} heads of {ah})",
                    "n_layers": L, "d_model": d, "n_heads": H, "d_head": dh, "seg_len": T,
-                   "n_context": S * T, "lr": cfg.lr, "optimizer": cfg.optimizer,
-                   "loss": "nip"},
+                   "n_context": S * T, "n_query": Q, "d_kv": d_kv, "lr": cfg.lr,
+                   "optimizer": cfg.optimizer, "loss": "nip"},
         "mfma_pct": round(100.0 * value * flop_tok / (peak * 1e12), 2),
         "flop_per_token": flop_tok,
         "roofline": roof,
         "stages": stages,
+        "stage_timing": "stages: one untimed profiling step, every stage timed; roofline: the "
+                        "dominant stage over the timed steps",
         "finite": finite,
     }
     if cpu_in is not None:
@@ -421,14 +510,9 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    mone.mone_ttl_set_stage_timing(H, args.steps * (S * 7 + 3))
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    stimes = mone.mone_ttl_stage_times(H)
+    elapsed, stimes, dom, (dms, dcnt) = timed_steps(
+        step, args.steps, lambda n, m: mone.mone_ttl_set_stage_timing(H, n, m),
+        lambda: mone.mone_ttl_stage_times(H), mone.STAGES, S * 7 + 3)
     finite = bool(torch.isfinite(w1).all().item() and torch.isfinite(w2).all().item()
                   and torch.isfinite(kv).all().item())
     sess.close()
@@ -439,26 +523,10 @@ def main():
     peak = PEAK_BF16_TFLOPS if cfg.act_dtype == "bf16" else PEAK_F32_TFLOPS
     mfma_pct = 100.0 * value * flop_tok / (peak * 1e12)
     work = stage_work(cfg, Q)
-    stages = {}
-    for name, (ms, cnt) in stimes.items():
-        if cnt == 0:
-            continue
-        fl, by = work[name]
-        avg_s = ms / cnt / 1e3
-        stages[name] = {"launches": cnt, "avg_ms": round(ms / cnt, 4),
-                        "tflops": round(fl / avg_s / 1e12, 1),
-                        "gbs": round(by / avg_s / 1e9, 1)}
-    dom = max(stages, key=lambda k: stimes[k][0])
+    stages = stage_table(stimes, work)
     dfl, dby = work[dom]
-    davg = stimes[dom][0] / stimes[dom][1] / 1e3
-    if dfl > 0:
-        roof = {"kernel": f"gemm_nt_kernel ({dom})", "bound": "mfma",
-                "achieved": round(dfl / davg / 1e12, 1), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(dfl / davg / 1e12 / peak, 4), "traffic": None}
-    else:
-        roof = {"kernel": dom, "bound": "hbm", "achieved": round(dby / davg / 1e9, 1),
-                "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(dby / davg / 1e9 / PEAK_HBM_GBS, 4), "traffic": None}
+    davg = dms / dcnt / 1e3
+    roof = roofline(f"gemm_nt_kernel ({dom})" if dfl > 0 else dom, dfl, dby, davg, peak)
     counted = (counted_traffic(dom) if (args.config == "8b" and cfg.optimizer == "sgd" and S >= 1)
                else None)
     if counted:
@@ -482,6 +550,8 @@ def main():
         "flop_per_token": flop_tok,
         "roofline": roof,
         "stages": stages,
+        "stage_timing": "stages: one untimed profiling step, every stage timed; roofline: the "
+                        "dominant stage over the timed steps",
         "finite": finite,
     }
     if cpu_in is not None:

@@ -165,7 +165,7 @@ int mone_swiglu_destroy(mone_swiglu* h);
 #define MONE_SW_STAGE_ATTN 11  /* mone_swiglu_attention */
 #define MONE_SW_N_STAGES 12
 
-int mone_swiglu_set_stage_timing(mone_swiglu* h, int32_t max_records);
+int mone_swiglu_set_stage_timing(mone_swiglu* h, int32_t max_records, uint32_t stage_mask);
 int mone_swiglu_stage_times(mone_swiglu* h, double* ms_sum, int32_t* count);
 
 #ifdef __cplusplus

@@ -210,11 +210,15 @@ const char* mone_ttl_last_error(void);
 #define MONE_STAGE_ATTN 9  /* mone_memory_attention */
 #define MONE_N_STAGES 10
 
-/* Enable (max_records > 0) or disable (0) per-stage timing: each subsequent stage launch is
+/* Enable (max_records > 0) or disable (0) per-stage timing: each subsequent launch of a stage
+ * whose bit is set in stage_mask (bit i = stage i; MONE_ALL_STAGES for every stage) is
  * bracketed by a pair of HIP events recorded on the call's stream, up to max_records pairs
- * (further launches are not timed).  Creates the events on the current device (host call,
- * no device allocation).  Enabling again discards earlier records. */
-int mone_ttl_set_stage_timing(mone_ttl* h, int32_t max_records);
+ * (further launches are not timed).  The events are created on the current device without a
+ * system-scope fence (timing only: recording them does not write back or invalidate caches
+ * between the timed kernels).  Host call, no device allocation.  Enabling again discards
+ * earlier records. */
+#define MONE_ALL_STAGES 0xffffffffu
+int mone_ttl_set_stage_timing(mone_ttl* h, int32_t max_records, uint32_t stage_mask);
 
 /* Synchronise on the recorded events and report, per stage, the summed elapsed milliseconds
  * (ms_sum, host double[MONE_N_STAGES]) and the number of timed launches (count, host

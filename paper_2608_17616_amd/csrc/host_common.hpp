@@ -166,16 +166,19 @@ inline int launch_attention(int L, int d_kv, bool act_bf16, const void* qh, cons
 }
 
 // Per-stage timing: each timed launch is bracketed by two HIP events on the launch's stream.
+// Only the stages whose bit is set in `mask` are timed (stage i is bit i).
 struct StageTimer {
   std::vector<hipEvent_t> ev;
   std::vector<int> stage;
   int cap = 0, used = 0;
+  uint32_t mask = 0xffffffffu;
 
-  void begin(hipStream_t s) {
-    if (used < cap) (void)hipEventRecord(ev[2 * used], s);
+  bool on(int st) const { return used < cap && ((mask >> st) & 1u); }
+  void begin(int st, hipStream_t s) {
+    if (on(st)) (void)hipEventRecord(ev[2 * used], s);
   }
   void end(int st, hipStream_t s) {
-    if (used < cap) {
+    if (on(st)) {
       (void)hipEventRecord(ev[2 * used + 1], s);
       stage[used] = st;
       ++used;
@@ -187,14 +190,17 @@ struct StageTimer {
     stage.clear();
     cap = used = 0;
   }
-  int enable(int max_records) {
+  int enable(int max_records, uint32_t stage_mask) {
     if (max_records < 0) return fail(MONE_EINVAL, "max_records is negative");
     destroy();
+    mask = stage_mask;
     if (max_records == 0) return MONE_OK;
     ev.assign(2 * (size_t)max_records, nullptr);
     stage.assign((size_t)max_records, 0);
     for (size_t i = 0; i < ev.size(); ++i) {
-      hipError_t e = hipEventCreate(&ev[i]);
+      // timing only: no system-scope fence at each record (no cache writeback and
+      // invalidation between the timed kernels, which would slow the work being timed)
+      hipError_t e = hipEventCreateWithFlags(&ev[i], hipEventDisableSystemFence);
       if (e != hipSuccess) {
         ev.resize(i);
         destroy();

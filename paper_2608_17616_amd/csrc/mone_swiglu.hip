@@ -173,7 +173,7 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
   hipError_t e;
 
   if constexpr (PAPER) {
-    H->timer.begin(s);
+    H->timer.begin(MONE_SW_STAGE_RATE, s);
     rate_kernel<E><<<dim3(Tp / kRateTokens, L), dim3(256), 0, s>>>(
         reinterpret_cast<const E*>(x), lsx, d, n, H->opt.rate_w, H->opt.rate_b, H->opt.decay_w,
         c.lr, rate, Tp, H->at<float>(Ly.vpart));
@@ -199,7 +199,7 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
     epi.kscale = H->fz.k_scale; epi.kshift = H->fz.k_shift; epi.rate = rate;
     epi.lr = c.lr; epi.inv_n = 1.0f / (float)n;
     epi.d = d; epi.dh = dh; epi.dhp = dhp; epi.H = NH; epi.Tp = Tp; epi.n = n;
-    H->timer.begin(s);
+    H->timer.begin(MONE_SW_STAGE_PROJ, s);
     // 128 x 128 tiles (measured faster here than 256 x 256, which leave most CUs idle in
     // their second round); 64-row tiles for short segments
     const TileShape tp = n <= 64 ? TILE_64x256 : TILE_128x128;
@@ -209,7 +209,7 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
   }
   // KEYS: per-token L2 norm per head and RoPE -> K, K^T
   {
-    H->timer.begin(s);
+    H->timer.begin(MONE_SW_STAGE_KEYS, s);
     sw_keys_kernel<E><<<dim3(nz / 64, NH, L), dim3(256), 0, s>>>(
         H->at<E>(Ly.kpre), d, NH, dh, dhp, Tp, H->at<float2>(Ly.rope), kh, ktr);
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch KEYS");
@@ -228,7 +228,7 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
     sp.n_store = -1;
     EpiSwDa<E> epi;
     epi.dat = dat; epi.ls = lhT; epi.Tp = Tp;
-    H->timer.begin(s);
+    H->timer.begin(MONE_SW_STAGE_DA, s);
     if ((e = launch_head_gemm<E>(&sp, 1, B, epi, s)) != hipSuccess)
       return hip_fail(e, "launch DA");
     H->timer.end(MONE_SW_STAGE_DA, s);
@@ -249,7 +249,7 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
     epi.loss_part = H->at<float>(Ly.loss_part); epi.ls = lhT; epi.Tp = Tp; epi.n = n; epi.H = NH;
     epi.parts = 4 * tiles_for(kHeadTile, 2 * dh, n);
     epi.lr = c.lr;
-    H->timer.begin(s);
+    H->timer.begin(MONE_SW_STAGE_FWD, s);
     if ((e = launch_head_gemm<E>(&sp, 1, B, epi, s)) != hipSuccess)
       return hip_fail(e, "launch FWD");
     H->timer.end(MONE_SW_STAGE_FWD, s);
@@ -284,7 +284,7 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
     epi.n_ig = PAPER ? H->at<float>(Ly.n_ig) : nullptr;
     epi.n_out = PAPER ? H->at<float>(Ly.n_out) : nullptr;
     epi.lsw = (long long)dh * dh; epi.dh = dh; epi.dhp = dhp; epi.H = NH;
-    H->timer.begin(s);
+    H->timer.begin(MONE_SW_STAGE_UPD, s);
     // the paper's optimiser renormalises whole rows in the epilogue: 64 x 256 tiles, one
     // workgroup per 64 rows of a head's matrix (d_h <= 256 columns)
     if constexpr (PAPER)
@@ -327,7 +327,7 @@ int run_sw_read(mone_swiglu* H, const mone_swiglu_reader* rd, const void* xq, in
     EpiSwQproj<E> epi;
     epi.qpre = qpre; epi.scale = rd->q_scale; epi.shift = rd->q_shift;
     epi.d = d; epi.Tp = Tp; epi.q = q;
-    H->timer.begin(s);
+    H->timer.begin(MONE_SW_STAGE_QPROJ, s);
     if ((e = launch_gemm<E>(tq, &sp, 1, L, epi, s)) != hipSuccess)
       return hip_fail(e, "launch QPROJ");
     sw_gate_kernel<E><<<dim3((q + 3) / 4, L), dim3(256), 0, s>>>(
@@ -336,7 +336,7 @@ int run_sw_read(mone_swiglu* H, const mone_swiglu_reader* rd, const void* xq, in
     H->timer.end(MONE_SW_STAGE_QPROJ, s);
   }
   // QKEYS: per-head L2 norm and RoPE at positions 0 .. q-1
-  H->timer.begin(s);
+  H->timer.begin(MONE_SW_STAGE_QKEYS, s);
   sw_keys_kernel<E><<<dim3(qz / 64, NH, L), dim3(256), 0, s>>>(
       qpre, d, NH, dh, dhp, Tp, H->at<float2>(Ly.rope), kq, H->at<E>(Ly.kt));
   if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch QKEYS");
@@ -357,7 +357,7 @@ int run_sw_read(mone_swiglu* H, const mone_swiglu_reader* rd, const void* xq, in
     sp.n_store = 2 * dh;
     EpiSwQfwd<E> epi;
     epi.a = abuf; epi.ls = (long long)Tp * dhp; epi.dhp = dhp;
-    H->timer.begin(s);
+    H->timer.begin(MONE_SW_STAGE_QFWD, s);
     if ((e = launch_gemm<E>(tq, &sp, 1, B, epi, s)) != hipSuccess)
       return hip_fail(e, "launch QFWD");
     H->timer.end(MONE_SW_STAGE_QFWD, s);
@@ -376,7 +376,7 @@ int run_sw_read(mone_swiglu* H, const mone_swiglu_reader* rd, const void* xq, in
     EpiSwQout<E> epi;
     epi.hout = qpre; epi.rms_w = rd->rms_w; epi.gate = gate;
     epi.d = d; epi.dh = dh; epi.H = NH; epi.Tp = Tp;
-    H->timer.begin(s);
+    H->timer.begin(MONE_SW_STAGE_QOUT, s);
     if ((e = launch_tiled<E, 64, 256, 1>(&sp, 1, B, epi, s, nullptr)) != hipSuccess)
       return hip_fail(e, "launch QOUT");
     H->timer.end(MONE_SW_STAGE_QOUT, s);
@@ -394,7 +394,7 @@ int run_sw_read(mone_swiglu* H, const mone_swiglu_reader* rd, const void* xq, in
     sp.n_store = D;
     EpiSwKv epi;
     epi.kv = kv; epi.ls = (long long)q * D; epi.D = D; epi.bf16_out = kv_bf16;
-    H->timer.begin(s);
+    H->timer.begin(MONE_SW_STAGE_QKV, s);
     if ((e = launch_gemm<E>(tq, &sp, 1, L, epi, s)) != hipSuccess)
       return hip_fail(e, "launch QKV");
     H->timer.end(MONE_SW_STAGE_QKV, s);
@@ -567,7 +567,7 @@ int mone_swiglu_attention(mone_swiglu* H, int32_t d_kv, const void* qh, const vo
   if (d_kv < 1) return fail(MONE_EINVAL, "d_kv = %d must be >= 1", d_kv);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const bool timed = q > 0;
-  if (timed) H->timer.begin(s);
+  if (timed) H->timer.begin(MONE_SW_STAGE_ATTN, s);
   const int rc = launch_attention(H->cfg.n_layers, d_kv, H->cfg.act_dtype == MONE_BF16, qh, kh,
                                   vh, kv_mem, kv_dtype, q, n_heads, n_kv_heads, out, out_dtype, s);
   if (rc == MONE_OK && timed) H->timer.end(MONE_SW_STAGE_ATTN, s);
@@ -582,10 +582,10 @@ int mone_swiglu_destroy(mone_swiglu* H) {
   return MONE_OK;
 }
 
-int mone_swiglu_set_stage_timing(mone_swiglu* H, int32_t max_records) {
+int mone_swiglu_set_stage_timing(mone_swiglu* H, int32_t max_records, uint32_t stage_mask) {
   g_err[0] = 0;
   if (!H) return fail(MONE_EINVAL, "handle is NULL");
-  return H->timer.enable(max_records);
+  return H->timer.enable(max_records, stage_mask);
 }
 
 int mone_swiglu_stage_times(mone_swiglu* H, double* ms_sum, int32_t* count) {

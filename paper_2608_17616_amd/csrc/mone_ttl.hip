@@ -148,7 +148,7 @@ struct mone_ttl {
   template <typename T>
   T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
 
-  void timing_begin(int, hipStream_t s) { timer.begin(s); }
+  void timing_begin(int stage, hipStream_t s) { timer.begin(stage, s); }
   void timing_end(int stage, hipStream_t s) { timer.end(stage, s); }
 };
 
@@ -576,10 +576,10 @@ int mone_ttl_destroy(mone_ttl* H) {
 
 const char* mone_ttl_last_error(void) { return g_err; }
 
-int mone_ttl_set_stage_timing(mone_ttl* H, int32_t max_records) {
+int mone_ttl_set_stage_timing(mone_ttl* H, int32_t max_records, uint32_t stage_mask) {
   g_err[0] = 0;
   if (!H) return fail(MONE_EINVAL, "handle is NULL");
-  return H->timer.enable(max_records);
+  return H->timer.enable(max_records, stage_mask);
 }
 
 int mone_ttl_stage_times(mone_ttl* H, double* ms_sum, int32_t* count) {

@@ -20,6 +20,7 @@ MONE_OK, MONE_EINVAL, MONE_EUNSUPPORTED, MONE_EHIP, MONE_ESTATE = 0, -1, -2, -3,
 MONE_F32, MONE_BF16 = 0, 1
 MONE_LOSS_MSE_SUM, MONE_LOSS_MSE_MEAN, MONE_LOSS_NIP = 0, 1, 2
 MONE_OPT_SGD, MONE_OPT_PAPER = 0, 1
+MONE_ALL_STAGES = 0xFFFFFFFF
 STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2", "rate", "renorm", "attn")
 MONE_N_STAGES = len(STAGES)
 
@@ -114,7 +115,7 @@ def lib() -> ctypes.CDLL:
         L.mone_ttl_destroy.argtypes = [vp]
         L.mone_ttl_last_error.argtypes = []
         L.mone_ttl_last_error.restype = ctypes.c_char_p
-        L.mone_ttl_set_stage_timing.argtypes = [vp, i32]
+        L.mone_ttl_set_stage_timing.argtypes = [vp, i32, ctypes.c_uint32]
         L.mone_ttl_stage_times.argtypes = [vp, ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_int32)]
         swp = ctypes.POINTER(mone_swiglu_config)
@@ -132,7 +133,7 @@ def lib() -> ctypes.CDLL:
         L.mone_swiglu_attention.argtypes = [vp, i32, vp, vp, vp, vp, i32, i32, i32, i32, vp, i32,
                                             vp]
         L.mone_swiglu_destroy.argtypes = [vp]
-        L.mone_swiglu_set_stage_timing.argtypes = [vp, i32]
+        L.mone_swiglu_set_stage_timing.argtypes = [vp, i32, ctypes.c_uint32]
         L.mone_swiglu_stage_times.argtypes = [vp, ctypes.POINTER(ctypes.c_double),
                                               ctypes.POINTER(ctypes.c_int32)]
         for name in EXPORTS:
@@ -240,8 +241,9 @@ def mone_ttl_destroy(handle: int) -> None:
     _check(lib().mone_ttl_destroy(handle))
 
 
-def mone_ttl_set_stage_timing(handle: int, max_records: int) -> None:
-    _check(lib().mone_ttl_set_stage_timing(handle, int(max_records)))
+def mone_ttl_set_stage_timing(handle: int, max_records: int,
+                              stage_mask: int = MONE_ALL_STAGES) -> None:
+    _check(lib().mone_ttl_set_stage_timing(handle, int(max_records), int(stage_mask)))
 
 
 def mone_ttl_stage_times(handle: int) -> dict:
@@ -372,8 +374,9 @@ def mone_swiglu_destroy(handle: int) -> None:
     _check(lib().mone_swiglu_destroy(handle))
 
 
-def mone_swiglu_set_stage_timing(handle: int, max_records: int) -> None:
-    _check(lib().mone_swiglu_set_stage_timing(handle, int(max_records)))
+def mone_swiglu_set_stage_timing(handle: int, max_records: int,
+                                 stage_mask: int = MONE_ALL_STAGES) -> None:
+    _check(lib().mone_swiglu_set_stage_timing(handle, int(max_records), int(stage_mask)))
 
 
 def mone_swiglu_stage_times(handle: int) -> dict:

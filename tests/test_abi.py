@@ -99,7 +99,7 @@ def test_null_handle_calls_fail_cleanly():
     out = (ctypes.c_float * 1)()
     assert L.mone_ttl_loss(None, out, None) == mone.MONE_EINVAL
     assert L.mone_ttl_destroy(None) == mone.MONE_OK
-    assert L.mone_ttl_set_stage_timing(None, 4) == mone.MONE_EINVAL
+    assert L.mone_ttl_set_stage_timing(None, 4, mone.MONE_ALL_STAGES) == mone.MONE_EINVAL
 
 
 def test_library_is_built_from_the_current_sources():
@@ -242,7 +242,7 @@ def test_swiglu_null_handle_calls_fail_cleanly():
     assert L.mone_swiglu_segment(None, 16, 1, None) == mone.MONE_EINVAL
     assert L.mone_swiglu_loss(None, out, None) == mone.MONE_EINVAL
     assert L.mone_swiglu_destroy(None) == mone.MONE_OK
-    assert L.mone_swiglu_set_stage_timing(None, 4) == mone.MONE_EINVAL
+    assert L.mone_swiglu_set_stage_timing(None, 4, mone.MONE_ALL_STAGES) == mone.MONE_EINVAL
     ms = (ctypes.c_double * mone.MONE_SW_N_STAGES)()
     cnt = (ctypes.c_int32 * mone.MONE_SW_N_STAGES)()
     assert L.mone_swiglu_stage_times(None, ms, cnt) == mone.MONE_EINVAL

@@ -243,3 +243,24 @@ def test_read_argument_checks():
         mone.mone_swiglu_read(p.sess.handle, None, xq, 4, kv, mone.MONE_F32)
     assert ei.value.code == mone.MONE_EINVAL
     mone.mone_swiglu_read(p.sess.handle, crd, None, 0, None, mone.MONE_F32)  # q = 0: no-op
+
+
+def test_stage_timing_and_mask():
+    """Every stage of a step is timed once per segment; with a mask only the masked stage."""
+    cfg = configs.SW_TINY.with_(optimizer="paper")
+    p = SwProblem(cfg)
+    h = p.sess.handle
+    mone.mone_swiglu_set_stage_timing(h, 64)
+    p.segment(0, cfg.seg_len)
+    t = mone.mone_swiglu_stage_times(h)
+    for st in ("rate", "proj", "keys", "da", "fwd", "upd"):
+        assert t[st][1] == 1 and t[st][0] > 0, (st, t[st])
+    assert t["qproj"][1] == 0
+    mone.mone_swiglu_set_stage_timing(h, 64, 1 << mone.SW_STAGES.index("upd"))
+    p.segment(1, cfg.seg_len)
+    p.segment(2, 50)
+    t = mone.mone_swiglu_stage_times(h)
+    assert t["upd"][1] == 2 and all(v[1] == 0 for k, v in t.items() if k != "upd")
+    mone.mone_swiglu_set_stage_timing(h, 0)  # off
+    p.segment(3, cfg.seg_len)
+    assert all(v[1] == 0 for v in mone.mone_swiglu_stage_times(h).values())
