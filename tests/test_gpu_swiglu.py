@@ -103,6 +103,7 @@ def _check(p, layers, tol, loss_tol):
                 errs[f"mom_{name}[{l}]"] = rel_l2(p.mom[m][l].cpu().numpy(), mom[m])
         den = abs(losses[-1]) if p.cfg.act_dtype == "f32" else p.loss_scale(l)
         errs[f"loss[{l}]"] = abs(loss[l] - losses[-1]) / max(den, 1e-30)
+    print("max errors:", {k: f"{v:.2e}" for k, v in sorted(errs.items(), key=lambda t: -t[1])[:4]})
     bad = {k: v for k, v in errs.items() if v > (loss_tol if k.startswith("loss") else tol)}
     assert not bad, f"{bad} (all: {errs})"
     return errs
@@ -221,6 +222,7 @@ def test_read_and_attention(case):
         errs[f"kv_end_to_end[{l}]"] = rel_l2(kv_h[l], sw.memory_kv(h2, rds[l]["w_kv"]))
         want_out = orc.memory_attention(att_h[0][l], att_h[1][l], att_h[2][l], want, hq, hkv)
         errs[f"attn[{l}]"] = rel_l2(out_h[l], want_out)
+    print("max errors:", {k: f"{v:.2e}" for k, v in sorted(errs.items(), key=lambda t: -t[1])[:4]})
     bad = {k: v for k, v in errs.items() if v > tol}
     assert not bad, f"{bad} (all: {errs})"
 
