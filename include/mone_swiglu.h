@@ -22,7 +22,7 @@
  *
  * Conventions are those of mone_ttl.h (row-major, caller-owned 16-byte-aligned device buffers,
  * host-side validation, mone_status return codes, mone_ttl_last_error()).
- * GPU-path limits: d_model a multiple of 64, d_head a multiple of 8 in [8, 256], seg_len at
+ * GPU-path limits: d_model a multiple of 64, d_head a multiple of 16 in [16, 256], seg_len at
  * most 65536 (MONE_EUNSUPPORTED otherwise).
  */
 #ifndef MONE_SWIGLU_H

@@ -69,8 +69,8 @@ int check_sw_config(const mone_swiglu_config* c) {
   if (!std::isfinite(c->rope_base) || !(c->rope_base > 0.0f))
     return fail(MONE_EINVAL, "rope_base must be finite and positive");
   if (c->d_model % 64) return fail(MONE_EUNSUPPORTED, "d_model must be a multiple of 64");
-  if (c->d_head % 8 || c->d_head > 256)
-    return fail(MONE_EUNSUPPORTED, "d_head must be a multiple of 8 in [8, 256]");
+  if (c->d_head % 16 || c->d_head > 256)
+    return fail(MONE_EUNSUPPORTED, "d_head must be a multiple of 16 in [16, 256]");
   if (c->seg_len > 65536) return fail(MONE_EUNSUPPORTED, "seg_len above 65536");
   const long long Tp = round_up(c->seg_len, 256), d = c->d_model;
   const long long E = c->act_dtype == MONE_BF16 ? 2 : 4;

@@ -364,55 +364,55 @@ __global__ void sw_rope_table_kernel(float2* __restrict__ tab, int Tp, int dh, d
   tab[i] = make_float2((float)cs, (float)sn);
 }
 
-// KEYS: one workgroup per (64 tokens, head e, layer l); one wave per token at a time.  From the
-// post-SiLU keys K' of the head, each token's keys are divided by max(norm, 1e-12) and rotated
-// by RoPE at the token's position (the table holds cos and sin per position and channel pair);
-// written as K [B][Tp][d_hp] (zero padding columns) and, through LDS, K^T [B][d_h][Tp].
-// Lane l holds channels 4l .. 4l + 3; the partner of channel c < d_h/2 is c + d_h/2, held by
-// lane l + d_h/8 (d_h is a multiple of 8).  Tokens >= n hold zeros in K' and stay zero.
+// KEYS: one workgroup per (64 tokens, head e, layer l).  From the post-SiLU keys K' of the head,
+// each token's keys are divided by max(norm, 1e-12) and rotated by RoPE at the token's position
+// (the table holds cos and sin per position and channel pair); written as K [B][Tp][d_hp] (zero
+// padding columns) and, through LDS, K^T [B][d_h][Tp].  Each half-wave (32 lanes) takes one
+// token, lane i of it the 8 channels [8i, 8i + 8) as one 16-byte vector; the partner channels
+// of vector i (RoPE pairs c and c + d_h/2) are vector i +- d_h/16, fetched by shuffle (d_h is a
+// multiple of 16 and at most 256).  Tokens >= n hold zeros in K' and stay zero.
 template <typename E>
 __global__ __launch_bounds__(256) void sw_keys_kernel(const E* __restrict__ kpre, int d, int H,
                                                       int dh, int dhp, int Tp,
                                                       const float2* __restrict__ rope,
                                                       E* __restrict__ kh, E* __restrict__ kt) {
-  __shared__ float tile[64][257];  // [token][channel], d_h <= 256
+  __shared__ float tile[64][257];  // [token][channel]
   const int j0 = blockIdx.x * 64, e = blockIdx.y, l = blockIdx.z, b = l * H + e;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int half = dh / 2, q = dh / 8, c = 4 * lane;
-  const bool act = c < dh;
-  const bool lo = c < half;
-  const int src = act ? (lo ? lane + q : lane - q) : lane;
-  for (int t = wave; t < 64; t += 4) {
+  const int li = lane & 31, hw = lane >> 5;  // vector index, half-wave
+  const int nv = dh / 8, hv = dh / 16, half = dh / 2, c = 8 * li;
+  const bool act = li < nv, lo = li < hv;
+  const int src = (lane & 32) + (act ? (lo ? li + hv : li - hv) : li);
+  for (int t = 2 * wave + hw; t < 64; t += 8) {
     const int j = j0 + t;
-    float x[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    if (act) {
-      const E* p = kpre + ((long long)l * Tp + j) * d + (long long)e * dh + c;
+    float x[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    if (act) load8(kpre + ((long long)l * Tp + j) * d + (long long)e * dh + c, x);
+    float ss = 0.0f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) x[i] = to_f32(p[i]);
-    }
-    float ss = x[0] * x[0] + x[1] * x[1] + x[2] * x[2] + x[3] * x[3];
+    for (int i = 0; i < 8; ++i) ss += x[i] * x[i];
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+    for (int off = 16; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);  // within the half
     const float inv = 1.0f / fmaxf(sqrtf(ss), 1e-12f);
-    float y[4];
+    float y[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) y[i] = __shfl(x[i], src, 64);
-    float o[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int i = 0; i < 8; ++i) y[i] = __shfl(x[i], src, 64);
+    float o[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
     if (act) {
-      const float2* cs = rope + (long long)j * half + (lo ? c : c - half);
+      const float4* cs = reinterpret_cast<const float4*>(rope + (long long)j * half +
+                                                         (lo ? c : c - half));
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float2 r = cs[i];
+        const float4 r = cs[i];  // (cos, sin) of channel pairs 2i and 2i + 1 of the vector
+        const float c0 = r.x, s0 = r.y, c1 = r.z, s1 = r.w;
         // c < d_h/2: x cos - partner sin; c >= d_h/2: partner sin + x cos
-        o[i] = (lo ? x[i] * r.x - y[i] * r.y : y[i] * r.y + x[i] * r.x) * inv;
-        tile[t][c + i] = o[i];
+        o[2 * i] = (lo ? x[2 * i] * c0 - y[2 * i] * s0 : y[2 * i] * s0 + x[2 * i] * c0) * inv;
+        o[2 * i + 1] = (lo ? x[2 * i + 1] * c1 - y[2 * i + 1] * s1
+                           : y[2 * i + 1] * s1 + x[2 * i + 1] * c1) * inv;
       }
-    }
-    if (c < dhp) {
-      E* kr = kh + ((long long)b * Tp + j) * dhp + c;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) kr[i] = from_f32<E>(o[i]);
+      for (int i = 0; i < 8; ++i) tile[t][c + i] = o[i];
     }
+    if (c < dhp) store8(kh + ((long long)b * Tp + j) * dhp + c, o);
   }
   __syncthreads();
   // K^T: 8 threads per channel row, 8 tokens (one vector) each

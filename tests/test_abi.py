@@ -192,6 +192,7 @@ def test_swiglu_workspace_formula():
     (dict(rope_base=0.0), mone.MONE_EINVAL),
     (dict(d_model=160, d_head=80), mone.MONE_EUNSUPPORTED),  # d_model not a multiple of 64
     (dict(d_model=320, n_heads=1, d_head=320), mone.MONE_EUNSUPPORTED),  # d_head above 256
+    (dict(d_model=192, n_heads=8, d_head=24), mone.MONE_EUNSUPPORTED),  # not a multiple of 16
     (dict(d_model=256, n_heads=16, d_head=16, seg_len=70000), mone.MONE_EUNSUPPORTED),
 ])
 def test_swiglu_invalid_configs_are_rejected(kw, code):
