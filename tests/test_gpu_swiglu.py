@@ -266,3 +266,37 @@ def test_stage_timing_and_mask():
     mone.mone_swiglu_set_stage_timing(h, 0)  # off
     p.segment(3, cfg.seg_len)
     assert all(v[1] == 0 for v in mone.mone_swiglu_stage_times(h).values())
+
+
+def test_deterministic_and_resumable():
+    """Two runs from the same state are bitwise identical, and a run split across handles (a
+    checkpoint of the weights and the momenta, resumed by a new handle) equals the one-shot
+    run: the renormalisation targets are the resumed weights' row norms, which the
+    renormalisation keeps equal to the initial ones (up to its rounding)."""
+    cfg = configs.SW_TINY.with_(act_dtype="bf16", optimizer="paper")
+    runs = []
+    for _ in range(2):
+        p = SwProblem(cfg)
+        for s in range(4):
+            p.segment(s, cfg.seg_len)
+        torch.cuda.synchronize()
+        runs.append([w.clone() for w in p.w] + [m.clone() for m in p.mom])
+    for a, b in zip(*runs):
+        assert torch.equal(a, b)
+    # split: 2 segments, checkpoint, new handle on the copies, 2 more segments
+    p = SwProblem(cfg)
+    for s in range(2):
+        p.segment(s, cfg.seg_len)
+    torch.cuda.synchronize()
+    ck_w = [w.clone() for w in p.w]
+    ck_m = [m.clone() for m in p.mom]
+    p.sess.close()
+    opt = p.opt[:4] + tuple(ck_m)
+    sess = mone.SwigluSession(cfg, p.proj, p.k_scale, p.k_shift, *ck_w, opt=opt)
+    for s in range(2, 4):
+        xs = [inputs.segment_x(cfg, l, s) for l in range(cfg.n_layers)]
+        sess.segment(torch.from_numpy(np.stack(xs)).to("cuda", p.act))
+    torch.cuda.synchronize()
+    for got, want in zip(ck_w + ck_m, runs[0]):
+        err = float((got - want).norm() / want.norm())
+        assert err < 1e-5, err
