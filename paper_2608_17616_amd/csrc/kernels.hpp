@@ -12,10 +12,11 @@
 //
 // Main loop.  BM x BN output per 256-thread workgroup (4 waves), K step of 128 bytes per row
 // (64 bf16 or 32 fp32).  Operand tiles go from memory straight into LDS (buffer_load ... lds,
-// no register staging) in two stages; the 16-byte column slot of row r is XOR-swizzled by
-// (r / 2) % 8, which each lane applies by choosing its source address, so fragment reads of 32
-// consecutive rows are free of bank conflicts.  Loads of K step k+1 are in flight while the
-// MFMAs of step k run.
+// no register staging) into rings of K-step slots (A two steps ahead for square tiles, B one);
+// the 16-byte column slot of row r is XOR-swizzled by (r / 2) % 8, which each lane applies by
+// choosing its source address, so fragment reads of 32 consecutive rows are free of bank
+// conflicts.  The loads of later K steps are spread over the MFMAs of the current one, and each
+// wave reads its fragments one sub-step ahead of the MFMAs that use them.
 //
 // MFMA: bf16 uses v_mfma_f32_32x32x16_bf16 (one 16-byte fragment per lane = 8 k-values), fp32
 // uses four v_mfma_f32_32x32x2_f32 on the four floats of the same 16-byte fragment.  Within a
@@ -28,7 +29,7 @@
 // columns of one row: 16- or 32-byte vector accesses) and, where a transposed copy is stored, a
 // column pass (8 rows of one column).  An epilogue may also take its rows in pairs (rows 2i and
 // 2i + 1 of a sub-block reach the same lane), for results that combine two interleaved output
-// rows.
+// rows, or, on 64 x 256 tiles, scale whole rows after a workgroup-wide sum of their squares.
 #pragma once
 
 #include <hip/hip_runtime.h>
