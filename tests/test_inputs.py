@@ -51,3 +51,32 @@ def test_config_table():
     assert c.flops_per_token() == 2 ** 32
     assert configs.STRESS.n_segments == 8192 and configs.TINY.n_segments == 8
     assert configs.ONE_B.flops_per_token() == 16 * 33554432
+
+
+# ---------------------------------------------------------------- the paper-form memory
+
+def test_swiglu_generators_are_keyed_and_independent():
+    cfg = configs.SW_TINY
+    p0, p1 = inputs.sw_layer_proj(cfg, 0), inputs.sw_layer_proj(cfg, 1)
+    assert p0.shape == (2 * cfg.d_model, cfg.d_model) and not np.array_equal(p0, p1)
+    assert np.array_equal(p0, inputs.sw_layer_proj(cfg, 0))
+    f = inputs.sw_layer_fast(cfg, 1)
+    assert all(w.shape == (cfg.n_heads, cfg.d_head, cfg.d_head) for w in f)
+    assert not np.array_equal(f[0], f[1]) and not np.array_equal(f[1], f[2])
+    s, b = inputs.sw_layer_affine(cfg, 0)
+    assert s.dtype == np.float32 and abs(float(s.mean()) - 1.0) < 0.05 and abs(float(b.mean())) < 0.05
+    r = inputs.sw_layer_reader(cfg, 0, 64)
+    assert r["w_kv"].shape == (128, cfg.d_model) and r["gate_w"].shape == (cfg.n_heads, cfg.d_model)
+    bf = configs.SW_TINY.with_(act_dtype="bf16")
+    q = inputs.sw_layer_proj(bf, 0)
+    assert np.array_equal(q, inputs.act_round(q, "bf16"))  # bf16-representable in bf16 mode
+
+
+def test_swiglu_flops_formula():
+    cfg = configs.SW_PAPER
+    d, H, dh = cfg.d_model, cfg.n_heads, cfg.d_head
+    # projections (2 * d * 2d) + per head: dA (2 dh^2), the two branches (4 dh^2), the three
+    # weight gradients (6 dh^2)
+    assert cfg.flops_per_token_layer() == 2 * d * 2 * d + H * (2 + 4 + 6) * dh * dh
+    assert cfg.flops_per_token() == cfg.n_layers * cfg.flops_per_token_layer()
+    assert cfg.n_segments == 256 and H * dh == d
