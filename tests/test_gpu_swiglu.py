@@ -300,3 +300,49 @@ def test_deterministic_and_resumable():
     for got, want in zip(ck_w + ck_m, runs[0]):
         err = float((got - want).norm() / want.norm())
         assert err < 1e-5, err
+
+
+def test_full_context_paper_shape_last_step():
+    """The paper's shape over a whole 128K-token context (256 segments) with the paper's
+    optimiser: the last step, from the GPU's own state before it, against the oracle's step on
+    that state (first and last layers), and every row norm still at its initial value."""
+    cfg = configs.SW_PAPER.with_(optimizer="paper")
+    p = SwProblem(cfg)
+    L, T, d, H = cfg.n_layers, cfg.seg_len, cfg.d_model, cfg.n_heads
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(7)
+    x = torch.empty(L, T, d, dtype=p.act, device="cuda")
+    for _ in range(cfg.n_segments - 1):
+        inputs.device_normal_(x, 1.0, gen)
+        p.sess.segment(x, T)
+    torch.cuda.synchronize()
+    snap_w = [w.cpu().numpy().astype(np.float64) for w in p.w]
+    snap_m = [m.cpu().numpy().astype(np.float64) for m in p.mom]
+    checked = [0, L - 1]
+    inputs.device_normal_(x, 1.0, gen)
+    xh = {}
+    for l in checked:
+        xh[l] = inputs.segment_x(cfg, l, cfg.n_segments - 1)
+        x[l].copy_(torch.from_numpy(xh[l]))
+    p.sess.segment(x, T)
+    torch.cuda.synchronize()
+    got_w = [w.cpu().numpy().astype(np.float64) for w in p.w]
+    got_m = [m.cpu().numpy().astype(np.float64) for m in p.mom]
+    w0 = [w.cpu().numpy().astype(np.float64) for w in p.w0]
+    errs = {}
+    for l in checked:
+        fast = tuple(w[l] for w in snap_w)
+        mom = tuple(m[l] for m in snap_m)
+        norms0 = sw.initial_norms(tuple(w[l] for w in w0))
+        new, new_m, _, _ = sw.paper_step(xh[l].astype(np.float64), fast, mom, p.frozen(l),
+                                         p.meta[l], norms0, cfg.lr, H, cfg.rope_base)
+        for k, name in enumerate(("w_in", "w_gate", "w_out")):
+            errs[f"{name}[{l}]"] = rel_l2(got_w[k][l], new[k])
+            errs[f"d{name}[{l}]"] = rel_l2(got_w[k][l] - fast[k], new[k] - fast[k])
+            errs[f"mom_{name}[{l}]"] = rel_l2(got_m[k][l], new_m[k])
+    print("max errors:", {k: f"{v:.2e}" for k, v in sorted(errs.items(), key=lambda t: -t[1])[:4]})
+    assert max(errs.values()) < 2e-2, errs
+    for k in range(3):  # row norms over every layer and head after the whole context
+        n_end = np.linalg.norm(got_w[k], axis=-1)
+        n_0 = np.linalg.norm(w0[k], axis=-1)
+        assert np.max(np.abs(n_end - n_0) / n_0) < 1e-4
