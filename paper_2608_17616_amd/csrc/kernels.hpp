@@ -749,7 +749,8 @@ struct EpiFwd2 : EpiBase {
 template <typename E, bool PAPER = false>
 struct EpiBwdW2 : EpiBase {
   static constexpr bool kPre = true;
-  static constexpr int kAux = PAPER ? 16 : 8;
+  static constexpr int kAux = 8;  // the master (PAPER: the momentum is read in the row pass,
+                                  // which keeps the 256 x 256 tile within its registers)
   static constexpr bool kRowNorm = PAPER;
   static constexpr bool kCols = !PAPER;
   static constexpr bool kWriteback = !PAPER;
@@ -775,7 +776,6 @@ struct EpiBwdW2 : EpiBase {
     } else {
       const long long o = (long long)layer * ls2 + (long long)row * h + col;
       load8(w2 + o, x0);
-      if constexpr (PAPER) load8(mom2 + o, *reinterpret_cast<float(*)[8]>(&x[8]));
     }
   }
   __device__ __forceinline__ float rows8(int pi, int layer, int row, int col, int, int,
@@ -791,9 +791,10 @@ struct EpiBwdW2 : EpiBase {
     if constexpr (PAPER) {
       const float b = beta[layer];
       float m[8], nw[8], ss = 0.0f;
+      load8(mom2 + o, m);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        m[e] = b * x[8 + e] + v[e];
+        m[e] = b * m[e] + v[e];
         nw[e] = x[e] - m[e];
         ss += nw[e] * nw[e];
       }
@@ -838,7 +839,7 @@ struct EpiBwdW2 : EpiBase {
 template <typename E, bool PAPER = false>
 struct EpiW1 : EpiBase {
   static constexpr bool kPre = true;
-  static constexpr int kAux = PAPER ? 16 : 8;
+  static constexpr int kAux = 8;  // the master (PAPER: the momentum is read in the row pass)
   static constexpr bool kRowNorm = PAPER;
   float* w1; E* w1s;
   long long ls1;  // h*d
@@ -852,8 +853,7 @@ struct EpiW1 : EpiBase {
   __device__ __forceinline__ void pre8(int, int layer, int row, int col, int, int,
                                        float (&w)[kAux]) const {
     const long long o = (long long)layer * ls1 + (long long)row * d + col;
-    load8(w1 + o, *reinterpret_cast<float(*)[8]>(&w[0]));
-    if constexpr (PAPER) load8(mom1 + o, *reinterpret_cast<float(*)[8]>(&w[8]));
+    load8(w1 + o, w);
   }
   __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
                                          float (&v)[8], const float (&w)[kAux]) const {
@@ -861,9 +861,10 @@ struct EpiW1 : EpiBase {
     if constexpr (PAPER) {
       const float b = beta[layer];
       float m[8], nw[8], ss = 0.0f;
+      load8(mom1 + o, m);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        m[e] = b * w[8 + e] + v[e];
+        m[e] = b * m[e] + v[e];
         nw[e] = w[e] - m[e];
         ss += nw[e] * nw[e];
       }
