@@ -84,6 +84,16 @@ int check_config(const mone_ttl_config* c) {
   return MONE_OK;
 }
 
+// Tile of a weight-gradient launch (BWD, UPD), whose contraction runs over the k tokens of the
+// segment.  Below 2048 tokens a 256 x 256 tile spends most of its time in the fp32
+// read-modify-write epilogue with one workgroup per CU; 128 x 128 tiles keep two workgroups per
+// CU, so one's epilogue overlaps the other's main loop (measured faster at k = 64 .. 1024, slower
+// at k = 2048).
+TileShape upd_tile(int m, int n_cols, int k, int layers) {
+  if (k < 2048 && m > 64 && n_cols > 64) return TILE_128x128;
+  return pick_tile(m, n_cols, layers);
+}
+
 Layout make_layout(const mone_ttl_config* c) {
   Layout L{};
   const size_t E = c->act_dtype == MONE_BF16 ? 2 : 4;
@@ -91,7 +101,6 @@ Layout make_layout(const mone_ttl_config* c) {
   const size_t d = c->d_model, h = c->d_hidden, D = 2 * (size_t)c->d_kv;
   L.Tp = (int)round_up(c->seg_len, 256);
   const size_t Tp = L.Tp;
-  // 4 wave partials per tile of the smallest tile shape (64 rows x 128 columns)
   // 4 wave partials per tile of the smallest tile shapes: forward 2's tiles over [Tp][D] and,
   // for the negative inner product, the W2 update's tiles over [D][h]
   const size_t lp_fwd2 = (Tp / 64) * ((D + 127) / 128), lp_w2 = ((D + 63) / 64) * ((h + 63) / 64);
@@ -286,7 +295,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     epi.nip = c.loss == MONE_LOSS_NIP ? 1 : 0;
     int tiles[2] = {0, 0};
     H->timing_begin(MONE_STAGE_BWD, s);
-    if ((e = launch_gemm<E>(pick_tile(h, n, Lc), sp, 2, Lc, epi, s, tiles)) != hipSuccess)
+    if ((e = launch_gemm<E>(upd_tile(h, n, n, Lc), sp, 2, Lc, epi, s, tiles)) != hipSuccess)
       return hip_fail(e, "launch BWD");
     H->timing_end(MONE_STAGE_BWD, s);
     if (c.loss == MONE_LOSS_NIP) H->last_loss_count = 4 * tiles[1];
@@ -311,7 +320,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     epi.ss1 = PAPER ? H->at<float>(Ly.ss1) : nullptr;
     epi.h = h;
     H->timing_begin(MONE_STAGE_UPD, s);
-    if ((e = launch_gemm<E>(pick_tile(h, d, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
+    if ((e = launch_gemm<E>(upd_tile(h, d, n, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
       return hip_fail(e, "launch UPD");
     H->timing_end(MONE_STAGE_UPD, s);
   }
