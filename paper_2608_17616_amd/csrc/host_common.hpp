@@ -124,7 +124,7 @@ hipError_t launch_gemm(TileShape t, const Spec* specs, int nspec, int layers, co
 }
 
 // Memory injection into attention (Eq. attn with Eq. std_attn): validation and the launch of
-// memory_attention_kernel for L layers of K/V width d_kv; one query row per wavefront.  With
+// memory_attention_kernel for L layers of K/V width d_kv; 16 query rows per workgroup.  With
 // q = 0 nothing is launched.
 inline int launch_attention(int L, int d_kv, bool act_bf16, const void* qh, const void* kh,
                             const void* vh, const void* kv_mem, int kv_dtype, int q, int n_heads,
@@ -143,15 +143,21 @@ inline int launch_attention(int L, int d_kv, bool act_bf16, const void* qh, cons
     return fail(MONE_EINVAL, "qh, kh, vh, kv_mem and out must be non-NULL");
   if (!aligned16(qh) || !aligned16(kh) || !aligned16(vh) || !aligned16(kv_mem) || !aligned16(out))
     return fail(MONE_EINVAL, "qh, kh, vh, kv_mem and out must be 16-byte aligned");
-  const dim3 grid((q + 3) / 4, n_heads, L), block(256);
+  const dim3 grid((q + 15) / 16, n_heads, L), block(256);
   const float scale = 1.0f / std::sqrt((float)dh);
   const bool kbf = kv_dtype == MONE_BF16, obf = out_dtype == MONE_BF16;
-  // the eight dtype combinations of (activations, memory K/V, output)
-#define MONE_ATTN(EA, EK, EO)                                                                   \
-  memory_attention_kernel<EA, EK, EO><<<grid, block, 0, s>>>(                                  \
+  // the eight dtype combinations of (activations, memory K/V, output), for heads of up to 128
+  // columns or up to 256
+#define MONE_ATTN_W(EA, EK, EO, DHM)                                                            \
+  memory_attention_kernel<EA, EK, EO, DHM><<<grid, block, 0, s>>>(                             \
       reinterpret_cast<const EA*>(qh), reinterpret_cast<const EA*>(kh),                         \
       reinterpret_cast<const EA*>(vh), reinterpret_cast<const EK*>(kv_mem),                     \
       reinterpret_cast<EO*>(out), q, n_heads, n_kv_heads, dh, d_kv, scale)
+#define MONE_ATTN(EA, EK, EO)                                                                   \
+  do {                                                                                          \
+    if (dh <= 128) MONE_ATTN_W(EA, EK, EO, 128);                                                \
+    else MONE_ATTN_W(EA, EK, EO, 256);                                                          \
+  } while (0)
   if (act_bf16) {
     if (kbf) { if (obf) MONE_ATTN(bf16_t, bf16_t, bf16_t); else MONE_ATTN(bf16_t, bf16_t, float); }
     else { if (obf) MONE_ATTN(bf16_t, float, bf16_t); else MONE_ATTN(bf16_t, float, float); }
@@ -160,6 +166,7 @@ inline int launch_attention(int L, int d_kv, bool act_bf16, const void* qh, cons
     else { if (obf) MONE_ATTN(float, float, bf16_t); else MONE_ATTN(float, float, float); }
   }
 #undef MONE_ATTN
+#undef MONE_ATTN_W
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "launch ATTN");
   return MONE_OK;

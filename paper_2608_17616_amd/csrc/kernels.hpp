@@ -1192,68 +1192,204 @@ __global__ __launch_bounds__(256) void renorm_w2_kernel(float* __restrict__ w2, 
 // ------------------------------------------------------------------------------------------
 // Memory injection into attention (read time)
 
-// out[l][i][a] = softmax over j <= i of the scaled scores of q_i against the query-side keys
-// k_j and the memory keys km_j, applied to [v_j ; vm_j] (one softmax over both sets).  Head a
-// of Q reads key/value head a / (n_heads / n_kv_heads); head width dh <= 256.  One wave per
-// (layer, head, query row), online softmax over the keys in order (deterministic).
-// Grid (ceil(q / 4), n_heads, L), 256 threads.
-template <typename E, typename EK, typename EO>
+// out[l][i][a] = softmax over the keys j <= i of both sets (the query-side keys k_j and the
+// memory keys km_j, one softmax) of the scaled scores q_i . k, applied to [v_j ; vm_j].  Head a
+// of Q reads key/value head a / (n_heads / n_kv_heads); head width dh <= DHM.
+// Workgroup: 16 query rows of one head and layer, 4 rows per wave.  Keys and values pass
+// through LDS in chunks of 32 of each set, as fp32.  Score pass: lane L takes key L of the chunk
+// (query-side keys on lanes 0-31, memory keys on lanes 32-63) over key rows of odd stride, so the
+// 64 lanes read 64 distinct banks while the query rows are broadcast.  The softmax is online
+// over the chunks in order (deterministic); the weighted sum has lanes over the head's columns.
+// Grid (ceil(q / 16), n_heads, L), 256 threads.
+template <typename E, typename EK, typename EO, int DHM>
 __global__ __launch_bounds__(256) void memory_attention_kernel(
     const E* __restrict__ qh, const E* __restrict__ kh, const E* __restrict__ vh,
     const EK* __restrict__ kvm, EO* __restrict__ out, int q, int n_heads, int n_kv_heads, int dh,
     int d_kv, float scale) {
-  const int l = blockIdx.z, a = blockIdx.y;
-  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (i >= q) return;
+  constexpr int KC = 32;       // keys of each set per chunk
+  constexpr int RW = 4;        // query rows per wave
+  constexpr int QB = 4 * RW;   // query rows per workgroup
+  constexpr int KS = DHM + 1;  // key row stride in LDS (odd)
+  constexpr int NT = DHM / 64; // head columns per lane in the weighted sum
+  __shared__ float ks[2 * KC * KS];   // [query-side keys ; memory keys] of the chunk
+  __shared__ __attribute__((aligned(16))) float vs[2 * KC * DHM];  // [query-side ; memory values]
+  __shared__ __attribute__((aligned(16))) float qs[QB * DHM];  // the block's query rows, scaled
+  const int l = blockIdx.z, a = blockIdx.y, i0 = blockIdx.x * QB;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = a / (n_heads / n_kv_heads);
+  const int dh4 = (dh + 3) & ~3;  // columns the score pass runs over (zero beyond dh)
   const long long qw = (long long)n_heads * dh, kw = (long long)n_kv_heads * dh;
-  const E* qi = qh + ((long long)l * q + i) * qw + (long long)a * dh;
+  const E* ql = qh + (long long)l * q * qw + (long long)a * dh;
   const E* kl = kh + (long long)l * q * kw + (long long)g * dh;
   const E* vl = vh + (long long)l * q * kw + (long long)g * dh;
   const EK* ml = kvm + (long long)l * q * 2 * d_kv + (long long)g * dh;
-  float qv[4], acc[4];
+  const int last = (i0 + QB < q ? i0 + QB : q) - 1;  // the block's last query row
+
+  // Operand rows are moved in groups of 8 columns with 16-byte loads when dh is a multiple of
+  // 8 (every row then starts 16-byte aligned), all of a thread's loads before its LDS writes;
+  // element by element otherwise.
+  const bool vec = (dh & 7) == 0;
+  const int g8 = dh >> 3;
+  if (vec) {
+    constexpr int UQ = (QB * (DHM / 8) + 255) / 256;
+    float x8[UQ][8];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int e = lane + 64 * t;
-    qv[t] = e < dh ? to_f32(qi[e]) * scale : 0.0f;
-    acc[t] = 0.0f;
+    for (int u = 0; u < UQ; ++u) {
+      const int x = tid + 256 * u, r = x / g8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x8[u][e] = 0.0f;
+      if (x < QB * g8 && i0 + r < q) load8(ql + (long long)(i0 + r) * qw + (x - r * g8) * 8, x8[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < UQ; ++u) {
+      const int x = tid + 256 * u, r = x / g8, c = (x - r * g8) * 8;
+      if (x >= QB * g8) continue;
+      float* dst = qs + r * DHM + c;
+      *reinterpret_cast<float4*>(dst) = make_float4(x8[u][0] * scale, x8[u][1] * scale,
+                                                    x8[u][2] * scale, x8[u][3] * scale);
+      *reinterpret_cast<float4*>(dst + 4) = make_float4(x8[u][4] * scale, x8[u][5] * scale,
+                                                        x8[u][6] * scale, x8[u][7] * scale);
+    }
+  } else {
+    for (int x = tid; x < QB * dh4; x += 256) {
+      const int r = x / dh4, d = x - r * dh4;
+      float v = 0.0f;
+      if (i0 + r < q && d < dh) v = to_f32(ql[(long long)(i0 + r) * qw + d]) * scale;
+      qs[r * DHM + d] = v;
+    }
   }
-  float m = -INFINITY, lsum = 0.0f;
-  for (int j = 0; j <= i; ++j) {
-    const E* kj = kl + (long long)j * kw;
-    const EK* mj = ml + (long long)j * 2 * d_kv;
-    float s1 = 0.0f, s2 = 0.0f;
+  float m[RW], lsum[RW], acc[RW][NT];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int e = lane + 64 * t;
-      if (e < dh) {
-        s1 += qv[t] * to_f32(kj[e]);
-        s2 += qv[t] * to_f32(mj[e]);
+  for (int r = 0; r < RW; ++r) {
+    m[r] = -INFINITY;
+    lsum[r] = 0.0f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[r][t] = 0.0f;
+  }
+  // rows past q repeat the last row (finite, never stored)
+  int row[RW];
+#pragma unroll
+  for (int r = 0; r < RW; ++r) {
+    const int i = i0 + wave * RW + r;
+    row[r] = i < last ? i : last;
+  }
+
+  for (int j0 = 0; j0 <= last; j0 += KC) {
+    __syncthreads();  // the previous chunk is consumed (and the query rows are in place)
+    // chunk row rr < KC: query-side key/value j0 + rr; rr >= KC: memory key/value j0 + rr - KC
+    if (vec) {
+      constexpr int UK = (2 * KC * (DHM / 8) + 255) / 256;
+      float k8[UK][8], v8[UK][8];
+#pragma unroll
+      for (int u = 0; u < UK; ++u) {
+        const int x = tid + 256 * u, rr = x / g8, c = (x - rr * g8) * 8;
+        const int j = j0 + (rr & (KC - 1));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) k8[u][e] = v8[u][e] = 0.0f;
+        if (x < 2 * KC * g8 && j < q) {
+          if (rr < KC) {
+            load8(kl + (long long)j * kw + c, k8[u]);
+            load8(vl + (long long)j * kw + c, v8[u]);
+          } else {
+            const EK* mj = ml + (long long)j * 2 * d_kv;
+            load8(mj + c, k8[u]);
+            load8(mj + d_kv + c, v8[u]);
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < UK; ++u) {
+        const int x = tid + 256 * u, rr = x / g8, c = (x - rr * g8) * 8;
+        if (x >= 2 * KC * g8) continue;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ks[rr * KS + c + e] = k8[u][e];
+        float* vd = vs + rr * DHM + c;
+        *reinterpret_cast<float4*>(vd) = make_float4(v8[u][0], v8[u][1], v8[u][2], v8[u][3]);
+        *reinterpret_cast<float4*>(vd + 4) = make_float4(v8[u][4], v8[u][5], v8[u][6], v8[u][7]);
+      }
+    } else {
+      for (int x = tid; x < 2 * KC * dh4; x += 256) {
+        const int rr = x / dh4, d = x - rr * dh4;
+        const int j = j0 + (rr & (KC - 1));
+        float kv = 0.0f, vv = 0.0f;
+        if (j < q && d < dh) {
+          if (rr < KC) {
+            kv = to_f32(kl[(long long)j * kw + d]);
+            vv = to_f32(vl[(long long)j * kw + d]);
+          } else {
+            const EK* mj = ml + (long long)j * 2 * d_kv;
+            kv = to_f32(mj[d]);
+            vv = to_f32(mj[d_kv + d]);
+          }
+        }
+        ks[rr * KS + d] = kv;
+        vs[rr * DHM + d] = vv;
       }
     }
+    __syncthreads();
+
+    // scores of this wave's rows against key `lane` of the chunk
+    float s[RW];
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      s1 += __shfl_xor(s1, off, 64);
-      s2 += __shfl_xor(s2, off, 64);
-    }
-    const float mn = fmaxf(m, fmaxf(s1, s2));
-    const float c = __expf(m - mn), p1 = __expf(s1 - mn), p2 = __expf(s2 - mn);
-    lsum = lsum * c + p1 + p2;
-    const E* vj = vl + (long long)j * kw;
-    const EK* vmj = mj + d_kv;
+    for (int r = 0; r < RW; ++r) s[r] = 0.0f;
+    const float* kr = ks + lane * KS;
+    const float* qr = qs + wave * RW * DHM;
+    for (int d = 0; d < dh4; d += 4) {
+      const float k0 = kr[d], k1 = kr[d + 1], k2 = kr[d + 2], k3 = kr[d + 3];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int e = lane + 64 * t;
-      if (e < dh) acc[t] = acc[t] * c + p1 * to_f32(vj[e]) + p2 * to_f32(vmj[e]);
+      for (int r = 0; r < RW; ++r) {
+        const float4 qv = *reinterpret_cast<const float4*>(qr + r * DHM + d);
+        s[r] += qv.x * k0 + qv.y * k1 + qv.z * k2 + qv.w * k3;
+      }
     }
-    m = mn;
+    const int j = j0 + (lane & (KC - 1));
+    float p[RW];
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+      const float sv = j <= row[r] ? s[r] : -INFINITY;
+      float mx = sv;
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+      const float mn = fmaxf(m[r], mx);  // finite: key 0 is in every row's first chunk
+      const float c = __expf(m[r] - mn);
+      p[r] = __expf(sv - mn);
+      float ps = p[r];
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) ps += __shfl_xor(ps, off, 64);
+      lsum[r] = lsum[r] * c + ps;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[r][t] *= c;
+      m[r] = mn;
+    }
+    // weighted sum: value row L of the chunk (the key of lane L) with weight p of lane L
+    for (int L = 0; L < 2 * KC; ++L) {
+      float pb[RW];
+#pragma unroll
+      for (int r = 0; r < RW; ++r)
+        pb[r] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p[r]), L));
+      const float* vr = vs + L * DHM;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const int d = lane + 64 * t;
+        if (d < dh) {
+          const float vv = vr[d];
+#pragma unroll
+          for (int r = 0; r < RW; ++r) acc[r][t] += pb[r] * vv;
+        }
+      }
+    }
   }
-  EO* oi = out + ((long long)l * q + i) * qw + (long long)a * dh;
-  const float inv = 1.0f / lsum;
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int e = lane + 64 * t;
-    if (e < dh) oi[e] = from_f32<EO>(acc[t] * inv);
+  for (int r = 0; r < RW; ++r) {
+    const int i = i0 + wave * RW + r;
+    if (i >= q) continue;
+    EO* oi = out + ((long long)l * q + i) * qw + (long long)a * dh;
+    const float inv = 1.0f / lsum[r];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int d = lane + 64 * t;
+      if (d < dh) oi[d] = from_f32<EO>(acc[r][t] * inv);
+    }
   }
 }
 
