@@ -38,15 +38,20 @@ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 inline long long round_up(long long v, long long a) { return (v + a - 1) / a * a; }
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-enum TileShape { TILE_256x256 = 0, TILE_128x128 = 1, TILE_64x256 = 2, TILE_256x64 = 3 };
+// TILE_64x256_DEEP: 64 x 256 tiles with a 4-slot ring per operand (one workgroup per CU).
+enum TileShape {
+  TILE_256x256 = 0, TILE_128x128 = 1, TILE_64x256 = 2, TILE_256x64 = 3, TILE_64x256_DEEP = 4
+};
 
 constexpr int kNumCUs = 256;
 
-// 64-row tiles for short row extents (short segments, query batches), 64-column tiles for
-// short column extents (the token axis of the transposed backward); 256 x 256 when the grouped
-// problem still has at least one such tile per CU; 128 x 128 otherwise.
+// 64-row tiles for short row extents (short segments, query batches), with the deep ring when
+// the launch has at most one tile per CU; 64-column tiles for short column extents (the token
+// axis of the transposed backward); 256 x 256 when the grouped problem still has at least one
+// such tile per CU; 128 x 128 otherwise.
 inline TileShape pick_tile(int m, int n, int layers) {
-  if (m <= 64) return TILE_64x256;
+  if (m <= 64)
+    return (long long)((n + 255) / 256) * layers <= kNumCUs ? TILE_64x256_DEEP : TILE_64x256;
   if (n <= 64) return TILE_256x64;
   const long long big = (long long)((m + 255) / 256) * ((n + 255) / 256) * layers;
   if (m >= 256 && n >= 256 && big >= kNumCUs) return TILE_256x256;
@@ -72,7 +77,7 @@ inline Opnd opnd(const void* p, long long lstride, int ld, int rows) {
   return o;
 }
 
-template <typename E, int BM, int BN, int WAVES_M, class Epi>
+template <typename E, int BM, int BN, int WAVES_M, int DEPTH = 0, class Epi>
 hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi,
                         hipStream_t s, int* tiles_per_layer) {
   GemmLaunch<Epi> G;
@@ -97,14 +102,14 @@ hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi
   if (tiles_per_layer)  // tiles per layer of each problem
     for (int i = 0; i < nspec; ++i) tiles_per_layer[i] = G.prob[i].tiles_m * G.prob[i].tiles_n;
   if (begin == 0) return hipSuccess;
-  gemm_nt_kernel<E, BM, BN, WAVES_M, Epi><<<dim3(begin), dim3(256), 0, s>>>(G);
+  gemm_nt_kernel<E, BM, BN, WAVES_M, Epi, DEPTH><<<dim3(begin), dim3(256), 0, s>>>(G);
   return hipGetLastError();
 }
 
 // Tiles per layer of a problem of m x n under tile shape t (what launch_gemm will use).
 inline int tiles_for(TileShape t, int m, int n) {
   const int bm = t == TILE_256x256 || t == TILE_256x64 ? 256 : t == TILE_128x128 ? 128 : 64;
-  const int bn = t == TILE_256x256 || t == TILE_64x256 ? 256 : t == TILE_128x128 ? 128 : 64;
+  const int bn = t == TILE_256x64 ? 64 : t == TILE_128x128 ? 128 : 256;
   return ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
 }
 
@@ -118,6 +123,8 @@ hipError_t launch_gemm(TileShape t, const Spec* specs, int nspec, int layers, co
       return launch_tiled<E, 128, 128, 2>(specs, nspec, layers, epi, s, tiles_per_layer);
     case TILE_256x64:
       return launch_tiled<E, 256, 64, 4>(specs, nspec, layers, epi, s, tiles_per_layer);
+    case TILE_64x256_DEEP:
+      return launch_tiled<E, 64, 256, 1, 4>(specs, nspec, layers, epi, s, tiles_per_layer);
     default:
       return launch_tiled<E, 64, 256, 1>(specs, nspec, layers, epi, s, tiles_per_layer);
   }

@@ -174,13 +174,15 @@ __device__ __forceinline__ void map_tile(int local, int total, int tiles_m, int 
   *tn = r / gm;
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int DEPTH = 0>
 struct TileCfg {
   // Main loop: A and B panels of 128-byte rows in separate LDS rings.  The 256 x 256 and
   // 128 x 128 tiles keep A two K steps ahead (3 slots) and B one step ahead (2 slots), which
-  // fills the 160 KiB of LDS for one 256 x 256 workgroup per CU or two 128 x 128 ones.
-  static constexpr int NA = BM == BN ? 3 : 2;
-  static constexpr int NB = 2;
+  // fills the 160 KiB of LDS for one 256 x 256 workgroup per CU or two 128 x 128 ones.  A deep
+  // ring (DEPTH slots for both operands, both DEPTH - 1 steps ahead) is for launches with at
+  // most one workgroup per CU, whose K steps would otherwise each wait a full memory latency.
+  static constexpr int NA = DEPTH > 0 ? DEPTH : BM == BN ? 3 : 2;
+  static constexpr int NB = DEPTH > 0 ? DEPTH : 2;
   static constexpr int ASLOT = BM * 128, BSLOT = BN * 128;
   static constexpr int RING = NA * ASLOT + NB * BSLOT;
   static constexpr int EPI_BYTES = 4 * 64 * 64 * 4;  // per-wave 64 x 64 fp32 staging
@@ -227,9 +229,9 @@ __device__ __forceinline__ void reads_then_interleave() {
   front_seq<NM, NRL - lead, NV>(std::make_integer_sequence<int, NM>{});
 }
 
-template <typename E, int BM, int BN, int WAVES_M, class Epi>
+template <typename E, int BM, int BN, int WAVES_M, class Epi, int DEPTH = 0>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
-  using TC = TileCfg<BM, BN>;
+  using TC = TileCfg<BM, BN, DEPTH>;
   constexpr int VEC = 16 / (int)sizeof(E);   // elements per 16-byte vector
   constexpr int BK = 8 * VEC;                // K per step: 8 vectors = 128 bytes per row
   constexpr int WAVES_N = 4 / WAVES_M;
@@ -380,7 +382,67 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   // more (later loads may overwrite them).
   constexpr int VMC = NA > 2 ? LA : 0;  // loads allowed in flight at the synchronisation
   constexpr int WAIT_STEP = (VMC & 15) | ((VMC >> 4) << 14) | (7 << 4);
-  if (nk > 0) {
+  if constexpr (DEPTH > 0) {
+    // Deep ring: step kt reads slot kt % DEPTH; during its first three sub-steps each wave
+    // loads step kt + DEPTH - 1 into the slot of step kt - 1, which the synchronisation ending
+    // step kt - 1 released.  Before the synchronisation that ends step kt each wave waits until
+    // its loads of step kt + 1 have landed; those of the DEPTH - 2 later steps stay in flight.
+    static_assert(DEPTH >= 3 && NA == DEPTH && NB == DEPTH, "deep ring");
+    constexpr int VMD = (DEPTH - 2) * (LA + LB);
+    static_assert(VMD < 64, "vmcnt range");
+    constexpr int WAIT_D = (VMD & 15) | ((VMD >> 4) << 14) | (7 << 4);
+    if (nk > 0) {
+      u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
+      // Prologue: steps 0 .. DEPTH - 2 (the part of each step chosen at run time here only).
+#pragma unroll
+      for (int j = 0; j < DEPTH - 1; ++j) {
+        if (j < nk0) { load_a(Part0{}, j, j, 0, LA); load_b(Part0{}, j, j, 0, LB); }
+        else { load_a(Part1{}, j, j, 0, LA); load_b(Part1{}, j, j, 0, LB); }
+      }
+      __builtin_amdgcn_s_waitcnt(WAIT_D);
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      int sl = 0;
+      read_frags(sl, sl, 0, fa0, fb0);
+      auto dstep = [&](int kt, auto pl) {
+        const int sl_load = sl == 0 ? DEPTH - 1 : sl - 1;  // slot of step kt - 1: free
+        const int kl = kt + DEPTH - 1;
+        constexpr int NF = FM + FN;
+        read_frags(sl, sl, 1, fa1, fb1);
+        load_b(pl, kl, sl_load, 0, LB / 2);
+        mfmas(fa0, fb0);
+        reads_then_interleave<NF, NM, LB / 2>();
+        read_frags(sl, sl, 2, fa0, fb0);
+        load_b(pl, kl, sl_load, LB / 2, LB);
+        mfmas(fa1, fb1);
+        reads_then_interleave<NF, NM, LB - LB / 2>();
+        read_frags(sl, sl, 3, fa1, fb1);
+        load_a(pl, kl, sl_load, 0, LA);
+        mfmas(fa0, fb0);
+        reads_then_interleave<NF, NM, LA>();
+        __builtin_amdgcn_s_waitcnt(WAIT_D);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        sl = sl + 1 == DEPTH ? 0 : sl + 1;
+        read_frags(sl, sl, 0, fa0, fb0);  // after the last step: a consumed slot, never used
+        mfmas(fa1, fb1);
+        reads_then_interleave<NF, NM, 0>();
+      };
+      if constexpr (NP == 1) {
+        for (int kt = 0; kt < nk; ++kt) dstep(kt, Part0{});
+      } else {
+        // both operands switch part when the loaded step reaches nk0
+        const int e1 = nk0 - (DEPTH - 1) < 0 ? 0 : (nk0 - (DEPTH - 1) > nk ? nk : nk0 - (DEPTH - 1));
+        int kt = 0;
+        for (; kt < e1; ++kt) dstep(kt, Part0{});
+        for (; kt < nk; ++kt) dstep(kt, Part1{});
+      }
+      __builtin_amdgcn_s_waitcnt(0);  // the last (out-of-range) loads have retired
+      __syncthreads();                // the epilogue reuses the LDS of the rings
+    }
+  } else if (nk > 0) {
     u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
     // Prologue: step 0 first, then (ring of 3) A's step 1 and the first half of B's step 1,
     // which may still be in flight when step 0 starts.
