@@ -176,7 +176,8 @@ int mone_memory_kv(mone_ttl* h, const void* xq, int32_t q, void* kv, int32_t kv_
  *   out     [L][q][n_heads*dh] of out_dtype
  * n_heads must be a multiple of n_kv_heads and n_kv_heads must divide d_kv.  Uses nothing of
  * the handle but its shape (L, d_kv, act_dtype); q = 0 is a no-op.  The work is O(q^2) per
- * head (one query row per wavefront): it is meant for query batches, not for long prefills. */
+ * head (16 query rows per workgroup, keys in chunks of 32 of each set): it is meant for query
+ * batches, not for long prefills. */
 int mone_memory_attention(mone_ttl* h, const void* qh, const void* kh, const void* vh,
                           const void* kv_mem, int32_t kv_dtype, int32_t q, int32_t n_heads,
                           int32_t n_kv_heads, void* out, int32_t out_dtype, void* stream);
