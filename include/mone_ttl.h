@@ -88,8 +88,9 @@ typedef struct mone_ttl mone_ttl; /* opaque host object */
 
 /* Number of workspace bytes a handle for `cfg` needs.  It depends on L, d, h, d_kv, T, the
  * activation dtype and the optimiser only -- never on the context length N, which is not an
- * argument anywhere: the memory's footprint is constant in N (Sec. 4.3).  Returns 0 if `cfg` is
- * invalid or unsupported (mone_ttl_last_error() says why). */
+ * argument anywhere: the memory's footprint is constant in N (Sec. 4.3).  It includes a fixed
+ * 16 MiB area for split-contraction partial sums (short segments and query batches).  Returns 0
+ * if `cfg` is invalid or unsupported (mone_ttl_last_error() says why). */
 size_t mone_ttl_workspace_bytes(const mone_ttl_config* cfg);
 
 /* Create a handle over caller-owned state (the initial state W_0, s = 0 in Sec. 3.1).

@@ -106,6 +106,55 @@ hipError_t launch_tiled(const Spec* specs, int nspec, int layers, const Epi& epi
   return hipGetLastError();
 }
 
+// Split-K of short-row launches with few tiles: the raw accumulators of at most one 64 x 256
+// tile per CU.
+constexpr size_t kSplitFloats = (size_t)kNumCUs * 64 * 256;
+
+// Splits per tile for a single-problem 64 x 256 launch of `tiles` tiles (all layers) over
+// `nsteps` K steps: doubled up to 4 while the launch keeps at most one workgroup per CU and
+// every split at least 8 K steps.
+inline int split_for(long long tiles, int nsteps) {
+  int sp = 1;
+  while (sp < 4 && tiles * sp * 2 <= kNumCUs && nsteps / (sp * 2) >= 8) sp *= 2;
+  return sp;
+}
+
+// The two passes of a split-K launch (64 x 256 tiles, one problem): `split` workgroups per tile
+// on the deep ring, each over a range of K steps, store their accumulators to `part`; then one
+// workgroup per tile sums them in split order and runs the epilogue.
+template <typename E, class Epi>
+hipError_t launch_split(const Spec& spec, int layers, const Epi& epi, float* part, int split,
+                        hipStream_t s, int* tiles_per_layer) {
+  constexpr int BK = 8 * (16 / (int)sizeof(E));
+  if (spec.nparts < 1 || spec.nparts > Epi::kParts) return hipErrorInvalidValue;
+  GemmLaunch<Epi> G;
+  std::memset(&G, 0, sizeof G);
+  Problem& P = G.prob[0];
+  P.part[0] = spec.part[0];
+  P.part[1] = spec.part[1];
+  P.nparts = spec.nparts;
+  P.tiles_m = (spec.m_extent + 63) / 64;
+  P.tiles_n = (spec.n + 255) / 256;
+  P.M = spec.m_store >= 0 ? spec.m_store : P.tiles_m * 64;
+  P.N = spec.n_store >= 0 ? spec.n_store : P.tiles_n * 256;
+  P.tile_begin = 0;
+  const int tiles = P.tiles_m * P.tiles_n * layers;
+  if (tiles_per_layer) *tiles_per_layer = P.tiles_m * P.tiles_n;
+  if (tiles == 0) return hipSuccess;
+  if ((size_t)tiles * split * 64 * 256 > kSplitFloats) return hipErrorInvalidValue;
+  const int nsteps = (spec.part[0].k_len + (spec.nparts > 1 ? spec.part[1].k_len : 0)) / BK;
+  G.nprob = 1;
+  G.epi = epi;
+  G.part = part;
+  G.split = split;
+  G.split_steps = (nsteps + split - 1) / split;
+  gemm_nt_kernel<E, 64, 256, 1, Epi, 4, kSplitPartial><<<dim3(tiles * split), dim3(256), 0, s>>>(G);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  gemm_nt_kernel<E, 64, 256, 1, Epi, 0, kSplitReduce><<<dim3(tiles), dim3(256), 0, s>>>(G);
+  return hipGetLastError();
+}
+
 // Tiles per layer of a problem of m x n under tile shape t (what launch_gemm will use).
 inline int tiles_for(TileShape t, int m, int n) {
   const int bm = t == TILE_256x256 || t == TILE_256x64 ? 256 : t == TILE_128x128 ? 128 : 64;
@@ -113,9 +162,21 @@ inline int tiles_for(TileShape t, int m, int n) {
   return ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
 }
 
+// `split_part` (kSplitFloats floats, or null): single-problem deep-ring launches whose tiles
+// leave CUs idle split their contraction (launch_split).
 template <typename E, class Epi>
 hipError_t launch_gemm(TileShape t, const Spec* specs, int nspec, int layers, const Epi& epi,
-                       hipStream_t s, int* tiles_per_layer = nullptr) {
+                       hipStream_t s, int* tiles_per_layer = nullptr,
+                       float* split_part = nullptr) {
+  if (t == TILE_64x256_DEEP && split_part && nspec == 1) {
+    constexpr int BK = 8 * (16 / (int)sizeof(E));
+    const long long tiles =
+        (long long)((specs[0].m_extent + 63) / 64) * ((specs[0].n + 255) / 256) * layers;
+    const int nsteps =
+        (specs[0].part[0].k_len + (specs[0].nparts > 1 ? specs[0].part[1].k_len : 0)) / BK;
+    const int sp = split_for(tiles, nsteps);
+    if (sp > 1) return launch_split<E>(specs[0], layers, epi, split_part, sp, s, tiles_per_layer);
+  }
   switch (t) {
     case TILE_256x256:
       return launch_tiled<E, 256, 256, 2>(specs, nspec, layers, epi, s, tiles_per_layer);

@@ -131,11 +131,20 @@ struct Problem {
   int tile_begin;          // first workgroup of this problem in the launch
 };
 
+// Split-K passes of a single-problem launch (mode 0: the whole contraction, then the epilogue).
+enum SplitMode { kSplitNone = 0, kSplitPartial = 1, kSplitReduce = 2 };
+
 template <class Epi>
 struct GemmLaunch {
   Problem prob[2];
   int nprob;
   Epi epi;
+  // Split-K (kernels instantiated with MODE != kSplitNone): in the partial pass workgroup b
+  // takes split b / tiles of tile b % tiles, runs its split_steps K steps and stores its raw
+  // accumulators to part; in the reduce pass each tile sums its splits' accumulators in split
+  // order and runs the epilogue.
+  float* part;
+  int split, split_steps;
 };
 
 // ------------------------------------------------------------------------------------------
@@ -229,7 +238,8 @@ __device__ __forceinline__ void reads_then_interleave() {
   front_seq<NM, NRL - lead, NV>(std::make_integer_sequence<int, NM>{});
 }
 
-template <typename E, int BM, int BN, int WAVES_M, class Epi, int DEPTH = 0>
+template <typename E, int BM, int BN, int WAVES_M, class Epi, int DEPTH = 0,
+          int MODE = kSplitNone>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   using TC = TileCfg<BM, BN, DEPTH>;
   constexpr int VEC = 16 / (int)sizeof(E);   // elements per 16-byte vector
@@ -246,11 +256,16 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
 
   // Problem of this workgroup: problem 0's tiles come first.  (Alternating the two problems'
   // tiles across the launch was measured slower: each XCD's L2 then serves both working sets.)
-  const int bid = blockIdx.x;
-  const int first1 = G.nprob > 1 ? G.prob[1].tile_begin : (int)gridDim.x;
+  int bid = blockIdx.x, gx = (int)gridDim.x, split_i = 0;
+  if constexpr (MODE == kSplitPartial) {  // single problem: gridDim.x = split * tiles
+    gx /= G.split;
+    split_i = bid / gx;
+    bid -= split_i * gx;
+  }
+  const int first1 = G.nprob > 1 ? G.prob[1].tile_begin : gx;
   const int pi = bid >= first1 ? 1 : 0;
   const int local = bid - (pi ? first1 : 0);
-  const int total = pi ? (int)gridDim.x - first1 : first1;
+  const int total = pi ? gx - first1 : first1;
   const Problem& P = G.prob[pi];
   int layer, tm, tn;
   map_tile(local, total, P.tiles_m, P.tiles_n, &layer, &tm, &tn);
@@ -270,7 +285,14 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
 
   const int nk0 = P.part[0].k_len / BK;
   constexpr int NP = Epi::kParts;
-  const int nk = nk0 + (NP > 1 && P.nparts > 1 ? P.part[1].k_len / BK : 0);
+  // K steps [kbeg, nk) of this workgroup; loads of steps at or past nk read zeros.
+  int kbeg = 0, nk = nk0 + (NP > 1 && P.nparts > 1 ? P.part[1].k_len / BK : 0);
+  if constexpr (MODE == kSplitPartial) {
+    kbeg = split_i * G.split_steps;
+    nk = nk < kbeg + G.split_steps ? nk : kbeg + G.split_steps;
+  } else if constexpr (MODE == kSplitReduce) {
+    nk = 0;
+  }
 
   // Per part: buffer descriptors over this layer's operand slices, and each lane's byte offset
   // for each of its load instructions.  Lane l of load instruction i fills LDS row
@@ -391,13 +413,15 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     constexpr int VMD = (DEPTH - 2) * (LA + LB);
     static_assert(VMD < 64, "vmcnt range");
     constexpr int WAIT_D = (VMD & 15) | ((VMD >> 4) << 14) | (7 << 4);
-    if (nk > 0) {
+    if (nk > kbeg) {
       u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
-      // Prologue: steps 0 .. DEPTH - 2 (the part of each step chosen at run time here only).
+      // Prologue: steps kbeg .. kbeg + DEPTH - 2 into slots 0 .. DEPTH - 2 (the part of each
+      // step chosen at run time here only).
 #pragma unroll
       for (int j = 0; j < DEPTH - 1; ++j) {
-        if (j < nk0) { load_a(Part0{}, j, j, 0, LA); load_b(Part0{}, j, j, 0, LB); }
-        else { load_a(Part1{}, j, j, 0, LA); load_b(Part1{}, j, j, 0, LB); }
+        const int kj = kbeg + j;
+        if (kj < nk0) { load_a(Part0{}, kj, j, 0, LA); load_b(Part0{}, kj, j, 0, LB); }
+        else { load_a(Part1{}, kj, j, 0, LA); load_b(Part1{}, kj, j, 0, LB); }
       }
       __builtin_amdgcn_s_waitcnt(WAIT_D);
       asm volatile("" ::: "memory");
@@ -431,11 +455,12 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
         reads_then_interleave<NF, NM, 0>();
       };
       if constexpr (NP == 1) {
-        for (int kt = 0; kt < nk; ++kt) dstep(kt, Part0{});
+        for (int kt = kbeg; kt < nk; ++kt) dstep(kt, Part0{});
       } else {
         // both operands switch part when the loaded step reaches nk0
-        const int e1 = nk0 - (DEPTH - 1) < 0 ? 0 : (nk0 - (DEPTH - 1) > nk ? nk : nk0 - (DEPTH - 1));
-        int kt = 0;
+        const int sw = nk0 - (DEPTH - 1);
+        const int e1 = sw < kbeg ? kbeg : (sw > nk ? nk : sw);
+        int kt = kbeg;
         for (; kt < e1; ++kt) dstep(kt, Part0{});
         for (; kt < nk; ++kt) dstep(kt, Part1{});
       }
@@ -518,6 +543,34 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     }
     __builtin_amdgcn_s_waitcnt(0);  // the last (out-of-range) loads have retired
     __syncthreads();                // the epilogue reuses the LDS of the rings
+  }
+
+  // Split-K: accumulators in their register layout, lane-contiguous, per (split, tile, wave).
+  if constexpr (MODE != kSplitNone) {
+    constexpr int NACC = FM * FN * 16;
+    const long long tile_off = ((long long)local * 4 + wave) * NACC * 64 + lane;
+    const long long split_stride = (long long)total * 4 * NACC * 64;
+    if constexpr (MODE == kSplitPartial) {
+      float* dst = G.part + split_i * split_stride + tile_off;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            __builtin_nontemporal_store(acc[i][j][r], dst + ((i * FN + j) * 16 + r) * 64);
+      return;
+    }
+    for (int sp = 0; sp < G.split; ++sp) {  // reduce: splits summed in order
+      const float* src = G.part + sp * split_stride + tile_off;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            acc[i][j][r] += __builtin_nontemporal_load(src + ((i * FN + j) * 16 + r) * 64);
+    }
   }
 
   // ---- epilogue: each wave stages its own accumulators through LDS, 64 x 64 at a time

@@ -53,7 +53,7 @@ namespace {
 struct Layout {
   int Tp;
   int loss_per_layer;
-  size_t w1c, w2c, w2t, a, at, dst, g, gt, dzt, xt, loss_part, loss_out;
+  size_t w1c, w2c, w2t, a, at, dst, g, gt, dzt, xt, loss_part, loss_out, split;
   size_t rate, vpart, beta, norm1, norm2, ss1, ss2, scale1, scale2;  // paper optimiser
   size_t total;
 };
@@ -124,6 +124,7 @@ Layout make_layout(const mone_ttl_config* c) {
   L.xt = take(nl * d * Tp * E);
   L.loss_part = take(nl * (size_t)L.loss_per_layer * 4);
   L.loss_out = take(nl * 4);
+  L.split = take(kSplitFloats * 4);  // split-K partial accumulators (short segments, reads)
   if (c->optimizer == MONE_OPT_PAPER) {
     L.rate = take(nl * Tp * 4);
     L.vpart = take(nl * (Tp / kRateTokens) * 4);
@@ -221,7 +222,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     EpiFwd1<E> epi;
     epi.a = A; epi.at = At; epi.dst = dSt; epi.ls = lth; epi.h = h; epi.Tp = Tp; epi.n = n;
     H->timing_begin(MONE_STAGE_FWD1, s);
-    if ((e = launch_gemm<E>(pick_tile(n, h, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
+    if ((e = launch_gemm<E>(pick_tile(n, h, Lc), &sp, 1, Lc, epi, s, nullptr, H->at<float>(Ly.split))) != hipSuccess)
       return hip_fail(e, "launch FWD1");
     H->timing_end(MONE_STAGE_FWD1, s);
   }
@@ -257,7 +258,7 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     epi.rate = PAPER ? H->at<float>(Ly.rate) : nullptr;
     int tiles = 0;
     H->timing_begin(MONE_STAGE_FWD2, s);
-    if ((e = launch_gemm<E>(pick_tile(n, D, Lc), &sp, 1, Lc, epi, s, &tiles)) != hipSuccess)
+    if ((e = launch_gemm<E>(pick_tile(n, D, Lc), &sp, 1, Lc, epi, s, &tiles, H->at<float>(Ly.split))) != hipSuccess)
       return hip_fail(e, "launch FWD2");
     H->timing_end(MONE_STAGE_FWD2, s);
     if (!nip) H->last_loss_count = 4 * tiles;
@@ -375,7 +376,7 @@ int run_kv(mone_ttl* H, const void* xq, int q, void* kv, int kv_bf16, hipStream_
       EpiKv1<E> epi;
       epi.a = A; epi.ls = lth; epi.h = h;
       H->timing_begin(MONE_STAGE_KV1, s);
-      if ((e = launch_gemm<E>(pick_tile(qc, h, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
+      if ((e = launch_gemm<E>(pick_tile(qc, h, Lc), &sp, 1, Lc, epi, s, nullptr, H->at<float>(Ly.split))) != hipSuccess)
         return hip_fail(e, "launch KV1");
       H->timing_end(MONE_STAGE_KV1, s);
     }
@@ -392,7 +393,7 @@ int run_kv(mone_ttl* H, const void* xq, int q, void* kv, int kv_bf16, hipStream_
       EpiKv2 epi;
       epi.kv = kvc; epi.ls = (long long)q * D; epi.D = D; epi.bf16_out = kv_bf16;
       H->timing_begin(MONE_STAGE_KV2, s);
-      if ((e = launch_gemm<E>(pick_tile(qc, D, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
+      if ((e = launch_gemm<E>(pick_tile(qc, D, Lc), &sp, 1, Lc, epi, s, nullptr, H->at<float>(Ly.split))) != hipSuccess)
         return hip_fail(e, "launch KV2");
       H->timing_end(MONE_STAGE_KV2, s);
     }
