@@ -21,6 +21,10 @@ pytestmark = pytest.mark.gpu
 SMALL = configs.MoneConfig("inv_bf16", n_layers=3, d_model=128, d_hidden=192, d_kv=64,
                            seg_len=160, n_context=640, act_dtype="bf16", lr=5e-2)
 SMALL_F32 = SMALL.with_(name="inv_f32", act_dtype="f32")
+# 64-token segments: the forward launches split their contraction over several workgroups
+# per tile (2 for Z = X W1^T, 2 for the two-part K2, one split straddling its part boundary)
+SHORT_F32 = configs.MoneConfig("inv_short_f32", n_layers=3, d_model=512, d_hidden=384,
+                               d_kv=128, seg_len=64, n_context=256, act_dtype="f32", lr=2e-2)
 
 
 @pytest.fixture(scope="module")
@@ -61,7 +65,7 @@ def test_lr_zero_and_empty_segment_leave_weights_bitwise(torch, cfg):
     sess.close()
 
 
-@pytest.mark.parametrize("cfg", [SMALL, SMALL_F32], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", [SMALL, SMALL_F32, SHORT_F32], ids=lambda c: c.name)
 def test_runs_are_deterministic_and_layers_independent(torch, cfg):
     print(f"[inv] determinism/locality {cfg.name}", flush=True)
     prob = DeviceProblem(cfg, [0])

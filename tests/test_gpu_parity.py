@@ -26,6 +26,10 @@ RAGGED_BF16 = RAGGED_F32.with_(name="ragged_bf16", act_dtype="bf16")
 MEAN_F32 = RAGGED_F32.with_(name="mean_f32", loss="mse_mean", lr=1.0)
 NIP_F32 = RAGGED_F32.with_(name="nip_f32", loss="nip", lr=5e-3)
 NIP_BF16 = NIP_F32.with_(name="nip_bf16", act_dtype="bf16")
+# segments of at most 64 tokens in fp32, shaped so that the forward launches and the read's
+# first GEMM split their contraction (one split of K2 straddles its two parts)
+SHORT_F32 = C("short_f32", n_layers=3, d_model=512, d_hidden=384, d_kv=128, seg_len=64,
+              n_context=234, act_dtype="f32", lr=2e-2)
 
 # name -> (config, checked layers, tokens per segment)
 CASES = {
@@ -41,6 +45,7 @@ CASES = {
     "3b": (configs.THREE_B, [0, 27], [1024] * 2),
     "8b": (configs.EIGHT_B, [0, 31], [2048] * 2),
     "stress": (configs.STRESS, [0, 15], [64] * 32),
+    "short_f32": (SHORT_F32, [0, 2], [64, 64, 37, 64, 5]),
 }
 
 
