@@ -100,7 +100,9 @@ int mone_swiglu_init(mone_swiglu** out, const mone_swiglu_config* cfg,
  *   x         [L][n_tokens][d] act_dtype.
  *   n_tokens  0 <= n_tokens <= seg_len; 0 is a no-op.  Positions restart at 0 in every
  *             segment.
- * Segments must be enqueued in context order. */
+ * Segments must be enqueued in context order.  The call enqueues kernels only (no allocation,
+ * memset or synchronisation) and keeps no state that alternates between calls, so one call may
+ * be captured in a HIP graph (timing hooks off) and replayed once per segment. */
 int mone_swiglu_segment(mone_swiglu* h, const void* x, int32_t n_tokens, void* stream);
 
 /* The segment loss L_s of the last non-empty segment, per layer, at the weights that step

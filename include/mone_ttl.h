@@ -146,7 +146,12 @@ int mone_ttl_init_paper(mone_ttl** out, const mone_ttl_config* cfg, const void* 
  * G = c R, W2 -= lr G^T A, W1 -= lr ((G W2) * SiLU'(Z))^T X, both gradients at the weights
  * the call started from.  All L layers run as one grouped launch per stage.  Segments must be
  * enqueued in context order (Sec. 3.4: W_0 -> W_1 -> ... -> W_S); `x` may be reused or freed
- * once the enqueued work has completed on `stream`. */
+ * once the enqueued work has completed on `stream`.
+ * Graph capture: the call enqueues kernels only (no allocation, memset or synchronisation), so
+ * it may be captured in a HIP graph, with the timing hooks off.  Consecutive calls alternate
+ * between two internal copies of W2^T (the backward reads the previous one while the update
+ * writes the next), so a graph must capture an even number of consecutive calls with the same
+ * n_tokens; replaying it then continues the handle's sequence, and eager calls may follow. */
 int mone_ttl_segment(mone_ttl* h, const void* x, int32_t n_tokens, void* stream);
 
 /* Read of the current state on query-side inputs, without any update (Eq. read; Sec. 3.4):
