@@ -384,8 +384,10 @@ def run_swiglu(args):
         "flop_per_token": flop_tok,
         "roofline": roof,
         "stages": stages,
-        "stage_timing": "stages: one untimed profiling step, every stage timed; roofline: the "
-                        "dominant stage over the timed steps",
+        "stage_timing": ("stages: one untimed profiling step, every stage timed; roofline: the "
+                         "dominant stage over the timed steps") if graph is None else
+                        ("timed steps: replays of the step captured in a HIP graph; stages and "
+                         "roofline: one eager profiling step, every stage timed"),
         "finite": finite,
     }
     if cpu_in is not None:
@@ -418,6 +420,10 @@ def main():
                          "paper's optimiser for the paper-form memory (whose negative inner "
                          "product loss is unbounded below: plain SGD lets the weights grow "
                          "without limit over a long context)")
+    ap.add_argument("--graph", action="store_true",
+                    help="configurations' memory: capture one whole step (its segment calls, "
+                         "the read and the attention) in a HIP graph and time its replays; the "
+                         "segment count must be even (the W2^T copies alternate per segment)")
     ap.add_argument("--memory", default="config", choices=("config", "swiglu"),
                     help="config: the configurations' 2-layer memory (default); swiglu: the "
                          "paper-form SwiGLU memory per fast-weight head at the paper's shape")
@@ -492,16 +498,26 @@ def main():
     H = sess.handle
     sptr = stream.cuda_stream
 
-    def step():
+    def step(sp=sptr):
         for s in range(S):
-            mone.mone_ttl_segment(H, ctx[s], T, sptr)
-        mone.mone_memory_kv(H, xq, Q, kv, mone.MONE_F32, sptr)
+            mone.mone_ttl_segment(H, ctx[s], T, sp)
+        mone.mone_memory_kv(H, xq, Q, kv, mone.MONE_F32, sp)
         mone.mone_memory_attention(H, aq, ak, av, kv, mone.MONE_F32, Q, hq, hkv, aout,
-                                   mone.MONE_F32, sptr)
+                                   mone.MONE_F32, sp)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    graph = None
+    if args.graph:
+        if S % 2:
+            print("bench.py: --graph needs an even number of segments", file=sys.stderr,
+                  flush=True)
+            sys.exit(2)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):  # timing hooks are off here
+            step(torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
     if args.calib_copy_mib:
         nb = args.calib_copy_mib << 20
         src = torch.empty(nb, dtype=torch.uint8, device=dev)
@@ -510,9 +526,25 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    elapsed, stimes, dom, (dms, dcnt) = timed_steps(
-        step, args.steps, lambda n, m: mone.mone_ttl_set_stage_timing(H, n, m),
-        lambda: mone.mone_ttl_stage_times(H), mone.STAGES, S * 7 + 3)
+    if graph is None:
+        elapsed, stimes, dom, (dms, dcnt) = timed_steps(
+            step, args.steps, lambda n, m: mone.mone_ttl_set_stage_timing(H, n, m),
+            lambda: mone.mone_ttl_stage_times(H), mone.STAGES, S * 7 + 3)
+    else:
+        # the stage table and the roofline come from one eager profiling step; the timed steps
+        # are replays of the captured step
+        mone.mone_ttl_set_stage_timing(H, S * 7 + 3, 0xFFFFFFFF)
+        step()
+        torch.cuda.synchronize()
+        stimes = mone.mone_ttl_stage_times(H)
+        mone.mone_ttl_set_stage_timing(H, 0, 0)
+        dom = max((n for n in stimes if stimes[n][1]), key=lambda n: stimes[n][0])
+        dms, dcnt = stimes[dom]
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
     finite = bool(torch.isfinite(w1).all().item() and torch.isfinite(w2).all().item()
                   and torch.isfinite(kv).all().item())
     sess.close()
@@ -542,7 +574,8 @@ def main():
         "config": {"workload": f"{cfg.name}-class TTL: L={L} d={d} h={h} D={D} T={T} "
                                f"N={S * T} ({S} segments) + read Q={Q}"
                                + (", paper optimiser" if cfg.optimizer == "paper" else "")
-                               + (f", loss {cfg.loss}" if args.loss else ""),
+                               + (f", loss {cfg.loss}" if args.loss else "")
+                               + (", HIP graph replay" if graph is not None else ""),
                    "n_layers": L, "d_model": d, "d_hidden": h, "d_out": D, "seg_len": T,
                    "n_context": S * T, "n_query": Q, "lr": cfg.lr, "optimizer": cfg.optimizer,
                    "loss": cfg.loss},
@@ -550,8 +583,10 @@ def main():
         "flop_per_token": flop_tok,
         "roofline": roof,
         "stages": stages,
-        "stage_timing": "stages: one untimed profiling step, every stage timed; roofline: the "
-                        "dominant stage over the timed steps",
+        "stage_timing": ("stages: one untimed profiling step, every stage timed; roofline: the "
+                         "dominant stage over the timed steps") if graph is None else
+                        ("timed steps: replays of the step captured in a HIP graph; stages and "
+                         "roofline: one eager profiling step, every stage timed"),
         "finite": finite,
     }
     if cpu_in is not None:
