@@ -21,8 +21,12 @@ RAGGED_F32_P = C("ragged_f32_paper", n_layers=3, d_model=192, d_hidden=320, d_kv
 RAGGED_BF16_P = RAGGED_F32_P.with_(name="ragged_bf16_paper", act_dtype="bf16")
 MEAN_F32_P = RAGGED_F32_P.with_(name="mean_f32_paper", loss="mse_mean", lr=2.0)
 
+# segments of at most 64 tokens in fp32: the forward launches split their contraction
+SHORT_F32_P = C("short_f32_paper", n_layers=3, d_model=512, d_hidden=384, d_kv=128, seg_len=64,
+                n_context=234, act_dtype="f32", lr=2e-2, optimizer="paper")
 CASES = {
     "tiny_paper": (TINY_P, [0], [128] * 6),
+    "short_f32_paper": (SHORT_F32_P, [0, 2], [64, 64, 37, 64, 5]),
     "ragged_f32_paper": (RAGGED_F32_P, [0, 2], [200, 137, 64, 1, 200, 77]),
     "ragged_bf16_paper": (RAGGED_BF16_P, [0, 2], [200, 137, 64, 1, 200, 77]),
     "mean_f32_paper": (MEAN_F32_P, [1], [200, 150, 200]),

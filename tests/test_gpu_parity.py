@@ -46,6 +46,9 @@ CASES = {
     "8b": (configs.EIGHT_B, [0, 31], [2048] * 2),
     "stress": (configs.STRESS, [0, 15], [64] * 32),
     "short_f32": (SHORT_F32, [0, 2], [64, 64, 37, 64, 5]),
+    # the negative inner product: K2 is the targets alone (one K part), split in two
+    "short_nip_f32": (SHORT_F32.with_(name="short_nip_f32", loss="nip", lr=5e-3), [0, 2],
+                      [64, 64, 37, 64, 5]),
 }
 
 
