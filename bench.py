@@ -384,10 +384,8 @@ def run_swiglu(args):
         "flop_per_token": flop_tok,
         "roofline": roof,
         "stages": stages,
-        "stage_timing": ("stages: one untimed profiling step, every stage timed; roofline: the "
-                         "dominant stage over the timed steps") if graph is None else
-                        ("timed steps: replays of the step captured in a HIP graph; stages and "
-                         "roofline: one eager profiling step, every stage timed"),
+        "stage_timing": "stages: one untimed profiling step, every stage timed; roofline: the "
+                        "dominant stage over the timed steps",
         "finite": finite,
     }
     if cpu_in is not None:
