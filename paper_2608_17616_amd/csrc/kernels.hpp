@@ -16,7 +16,10 @@
 // the 16-byte column slot of row r is XOR-swizzled by (r / 2) % 8, which each lane applies by
 // choosing its source address, so fragment reads of 32 consecutive rows are free of bank
 // conflicts.  The loads of later K steps are spread over the MFMAs of the current one, and each
-// wave reads its fragments one sub-step ahead of the MFMAs that use them.
+// wave reads its fragments one sub-step ahead of the MFMAs that use them.  Launches with at most
+// one tile per CU use a deep ring instead (4 slots per operand, both 3 steps ahead), and may
+// split each tile's K steps over several workgroups: a partial pass stores raw accumulators,
+// and a reduce pass sums them in split order before the epilogue.
 //
 // MFMA: bf16 uses v_mfma_f32_32x32x16_bf16 (one 16-byte fragment per lane = 8 k-values), fp32
 // uses four v_mfma_f32_32x32x2_f32 on the four floats of the same 16-byte fragment.  Within a
