@@ -148,7 +148,8 @@ hipError_t launch_split(const Spec& spec, int layers, const Epi& epi, float* par
   G.part = part;
   G.split = split;
   G.split_steps = (nsteps + split - 1) / split;
-  gemm_nt_kernel<E, 64, 256, 1, Epi, 4, kSplitPartial><<<dim3(tiles * split), dim3(256), 0, s>>>(G);
+  gemm_nt_kernel<E, 64, 256, 1, Epi, 4, kSplitPartial>
+      <<<dim3(tiles * split), dim3(256), 0, s>>>(G);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   gemm_nt_kernel<E, 64, 256, 1, Epi, 0, kSplitReduce><<<dim3(tiles), dim3(256), 0, s>>>(G);

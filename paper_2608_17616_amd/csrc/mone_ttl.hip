@@ -222,7 +222,8 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     EpiFwd1<E> epi;
     epi.a = A; epi.at = At; epi.dst = dSt; epi.ls = lth; epi.h = h; epi.Tp = Tp; epi.n = n;
     H->timing_begin(MONE_STAGE_FWD1, s);
-    if ((e = launch_gemm<E>(pick_tile(n, h, Lc), &sp, 1, Lc, epi, s, nullptr, H->at<float>(Ly.split))) != hipSuccess)
+    if ((e = launch_gemm<E>(pick_tile(n, h, Lc), &sp, 1, Lc, epi, s, nullptr,
+                            H->at<float>(Ly.split))) != hipSuccess)
       return hip_fail(e, "launch FWD1");
     H->timing_end(MONE_STAGE_FWD1, s);
   }
@@ -258,7 +259,8 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
     epi.rate = PAPER ? H->at<float>(Ly.rate) : nullptr;
     int tiles = 0;
     H->timing_begin(MONE_STAGE_FWD2, s);
-    if ((e = launch_gemm<E>(pick_tile(n, D, Lc), &sp, 1, Lc, epi, s, &tiles, H->at<float>(Ly.split))) != hipSuccess)
+    if ((e = launch_gemm<E>(pick_tile(n, D, Lc), &sp, 1, Lc, epi, s, &tiles,
+                            H->at<float>(Ly.split))) != hipSuccess)
       return hip_fail(e, "launch FWD2");
     H->timing_end(MONE_STAGE_FWD2, s);
     if (!nip) H->last_loss_count = 4 * tiles;
@@ -376,7 +378,8 @@ int run_kv(mone_ttl* H, const void* xq, int q, void* kv, int kv_bf16, hipStream_
       EpiKv1<E> epi;
       epi.a = A; epi.ls = lth; epi.h = h;
       H->timing_begin(MONE_STAGE_KV1, s);
-      if ((e = launch_gemm<E>(pick_tile(qc, h, Lc), &sp, 1, Lc, epi, s, nullptr, H->at<float>(Ly.split))) != hipSuccess)
+      if ((e = launch_gemm<E>(pick_tile(qc, h, Lc), &sp, 1, Lc, epi, s, nullptr,
+                              H->at<float>(Ly.split))) != hipSuccess)
         return hip_fail(e, "launch KV1");
       H->timing_end(MONE_STAGE_KV1, s);
     }
@@ -393,7 +396,8 @@ int run_kv(mone_ttl* H, const void* xq, int q, void* kv, int kv_bf16, hipStream_
       EpiKv2 epi;
       epi.kv = kvc; epi.ls = (long long)q * D; epi.D = D; epi.bf16_out = kv_bf16;
       H->timing_begin(MONE_STAGE_KV2, s);
-      if ((e = launch_gemm<E>(pick_tile(qc, D, Lc), &sp, 1, Lc, epi, s, nullptr, H->at<float>(Ly.split))) != hipSuccess)
+      if ((e = launch_gemm<E>(pick_tile(qc, D, Lc), &sp, 1, Lc, epi, s, nullptr,
+                              H->at<float>(Ly.split))) != hipSuccess)
         return hip_fail(e, "launch KV2");
       H->timing_end(MONE_STAGE_KV2, s);
     }
