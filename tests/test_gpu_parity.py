@@ -46,6 +46,10 @@ CASES = {
     "8b": (configs.EIGHT_B, [0, 31], [2048] * 2),
     "stress": (configs.STRESS, [0, 15], [64] * 32),
     "short_f32": (SHORT_F32, [0, 2], [64, 64, 37, 64, 5]),
+    # the longest supported segment, then a ragged one (1024-step weight-gradient contractions)
+    "longest_f32": (C("longest_f32", n_layers=2, d_model=64, d_hidden=128, d_kv=64,
+                      seg_len=65536, n_context=105536, act_dtype="f32", lr=1e-2), [0, 1],
+                    [65536, 40000]),
     # the negative inner product: K2 is the targets alone (one K part), split in two
     "short_nip_f32": (SHORT_F32.with_(name="short_nip_f32", loss="nip", lr=5e-3), [0, 2],
                       [64, 64, 37, 64, 5]),

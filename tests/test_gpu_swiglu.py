@@ -150,6 +150,18 @@ def test_fp32_odd_head_width_and_short_segments():
     _check(p, [0], 1e-4, 1e-4)
 
 
+def test_fp32_longest_segment():
+    """The longest supported segment (65536 tokens: RoPE positions up to 65535, 1024-step
+    weight-gradient contractions), then a ragged one."""
+    cfg = configs.SwigluConfig("sw_long", n_layers=1, d_model=128, n_heads=2, d_head=64,
+                               seg_len=65536, n_context=105536, act_dtype="f32", lr=1.0,
+                               optimizer="paper")
+    p = SwProblem(cfg)
+    for s, n in enumerate([65536, 40000]):
+        p.segment(s, n)
+    _check(p, [0], 1e-4, 1e-4)
+
+
 def test_empty_segment_is_a_no_op_and_loss_needs_a_segment():
     cfg = configs.SW_TINY
     p = SwProblem(cfg)
