@@ -1150,37 +1150,6 @@ __device__ __forceinline__ float softplusf_(float z) {
   return fmaxf(z, 0.0f) + log1pf(__expf(-fabsf(z)));
 }
 
-// Dot products of a row of n_el elements with a float vector, summed by a whole wave in a fixed
-// order (lane-strided 8-element chunks, then a xor tree).
-template <typename E>
-__device__ __forceinline__ void wave_dot2(const E* __restrict__ row, const float* __restrict__ u,
-                                          const float* __restrict__ v, int n_el, int lane,
-                                          float* pu, float* pv) {
-  float su = 0.0f, sv = 0.0f;
-  for (int c = lane * 8; c < n_el; c += 64 * 8) {
-    float x[8];
-    if constexpr (sizeof(E) == 2) {
-      load8(reinterpret_cast<const bf16_t*>(row) + c, x);
-    } else {
-      const float4 a = *reinterpret_cast<const float4*>(row + c);
-      const float4 b = *reinterpret_cast<const float4*>(row + c + 4);
-      x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      su += x[e] * u[c + e];
-      sv += x[e] * v[c + e];
-    }
-  }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    su += __shfl_xor(su, off, 64);
-    sv += __shfl_xor(sv, off, 64);
-  }
-  *pu = su;
-  *pv = sv;
-}
-
 // Per-token rates rate[l][j] = lr * softplus(u_l . x_j + b_u[l]) for j < n (0 for n <= j < Tp),
 // and per-block sums of v_l . x_j over the block's kRateTokens tokens (summed in token order),
 // from which decay_kernel forms the momentum decay.  Grid (Tp / kRateTokens, L), 256 threads:
@@ -1197,16 +1166,51 @@ __global__ __launch_bounds__(256) void rate_kernel(const E* __restrict__ x, long
   const int l = blockIdx.y, j0 = blockIdx.x * kRateTokens, wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   __shared__ float wsum[4];
+  // This wave's TW tokens side by side: per 8-element chunk of the lane, u and v are read once
+  // and the TW tokens' loads are issued together (each token's sums keep the chunk order).
+  const E* xl = x + (long long)l * x_ls;
+  const float* ul = u + (long long)l * d;
+  const float* vl = v + (long long)l * d;
+  const int jw = j0 + wave * TW;
+  float su[TW], sv[TW];
+#pragma unroll
+  for (int t = 0; t < TW; ++t) su[t] = sv[t] = 0.0f;
+  for (int c = lane * 8; c < d; c += 64 * 8) {
+    float uu[8], vv[8], xv[TW][8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uu[e] = ul[c + e];
+      vv[e] = vl[c + e];
+    }
+#pragma unroll
+    for (int t = 0; t < TW; ++t) {
+      if (jw + t < n) {
+        load8(xl + (long long)(jw + t) * d + c, xv[t]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xv[t][e] = 0.0f;
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < TW; ++t)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        su[t] += xv[t][e] * uu[e];
+        sv[t] += xv[t][e] * vv[e];
+      }
+  }
   float acc = 0.0f;
+#pragma unroll
   for (int t = 0; t < TW; ++t) {
-    const int j = j0 + wave * TW + t;
-    float pu = 0.0f, pv = 0.0f;
-    if (j < n)
-      wave_dot2(x + (long long)l * x_ls + (long long)j * d, u + (long long)l * d,
-                v + (long long)l * d, d, lane, &pu, &pv);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      su[t] += __shfl_xor(su[t], off, 64);
+      sv[t] += __shfl_xor(sv[t], off, 64);
+    }
+    const int j = jw + t;
     if (lane == 0) {
-      rate[(long long)l * Tp + j] = j < n ? lr * softplusf_(pu + bu[l]) : 0.0f;
-      acc += pv;
+      rate[(long long)l * Tp + j] = j < n ? lr * softplusf_(su[t] + bu[l]) : 0.0f;
+      acc += j < n ? sv[t] : 0.0f;
     }
   }
   if (lane == 0) wsum[wave] = acc;
