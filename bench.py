@@ -100,37 +100,68 @@ def counted_traffic(stage, record="hbm_traffic_8b.json"):
         return None
 
 
+class _HostThreads:
+    """The oracle's BLAS thread count for the CPU baseline: the host's share of cores for this
+    job (the affinity mask, capped by OMP_NUM_THREADS), set for the duration of the block."""
+
+    def __enter__(self):
+        self.affinity = len(os.sched_getaffinity(0))
+        env = os.environ.get("OMP_NUM_THREADS", "")
+        self.cores = min(self.affinity, int(env)) if env.isdigit() and int(env) > 0 \
+            else self.affinity
+        try:
+            from threadpoolctl import threadpool_limits
+            self._lim = threadpool_limits(limits=self.cores, user_api="blas")
+        except Exception:  # pragma: no cover
+            self._lim = None
+        return self
+
+    def __exit__(self, *exc):
+        if self._lim is not None:
+            self._lim.restore_original_limits()
+        return False
+
+    def record(self, value, t, done, cfg):
+        return {"value": value, "unit": "tokens/s", "cores": int(self.cores), "kind": "oracle",
+                "sample": f"layer 0, {done} consecutive segments of T={cfg.seg_len} tokens "
+                          f"({t:.1f} s, float64 NumPy), scaled to {cfg.n_layers} layers",
+                "affinity_cores": int(self.affinity), "cpu_model": _cpu_model()}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(cfg, w1, w2, wkv, xs, budget_s, meta=None):
     import numpy as np
 
     import oracle as orc
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()
-                     if i.get("user_api") == "blas"] or [1])
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count() or 1
-    w1 = np.asarray(w1, np.float64)
-    w2 = np.asarray(w2, np.float64)
-    if meta is not None:
-        norms0 = (orc.row_norms(w1), orc.row_norms(w2))
-        m1, m2 = np.zeros_like(w1), np.zeros_like(w2)
-    done, t0 = 0, time.perf_counter()
-    while True:
-        x = xs[done % len(xs)]
-        if meta is None:
-            w1, w2, _ = orc.ttl_step(x, w1, w2, wkv, cfg.lr, cfg.loss)
-        else:
-            w1, w2, m1, m2, _, _ = orc.paper_step(x, w1, w2, m1, m2, wkv, meta, norms0, cfg.lr,
-                                                  cfg.loss)
-        done += 1
-        if time.perf_counter() - t0 >= budget_s or done >= 64:
-            break
-    t = time.perf_counter() - t0
-    tok_s = done * cfg.seg_len / t / cfg.n_layers
-    return {"value": tok_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"layer 0, {done} consecutive segments of T={cfg.seg_len} tokens "
-                      f"({t:.1f} s, float64 NumPy), scaled to {cfg.n_layers} layers"}
+    with _HostThreads() as ht:
+        w1 = np.asarray(w1, np.float64)
+        w2 = np.asarray(w2, np.float64)
+        if meta is not None:
+            norms0 = (orc.row_norms(w1), orc.row_norms(w2))
+            m1, m2 = np.zeros_like(w1), np.zeros_like(w2)
+        done, t0 = 0, time.perf_counter()
+        while True:
+            x = xs[done % len(xs)]
+            if meta is None:
+                w1, w2, _ = orc.ttl_step(x, w1, w2, wkv, cfg.lr, cfg.loss)
+            else:
+                w1, w2, m1, m2, _, _ = orc.paper_step(x, w1, w2, m1, m2, wkv, meta, norms0,
+                                                      cfg.lr, cfg.loss)
+            done += 1
+            if time.perf_counter() - t0 >= budget_s or done >= 64:
+                break
+        t = time.perf_counter() - t0
+        return ht.record(done * cfg.seg_len / t / cfg.n_layers, t, done, cfg)
 
 
 def sw_stage_work(cfg):
@@ -226,35 +257,27 @@ def sw_cpu_baseline(cfg, host, xs, budget_s, meta):
     import numpy as np
 
     import oracle.swiglu_memory as sw
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()
-                     if i.get("user_api") == "blas"] or [1])
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count() or 1
-    proj, scale, shift, fast = host
-    d = cfg.d_model
-    frozen = dict(p_k=proj[:d], p_v=proj[d:], scale=scale, shift=shift)
-    fast = tuple(np.asarray(w, np.float64) for w in fast)
-    if meta is not None:
-        norms0 = sw.initial_norms(fast)
-        mom = tuple(np.zeros_like(w) for w in fast)
-    done, t0 = 0, time.perf_counter()
-    while True:
-        x = xs[done % len(xs)]
-        if meta is None:
-            fast, _ = sw.sgd_step(x, fast, frozen, cfg.lr, cfg.n_heads, cfg.rope_base)
-        else:
-            fast, mom, _, _ = sw.paper_step(x, fast, mom, frozen, meta, norms0, cfg.lr,
-                                            cfg.n_heads, cfg.rope_base)
-        done += 1
-        if time.perf_counter() - t0 >= budget_s or done >= 256:
-            break
-    t = time.perf_counter() - t0
-    return {"value": done * cfg.seg_len / t / cfg.n_layers, "unit": "tokens/s",
-            "cores": int(cores), "kind": "oracle",
-            "sample": f"layer 0, {done} consecutive segments of T={cfg.seg_len} tokens "
-                      f"({t:.1f} s, float64 NumPy), scaled to {cfg.n_layers} layers"}
+    with _HostThreads() as ht:
+        proj, scale, shift, fast = host
+        d = cfg.d_model
+        frozen = dict(p_k=proj[:d], p_v=proj[d:], scale=scale, shift=shift)
+        fast = tuple(np.asarray(w, np.float64) for w in fast)
+        if meta is not None:
+            norms0 = sw.initial_norms(fast)
+            mom = tuple(np.zeros_like(w) for w in fast)
+        done, t0 = 0, time.perf_counter()
+        while True:
+            x = xs[done % len(xs)]
+            if meta is None:
+                fast, _ = sw.sgd_step(x, fast, frozen, cfg.lr, cfg.n_heads, cfg.rope_base)
+            else:
+                fast, mom, _, _ = sw.paper_step(x, fast, mom, frozen, meta, norms0, cfg.lr,
+                                                cfg.n_heads, cfg.rope_base)
+            done += 1
+            if time.perf_counter() - t0 >= budget_s or done >= 256:
+                break
+        t = time.perf_counter() - t0
+        return ht.record(done * cfg.seg_len / t / cfg.n_layers, t, done, cfg)
 
 
 def run_swiglu(args):

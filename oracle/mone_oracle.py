@@ -23,19 +23,26 @@ of the paper's richer defaults; each choice is stated where it is made):
     L_s = (1/T) sum_j l_j (the segment-level average of Sec. 3.3).
   * update: W_s = W_{s-1} - lr * grad L_s(W_{s-1})  (Eq. update with mu_s = lr * gradient).
 
+Two test-only memories run through the same step code, so that closed forms can pin it:
+  * activation = "identity": M(x) = W2 W1 x, the 2-layer memory with a linear hidden layer;
+  * w1 = None: the linear memory M(x) = W2 x with one matrix W2 of shape [D, d].
+Neither is part of the method; the kernels implement the SiLU memory only.
+
 Everything is float64 NumPy.  Matrix products use numpy's matmul as a library primitive; there is
 no blocking, fusion or reordering beyond the definitions.
 
 Pins (tests in tests/test_oracle_*.py): hand-derived scalar case, central finite differences,
-torch.autograd (float64, CPU), brute-force loops, first-order descent, and invariants (lr = 0,
-zero residual, token duplication under the segment average, segment order, incremental ==
-one-shot, layer independence).
+torch.autograd (float64, CPU), brute-force loops, first-order descent, closed forms of the linear
+and identity-activation memories (one step in Gram-matrix form, the fixed point W -> W_kv and its
+contraction rate), and invariants (lr = 0, zero residual, token duplication under the segment
+average, segment order, incremental == one-shot, layer independence).
 """
 from __future__ import annotations
 
 import numpy as np
 
 LOSSES = ("mse_sum", "mse_mean", "nip")
+ACTIVATIONS = ("silu", "identity")  # "identity" is test-only
 
 
 def sigmoid(z):
@@ -62,12 +69,34 @@ def _f64(a):
     return np.asarray(a, dtype=np.float64)
 
 
-def memory_forward(x, w1, w2):
+def _act(z, activation: str):
+    """Hidden-layer activation: SiLU (the method), or the identity (test only)."""
+    if activation == "silu":
+        return silu(z)
+    if activation == "identity":
+        return z
+    raise ValueError(activation)
+
+
+def _act_grad(z, activation: str):
+    """Derivative of the hidden-layer activation at z."""
+    if activation == "silu":
+        return silu_grad(z)
+    if activation == "identity":
+        return np.ones_like(z)
+    raise ValueError(activation)
+
+
+def memory_forward(x, w1, w2, activation: str = "silu"):
     """Memory MLP on the rows of x ([n, d]): returns (Z, A, Y) with
-    Z = x W1^T ([n, h]), A = SiLU(Z), Y = A W2^T ([n, D]) -- i.e. y_j = W2 SiLU(W1 x_j)."""
-    x, w1, w2 = _f64(x), _f64(w1), _f64(w2)
-    z = x @ w1.T
-    a = silu(z)
+    Z = x W1^T ([n, h]), A = SiLU(Z), Y = A W2^T ([n, D]) -- i.e. y_j = W2 SiLU(W1 x_j).
+    With w1 = None (test only) the memory is the linear map y_j = W2 x_j: Z = A = x."""
+    x, w2 = _f64(x), _f64(w2)
+    if w1 is None:
+        z = a = x
+    else:
+        z = x @ _f64(w1).T
+        a = _act(z, activation)
     y = a @ w2.T
     return z, a, y
 
@@ -116,7 +145,7 @@ def segment_loss(x, w1, w2, wkv, loss: str = "mse_sum") -> float:
     return float(np.sum(_per_token_loss(y, targets(x, wkv), loss)) / n)
 
 
-def segment_grad(x, w1, w2, wkv, loss: str = "mse_sum"):
+def segment_grad(x, w1, w2, wkv, loss: str = "mse_sum", activation: str = "silu"):
     """Gradient of L_s with respect to this layer's own fast weights only (Sec. 3.4).
 
     Returns (dL/dW1 [h, d], dL/dW2 [D, h], L_s).  Backpropagation through the two matrices:
@@ -124,36 +153,41 @@ def segment_grad(x, w1, w2, wkv, loss: str = "mse_sum"):
       dL/dW2 = G^T A
       dZ = (G W2) * SiLU'(Z)
       dL/dW1 = dZ^T x
-    An empty segment has no tokens and contributes a zero gradient.
+    An empty segment has no tokens and contributes a zero gradient.  The test-only linear memory
+    (w1 = None) has no first matrix, so its dL/dW1 is None.
     """
-    x, w1, w2, wkv = _f64(x), _f64(w1), _f64(w2), _f64(wkv)
+    x, w2, wkv = _f64(x), _f64(w2), _f64(wkv)
     n = x.shape[0]
     if n == 0:
-        return np.zeros_like(w1), np.zeros_like(w2), 0.0
-    z, a, y = memory_forward(x, w1, w2)
+        return (None if w1 is None else np.zeros_like(_f64(w1))), np.zeros_like(w2), 0.0
+    z, a, y = memory_forward(x, w1, w2, activation)
     t = targets(x, wkv)
     c = _loss_scale(n, w2.shape[0], loss)
     g = _output_grad(y, t, c, loss)
     gw2 = g.T @ a
-    dz = (g @ w2) * silu_grad(z)
-    gw1 = dz.T @ x
+    gw1 = None
+    if w1 is not None:
+        dz = (g @ w2) * _act_grad(z, activation)
+        gw1 = dz.T @ x
     return gw1, gw2, float(np.sum(_per_token_loss(y, t, loss)) / n)
 
 
-def ttl_step(x, w1, w2, wkv, lr: float, loss: str = "mse_sum"):
+def ttl_step(x, w1, w2, wkv, lr: float, loss: str = "mse_sum", activation: str = "silu"):
     """One test-time-learning step of one layer on one segment (Eq. update):
     both matrices move along the gradient taken at W_{s-1}.  Returns (W1_s, W2_s, L_s)."""
-    gw1, gw2, ls = segment_grad(x, w1, w2, wkv, loss)
-    return _f64(w1) - lr * gw1, _f64(w2) - lr * gw2, ls
+    gw1, gw2, ls = segment_grad(x, w1, w2, wkv, loss, activation)
+    w1_new = None if w1 is None else _f64(w1) - lr * gw1
+    return w1_new, _f64(w2) - lr * gw2, ls
 
 
-def ttl_run(segments, w1, w2, wkv, lr: float, loss: str = "mse_sum"):
+def ttl_run(segments, w1, w2, wkv, lr: float, loss: str = "mse_sum", activation: str = "silu"):
     """Sequential TTL of one layer: W_0 -> W_1 -> ... -> W_S over the segments in the given order.
     Returns (W1_S, W2_S, [L_1, ..., L_S])."""
-    w1, w2 = _f64(w1), _f64(w2)
+    w1 = None if w1 is None else _f64(w1)
+    w2 = _f64(w2)
     losses = []
     for x in segments:
-        w1, w2, ls = ttl_step(x, w1, w2, wkv, lr, loss)
+        w1, w2, ls = ttl_step(x, w1, w2, wkv, lr, loss, activation)
         losses.append(ls)
     return w1, w2, losses
 

@@ -20,7 +20,8 @@
 // The read reuses the step's scratch: K' holds the pre-normalisation queries and then the memory
 // tokens h, K the queries, dY0 the hidden activations A (row-major, zero padding) and dA0^T's
 // space the transposed W_out copy.
-//                  paper optimiser (fp32): rates [L][Tp], decay block sums, decay [L],
+//                  paper optimiser (fp32): rates [L][Tp], decay block sums
+//                  [L][Tp/kRateTokens], decay [L],
 //                  initial row norms
 // A segment step, each stage one launch grouped over all layers (PROJ) or all B heads:
 //   [RATE]  per-token rates and momentum decay (paper optimiser)

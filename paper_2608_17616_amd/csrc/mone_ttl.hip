@@ -14,7 +14,8 @@
 //                  G   [L][Tp][D], G^T [L][D][Tp]
 //                  dZ^T [L][h][Tp], X^T [L][d][Tp]
 //                  loss partials [L][P], loss [L] fp32
-//                  paper optimiser only (fp32): rates [L][Tp], decay block sums [L][Tp/64],
+//                  paper optimiser only (fp32): rates [L][Tp], decay block sums
+//                  [L][Tp/kRateTokens] (one per 16-token block),
 //                  decay [L], initial row norms [L][h] and [L][D], row-segment sums of
 //                  squares [L][h][d/64] and [L][D][h/64], row scales [L][h] and [L][D]
 // Tp = seg_len rounded up to 256; rows and columns beyond the segment's n tokens are zero, so
