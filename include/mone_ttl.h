@@ -154,6 +154,23 @@ int mone_ttl_init_paper(mone_ttl** out, const mone_ttl_config* cfg, const void* 
  * n_tokens; replaying it then continues the handle's sequence, and eager calls may follow. */
 int mone_ttl_segment(mone_ttl* h, const void* x, int32_t n_tokens, void* stream);
 
+/* For callers that cannot allocate device memory (code under stream capture, tight serving
+ * loops, hosts that forbid hipMalloc): one SGD step of every layer on one segment, exactly the
+ * step of mone_ttl_init followed by mone_ttl_segment, with no handle and no caller workspace.
+ *   cfg, wkv, w1, w2, x, n_tokens, stream: as for mone_ttl_init and mone_ttl_segment; w1 and
+ *            w2 are updated in place.  cfg->optimizer must be MONE_OPT_SGD.
+ * The workspace is a static device array of 64 MiB inside the library, one per device, held
+ * until the process ends; its address is taken once per device, on the first call with that
+ * device current.  Every call clears it and rebuilds the weight copies from w1 and w2, so
+ * consecutive calls continue the TTL chain W_0 -> W_1 -> ... like consecutive
+ * mone_ttl_segment calls.  All calls on one device share the array: calls that overlap on one
+ * device (other streams, other threads) race and must not be issued.
+ * No hipMalloc, hipFree or other allocation, host or device.  Returns MONE_EUNSUPPORTED, before
+ * any HIP call, for a configuration whose workspace (mone_ttl_workspace_bytes) exceeds 64 MiB,
+ * and for MONE_OPT_PAPER. */
+int mone_ttl_step_noalloc(const mone_ttl_config* cfg, const void* wkv, float* w1, float* w2,
+                          const void* x, int32_t n_tokens, void* stream);
+
 /* Read of the current state on query-side inputs, without any update (Eq. read; Sec. 3.4):
  *   KV = W2 SiLU(W1 x_q) for every query row of every layer.
  *   xq       [L][q][d] act_dtype.

@@ -39,6 +39,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -410,43 +411,33 @@ int run_kv(mone_ttl* H, const void* xq, int q, void* kv, int kv_bf16, hipStream_
 
 namespace {
 
-int create_handle(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, float* w1,
-                  float* w2, const mone_paper_optimizer* opt, void* workspace,
-                  size_t workspace_bytes, void* stream) {
-  if (!out) return fail(MONE_EINVAL, "out is NULL");
-  *out = nullptr;
-  int rc = check_config(cfg);
-  if (rc != MONE_OK) return rc;
-  if (!wkv || !w1 || !w2 || !workspace)
-    return fail(MONE_EINVAL, "wkv, w1, w2 and workspace must be non-NULL");
+// Pointer checks shared by the handle and the no-allocation step.
+int check_state(const void* wkv, const float* w1, const float* w2) {
+  if (!wkv || !w1 || !w2) return fail(MONE_EINVAL, "wkv, w1 and w2 must be non-NULL");
   if (!aligned16(wkv) || !aligned16(w1) || !aligned16(w2))
     return fail(MONE_EINVAL, "wkv, w1 and w2 must be 16-byte aligned");
-  if (((uintptr_t)workspace & (kAlign - 1)) != 0)
-    return fail(MONE_EINVAL, "workspace must be 256-byte aligned");
-  const Layout Ly = make_layout(cfg);
-  if (workspace_bytes < Ly.total)
-    return fail(MONE_EINVAL, "workspace has %zu bytes, %zu needed", workspace_bytes, Ly.total);
+  return MONE_OK;
+}
 
-  mone_ttl* H = new (std::nothrow) mone_ttl();
-  if (!H) return fail(MONE_EINVAL, "host allocation failed");
+// Fills a handle over the workspace ws (the layout's total bytes): clears the workspace and
+// builds the weight copies from the fp32 masters (and, with the paper's optimiser, the row-norm
+// targets).  No host or device allocation.
+int init_state(mone_ttl* H, const mone_ttl_config* cfg, const Layout& Ly, const void* wkv,
+               float* w1, float* w2, const mone_paper_optimizer* opt, unsigned char* ws,
+               hipStream_t s) {
   H->cfg = *cfg;
   H->lay = Ly;
   H->wkv = wkv;
   H->w1 = w1;
   H->w2 = w2;
-  H->ws = reinterpret_cast<unsigned char*>(workspace);
+  H->ws = ws;
   H->last_n = 0;
   H->last_loss_count = 0;
   H->w2t_cur = 0;
   if (opt) H->opt = *opt;
-
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int Lc = cfg->n_layers, d = cfg->d_model, h = cfg->d_hidden, D = 2 * cfg->d_kv;
-  hipError_t e = hipMemsetAsync(workspace, 0, Ly.total, s);
-  if (e != hipSuccess) {
-    delete H;
-    return hip_fail(e, "clearing the workspace");
-  }
+  hipError_t e = hipMemsetAsync(ws, 0, Ly.total, s);
+  if (e != hipSuccess) return hip_fail(e, "clearing the workspace");
   const long long n1 = (long long)Lc * h * d, n2 = (long long)Lc * D * h;
   if (cfg->act_dtype == MONE_BF16) {
     convert_kernel<bf16_t><<<dim3(2048), dim3(256), 0, s>>>(w1, H->at<bf16_t>(Ly.w1c), n1, 1.0f);
@@ -462,11 +453,63 @@ int create_handle(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, f
     row_norm_kernel<<<dim3((h + 3) / 4, Lc), dim3(256), 0, s>>>(w1, h, d, H->at<float>(Ly.norm1));
     row_norm_kernel<<<dim3((D + 3) / 4, Lc), dim3(256), 0, s>>>(w2, D, h, H->at<float>(Ly.norm2));
   }
-  if ((e = hipGetLastError()) != hipSuccess) {
+  if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "building the weight copies");
+  return MONE_OK;
+}
+
+int create_handle(mone_ttl** out, const mone_ttl_config* cfg, const void* wkv, float* w1,
+                  float* w2, const mone_paper_optimizer* opt, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+  if (!out) return fail(MONE_EINVAL, "out is NULL");
+  *out = nullptr;
+  int rc = check_config(cfg);
+  if (rc != MONE_OK) return rc;
+  if ((rc = check_state(wkv, w1, w2)) != MONE_OK) return rc;
+  if (!workspace) return fail(MONE_EINVAL, "workspace must be non-NULL");
+  if (((uintptr_t)workspace & (kAlign - 1)) != 0)
+    return fail(MONE_EINVAL, "workspace must be 256-byte aligned");
+  const Layout Ly = make_layout(cfg);
+  if (workspace_bytes < Ly.total)
+    return fail(MONE_EINVAL, "workspace has %zu bytes, %zu needed", workspace_bytes, Ly.total);
+
+  mone_ttl* H = new (std::nothrow) mone_ttl();
+  if (!H) return fail(MONE_EINVAL, "host allocation failed");
+  rc = init_state(H, cfg, Ly, wkv, w1, w2, opt, reinterpret_cast<unsigned char*>(workspace),
+                  reinterpret_cast<hipStream_t>(stream));
+  if (rc != MONE_OK) {
     delete H;
-    return hip_fail(e, "building the weight copies");
+    return rc;
   }
   *out = H;
+  return MONE_OK;
+}
+
+// Workspace of mone_ttl_step_noalloc: a static device array, one copy per device for the life
+// of the process.  In host code `scratch` names a host-side stand-in, never the device memory:
+// its device address comes from hipGetSymbolAddress, once per device, and only that address
+// is passed to kernels and to hipMemsetAsync.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+unsigned char* g_scratch_dev[kMaxDevices] = {};
+
+int scratch_address(unsigned char** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(MONE_EUNSUPPORTED, "device %d", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p || ((uintptr_t)p & (kAlign - 1)) != 0)
+      return fail(MONE_EHIP, "static scratch at %p is not 256-byte aligned", p);
+    g_scratch_dev[dev] = reinterpret_cast<unsigned char*>(p);
+  }
+  *out = g_scratch_dev[dev];
   return MONE_OK;
 }
 
@@ -521,6 +564,34 @@ int mone_ttl_segment(mone_ttl* H, const void* x, int32_t n_tokens, void* stream)
                  : run_segment<bf16_t, false>(H, x, n_tokens, s);
   return paper ? run_segment<float, true>(H, x, n_tokens, s)
                : run_segment<float, false>(H, x, n_tokens, s);
+}
+
+int mone_ttl_step_noalloc(const mone_ttl_config* cfg, const void* wkv, float* w1, float* w2,
+                          const void* x, int32_t n_tokens, void* stream) {
+  g_err[0] = 0;
+  int rc = check_config(cfg);
+  if (rc != MONE_OK) return rc;
+  if (cfg->optimizer != MONE_OPT_SGD)
+    return fail(MONE_EUNSUPPORTED, "mone_ttl_step_noalloc takes plain SGD only (the paper's "
+                "optimiser keeps state across segments: use a handle)");
+  if ((rc = check_state(wkv, w1, w2)) != MONE_OK) return rc;
+  if (n_tokens < 0 || n_tokens > cfg->seg_len)
+    return fail(MONE_EINVAL, "n_tokens %d outside [0, seg_len=%d]", n_tokens, cfg->seg_len);
+  const Layout Ly = make_layout(cfg);
+  if (Ly.total > kScratchBytes)
+    return fail(MONE_EUNSUPPORTED, "this configuration needs %zu bytes of workspace; the static "
+                "scratch of mone_ttl_step_noalloc holds %zu (use mone_ttl_init with a workspace)",
+                Ly.total, kScratchBytes);
+  if (n_tokens == 0) return MONE_OK;
+  if (!x) return fail(MONE_EINVAL, "x is NULL");
+  if (!aligned16(x)) return fail(MONE_EINVAL, "x must be 16-byte aligned");
+  unsigned char* ws = nullptr;
+  if ((rc = scratch_address(&ws)) != MONE_OK) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  mone_ttl H;  // on the stack: the handle's state for this one step
+  if ((rc = init_state(&H, cfg, Ly, wkv, w1, w2, nullptr, ws, s)) != MONE_OK) return rc;
+  return cfg->act_dtype == MONE_BF16 ? run_segment<bf16_t, false>(&H, x, n_tokens, s)
+                                     : run_segment<float, false>(&H, x, n_tokens, s);
 }
 
 int mone_memory_kv(mone_ttl* H, const void* xq, int32_t q, void* kv, int32_t kv_dtype,

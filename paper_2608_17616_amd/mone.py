@@ -30,7 +30,8 @@ MONE_SW_N_STAGES = len(SW_STAGES)
 
 # every symbol include/mone_ttl.h and include/mone_swiglu.h declare
 EXPORTS = ("mone_ttl_workspace_bytes", "mone_ttl_init", "mone_ttl_init_paper",
-           "mone_ttl_segment", "mone_memory_kv", "mone_memory_attention",
+           "mone_ttl_segment", "mone_ttl_step_noalloc", "mone_memory_kv",
+           "mone_memory_attention",
            "mone_ttl_loss", "mone_ttl_destroy", "mone_ttl_last_error",
            "mone_ttl_set_stage_timing", "mone_ttl_stage_times",
            "mone_swiglu_workspace_bytes", "mone_swiglu_init", "mone_swiglu_segment",
@@ -109,6 +110,7 @@ def lib() -> ctypes.CDLL:
                                           ctypes.POINTER(mone_paper_optimizer), vp,
                                           ctypes.c_size_t, vp]
         L.mone_ttl_segment.argtypes = [vp, vp, i32, vp]
+        L.mone_ttl_step_noalloc.argtypes = [cfgp, vp, vp, vp, vp, i32, vp]
         L.mone_memory_kv.argtypes = [vp, vp, i32, vp, i32, vp]
         L.mone_memory_attention.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, i32, vp]
         L.mone_ttl_loss.argtypes = [vp, ctypes.POINTER(ctypes.c_float), vp]
@@ -217,6 +219,12 @@ def paper_optimizer(rate_w, rate_b, decay_w, decay_b, mom1, mom2) -> mone_paper_
 
 def mone_ttl_segment(handle: int, x, n_tokens: int, stream=None) -> None:
     _check(lib().mone_ttl_segment(handle, _ptr(x), int(n_tokens), _stream(stream)))
+
+
+def mone_ttl_step_noalloc(cfg: mone_ttl_config, wkv, w1, w2, x, n_tokens: int,
+                          stream=None) -> None:
+    _check(lib().mone_ttl_step_noalloc(ctypes.byref(cfg), _ptr(wkv), _ptr(w1), _ptr(w2), _ptr(x),
+                                       int(n_tokens), _stream(stream)))
 
 
 def mone_memory_kv(handle: int, xq, q: int, kv, kv_dtype: int, stream=None) -> None:

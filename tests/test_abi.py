@@ -252,3 +252,27 @@ def test_swiglu_null_handle_calls_fail_cleanly():
     assert L.mone_swiglu_read(None, ctypes.byref(rd), 16, 1, 16, 0, None) == mone.MONE_EINVAL
     assert L.mone_swiglu_attention(None, 64, 16, 16, 16, 16, 0, 4, 4, 2, 16, 0,
                                    None) == mone.MONE_EINVAL
+
+
+def test_noalloc_step_rejects_before_any_hip_call():
+    # every check of the no-allocation step precedes its first HIP call, so none touches a GPU
+    dummy = 4096  # a 16-byte-aligned non-NULL address that is never used
+    big = mone.config_from(configs.ONE_B)  # workspace far beyond the 64 MiB static scratch
+    with pytest.raises(mone.MoneError) as e:
+        mone.mone_ttl_step_noalloc(big, dummy, dummy, dummy, dummy, 16, 0)
+    assert e.value.code == mone.MONE_EUNSUPPORTED and "scratch" in str(e.value)
+    paper = _cfg(optimizer="paper")
+    with pytest.raises(mone.MoneError) as e:
+        mone.mone_ttl_step_noalloc(paper, dummy, dummy, dummy, dummy, 16, 0)
+    assert e.value.code == mone.MONE_EUNSUPPORTED
+    small = _cfg()
+    with pytest.raises(mone.MoneError) as e:
+        mone.mone_ttl_step_noalloc(small, None, dummy, dummy, dummy, 16, 0)
+    assert e.value.code == mone.MONE_EINVAL
+    for n in (-1, 101):
+        with pytest.raises(mone.MoneError) as e:
+            mone.mone_ttl_step_noalloc(small, dummy, dummy, dummy, dummy, n, 0)
+        assert e.value.code == mone.MONE_EINVAL
+    with pytest.raises(mone.MoneError) as e:
+        mone.mone_ttl_step_noalloc(small, dummy, dummy, dummy, None, 16, 0)
+    assert e.value.code == mone.MONE_EINVAL
