@@ -2,8 +2,9 @@
 """Throughput of the MoNe test-time-learning hot path on one MI355X.
 
 One step = the whole hot path over one synthetic context: every segment of the context goes
-through mone_ttl_segment (all layers, grouped launches), then mone_memory_kv reads the final
-state on a query batch.  The default workload is the 8B-class shape: 32 layers, d = h = 4096,
+through one mone_ttl_segments call (all layers, grouped launches; short segments in the block
+form, the others one by one; --call segment issues one call per segment), then mone_memory_kv
+reads the final state on a query batch.  The default workload is the 8B-class shape: 32 layers, d = h = 4096,
 D = 2048 (8 KV heads x 128 for K and for V), T = 2048, N = 131072 context tokens
 (64 segments), Q = 64 query tokens, bf16 activations, fp32 fast weights, lr 1e-3.
 
@@ -36,8 +37,23 @@ PEAK_F32_TFLOPS = 157.3     # MI355X dense fp32 matrix
 PEAK_HBM_GBS = 8000.0
 
 
-def stage_work(cfg, q):
-    """Algorithmic FLOPs and bytes of one launch of each stage (all layers)."""
+def block_segments(cfg):
+    """Segments per block of mone_ttl_segments' block form for this configuration (1: the
+    segments run one by one), by the rule the library's header states."""
+    T = cfg.seg_len
+    if cfg.block_tokens < 0 or not (cfg.optimizer == "sgd" and cfg.loss in ("mse_sum", "mse_mean")
+                                    and T % 64 == 0):
+        return 1
+    if cfg.block_tokens > 0:
+        return cfg.block_tokens // T
+    weights = cfg.n_layers * cfg.d_hidden * (cfg.d_model + cfg.d_out)
+    return 512 // T if T <= 256 and weights >= 1 << 24 else 1
+
+
+def stage_work(cfg, q, blk=1):
+    """Algorithmic FLOPs and bytes of one launch of each stage (all layers).  With the block
+    form (blk segments per block) the staging and the block stages cover a block of blk*T
+    tokens, and BSEQ one segment (its corrections averaged over the block)."""
     L, d, h, D, T = cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out, cfg.seg_len
     E = 2 if cfg.act_dtype == "bf16" else 4
     hkv = max(1, cfg.d_kv // 128)
@@ -45,6 +61,22 @@ def stage_work(cfg, q):
     # causal scores and weighted sums over q query keys and q memory keys per query row
     attn = (L * hq * 2 * (q * (q + 1)) * 2 * dh,
             L * q * ((hq + 2 * hkv) * dh * E + D * 4 + hq * dh * 4))
+    if blk > 1:
+        bt = blk * T
+        kp = T * (blk - 1) / 2  # earlier segments' tokens, averaged over the block
+        return {
+            "xt": (0, L * bt * d * E * 2),
+            "bfwd": (L * (2 * bt * d * (h + D) + 2 * bt * bt * d),
+                     L * (E * (bt * d + h * d + D * d + bt * bt) + 4 * bt * (h + D))),
+            "bseq": (L * (4 * T * h * D + 2 * T * kp * (3 * h + 2 * D)),
+                     L * (2 * D * h * E + T * (8 * h + 8 * D + E * (5 * h + 3 * D)))),
+            "bupd": (L * 2 * bt * (D * h + h * d),
+                     L * (8 * (D * h + h * d) + E * (2 * D * h + h * d)
+                          + E * bt * (D + 2 * h + d))),
+            "kv1": (L * 2 * q * d * h, L * (q * d + h * d + q * h) * E),
+            "kv2": (L * 2 * q * h * D, L * (q * h + D * h) * E + L * q * D * 4),
+            "attn": attn,
+        }
     if cfg.optimizer == "paper":
         # momentum read-modify-write in the update epilogues; the copies move to RENORM
         cp1 = E if cfg.act_dtype == "bf16" else 0
@@ -445,6 +477,13 @@ def main():
                     help="configurations' memory: capture one whole step (its segment calls, "
                          "the read and the attention) in a HIP graph and time its replays; the "
                          "segment count must be even (the W2^T copies alternate per segment)")
+    ap.add_argument("--call", default="segments", choices=("segments", "segment"),
+                    help="configurations' memory: the whole context through one "
+                         "mone_ttl_segments call (default; the block form for short segments), "
+                         "or one call per segment")
+    ap.add_argument("--block-tokens", type=int, default=0,
+                    help="configurations' memory: tokens per block of the block form (0: the "
+                         "library's choice, -1: none)")
     ap.add_argument("--memory", default="config", choices=("config", "swiglu"),
                     help="config: the configurations' 2-layer memory (default); swiglu: the "
                          "paper-form SwiGLU memory per fast-weight head at the paper's shape")
@@ -465,7 +504,8 @@ def main():
 
     from paper_2608_17616_amd import configs, inputs, mone
 
-    cfg = configs.CONFIGS[args.config].with_(optimizer=args.optimizer)
+    cfg = configs.CONFIGS[args.config].with_(optimizer=args.optimizer,
+                                             block_tokens=args.block_tokens)
     if args.loss:
         cfg = cfg.with_(loss=args.loss)
     L, d, h, D, T, Q = (cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out, cfg.seg_len,
@@ -482,9 +522,11 @@ def main():
     w2 = inputs.device_normal_(torch.empty(L, D, h, dtype=torch.float32, device=dev),
                                1 / np.sqrt(h), gen)
     wkv = inputs.device_normal_(torch.empty(L, D, d, dtype=act, device=dev), 1 / np.sqrt(d), gen)
-    ctx = torch.empty(S, L, T, d, dtype=act, device=dev)
+    # each layer's part of the context in one piece: token t of segment s of layer l at
+    # ctx[l, s*T + t]
+    ctx = torch.empty(L, S * T, d, dtype=act, device=dev)
     for s in range(S):
-        inputs.device_normal_(ctx[s], 1.0, gen)
+        inputs.device_normal_(ctx[:, s * T:(s + 1) * T], 1.0, gen)
     xq = inputs.device_normal_(torch.empty(L, Q, d, dtype=act, device=dev), 1.0, gen)
     kv = torch.empty(L, Q, D, dtype=torch.float32, device=dev)
     # memory injection into attention after the read: grouped-query heads of width 128 (64 when
@@ -502,7 +544,7 @@ def main():
     if n_cpu:
         cpu_in = (w1[0].double().cpu().numpy(), w2[0].double().cpu().numpy(),
                   wkv[0].double().cpu().numpy(),
-                  [ctx[s, 0].double().cpu().numpy() for s in range(n_cpu)])
+                  [ctx[0, s * T:(s + 1) * T].double().cpu().numpy() for s in range(n_cpu)])
 
     opt = None
     if cfg.optimizer == "paper":
@@ -519,9 +561,15 @@ def main():
     H = sess.handle
     sptr = stream.cuda_stream
 
+    lstride = ctx.stride(0)
+    blk = block_segments(cfg) if args.call == "segments" else 1
+
     def step(sp=sptr):
-        for s in range(S):
-            mone.mone_ttl_segment(H, ctx[s], T, sp)
+        if args.call == "segments":
+            mone.mone_ttl_segments(H, ctx, lstride, S, sp)
+        else:
+            for s in range(S):
+                mone.mone_ttl_segments(H, ctx[:, s * T:], lstride, 1, sp)
         mone.mone_memory_kv(H, xq, Q, kv, mone.MONE_F32, sp)
         mone.mone_memory_attention(H, aq, ak, av, kv, mone.MONE_F32, Q, hq, hkv, aout,
                                    mone.MONE_F32, sp)
@@ -531,9 +579,10 @@ def main():
     torch.cuda.synchronize()
     graph = None
     if args.graph:
-        if S % 2:
-            print("bench.py: --graph needs an even number of segments", file=sys.stderr,
-                  flush=True)
+        # the W2^T copies alternate per block (per segment outside the block form)
+        if (S // blk + (1 if S % blk else 0)) % 2:
+            print("bench.py: --graph needs an even number of blocks (segments outside the "
+                  "block form)", file=sys.stderr, flush=True)
             sys.exit(2)
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):  # timing hooks are off here
@@ -575,7 +624,7 @@ def main():
     flop_tok = cfg.flops_per_token()
     peak = PEAK_BF16_TFLOPS if cfg.act_dtype == "bf16" else PEAK_F32_TFLOPS
     mfma_pct = 100.0 * value * flop_tok / (peak * 1e12)
-    work = stage_work(cfg, Q)
+    work = stage_work(cfg, Q, blk)
     stages = stage_table(stimes, work)
     dfl, dby = work[dom]
     davg = dms / dcnt / 1e3
@@ -596,7 +645,9 @@ def main():
                                f"N={S * T} ({S} segments) + read Q={Q}"
                                + (", paper optimiser" if cfg.optimizer == "paper" else "")
                                + (f", loss {cfg.loss}" if args.loss else "")
-                               + (", HIP graph replay" if graph is not None else ""),
+                               + (", HIP graph replay" if graph is not None else "")
+                               + (f", block form ({blk} segments per block)" if blk > 1
+                                  else ""),
                    "n_layers": L, "d_model": d, "d_hidden": h, "d_out": D, "seg_len": T,
                    "n_context": S * T, "n_query": Q, "lr": cfg.lr, "optimizer": cfg.optimizer,
                    "loss": cfg.loss},

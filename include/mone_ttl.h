@@ -82,6 +82,12 @@ typedef struct {
   float lr;          /* learning rate (finite, may be 0); with MONE_OPT_PAPER it scales the
                         per-token rates */
   int32_t optimizer; /* mone_optimizer */
+  int32_t block_tokens; /* block form of mone_ttl_segments: tokens per block.  0 chooses: 512
+                           when the block form applies (plain SGD, a squared-error loss, seg_len
+                           a multiple of 64 of at most 256) and the fast weights of all layers
+                           hold at least 2^24 elements, else none.  Negative: none.  Positive:
+                           a multiple of seg_len, from 2 * seg_len to 4096, where the block form
+                           applies (else MONE_EUNSUPPORTED). */
 } mone_ttl_config;
 
 typedef struct mone_ttl mone_ttl; /* opaque host object */
@@ -171,6 +177,27 @@ int mone_ttl_segment(mone_ttl* h, const void* x, int32_t n_tokens, void* stream)
 int mone_ttl_step_noalloc(const mone_ttl_config* cfg, const void* wkv, float* w1, float* w2,
                           const void* x, int32_t n_tokens, void* stream);
 
+/* Several consecutive segments of seg_len tokens in one call (Sec. 3.1: the context read
+ * segment after segment; Sec. 3.4: each layer's chain W_0 -> W_1 -> ... in context order):
+ * the same as n_segments calls of mone_ttl_segment with n_tokens = seg_len, up to rounding.
+ *   x             the segments' hidden states: token t of segment s of layer l at
+ *                 x + l * layer_stride + (s * seg_len + t) * d_model (elements of act_dtype),
+ *                 i.e. each layer's part of the context in one piece.
+ *   layer_stride  elements between layers, >= n_segments * seg_len * d_model; x and
+ *                 layer_stride * element size 16-byte aligned.
+ *   n_segments    >= 0 (0 is a no-op).
+ * With a block form (cfg->block_tokens; by default for short segments of large memories,
+ * whose steps are bound by rewriting every fast weight for few tokens), the segments run in
+ * blocks of block_tokens / seg_len: a block computes each segment's step at the weights it
+ * started from plus the earlier segments' updates, which enter through T x T products of the
+ * segments' tokens, hidden activations and loss gradients (exact algebra of the sequential
+ * chain, summed in another order), and writes the fast weights once per block (a last
+ * block may hold fewer segments; a single one runs alone).  Otherwise the segments run one by
+ * one.  The workspace of such configurations includes the block's buffers
+ * (mone_ttl_workspace_bytes).  mone_ttl_loss then reports the last segment's loss. */
+int mone_ttl_segments(mone_ttl* h, const void* x, int64_t layer_stride, int32_t n_segments,
+                      void* stream);
+
 /* Read of the current state on query-side inputs, without any update (Eq. read; Sec. 3.4):
  *   KV = W2 SiLU(W1 x_q) for every query row of every layer.
  *   xq       [L][q][d] act_dtype.
@@ -232,7 +259,11 @@ const char* mone_ttl_last_error(void);
 #define MONE_STAGE_RATE 7  /* MONE_OPT_PAPER: per-token rates and the momentum decay */
 #define MONE_STAGE_RENORM 8 /* MONE_OPT_PAPER: row renormalisation of W1, W2 and their copies */
 #define MONE_STAGE_ATTN 9  /* mone_memory_attention */
-#define MONE_N_STAGES 10
+#define MONE_STAGE_BFWD 10 /* block form: X W1^T, the targets and the token Gram X X^T */
+#define MONE_STAGE_BSEQ 11 /* block form: one segment's corrected forward, loss gradient and
+                              backward (five launches) */
+#define MONE_STAGE_BUPD 12 /* block form: the block's W2 and W1 updates */
+#define MONE_N_STAGES 13
 
 /* Enable (max_records > 0) or disable (0) per-stage timing: each subsequent launch of a stage
  * whose bit is set in stage_mask (bit i = stage i; MONE_ALL_STAGES for every stage) is

@@ -30,6 +30,7 @@ class MoneConfig:
     n_query: int = 64  # Q: query tokens for the read step
     seed: int = 0
     optimizer: str = "sgd"  # "sgd" or "paper" (per-token rates, momentum, renormalisation)
+    block_tokens: int = 0   # block form of multi-segment calls: 0 automatic, < 0 none, > 0 size
 
     @property
     def d_out(self) -> int:

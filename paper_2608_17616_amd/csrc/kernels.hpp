@@ -1043,6 +1043,181 @@ struct EpiKv2 : EpiBase {
 };
 
 // ------------------------------------------------------------------------------------------
+// Epilogues of the block form of consecutive segments (mone_ttl_segments).  A block of B
+// segments j = 0..B-1 of T tokens each (block rows jT .. jT + T - 1) starts from the weights
+// W_0 it finds.  Each segment's step uses W_{j-1} = W_0 minus the updates of the block's
+// earlier segments, and those enter as products with T x T token blocks (exact algebra, the
+// summation order aside):
+//   Z_j  = X_j W1_{j-1}^T = X_j W1_0^T - lr sum_{i<j} (X_j X_i^T) dZ_i
+//   Y_j  = A_j W2_{j-1}^T = A_j W2_0^T - lr sum_{i<j} (A_j A_i^T) G_i
+//   dA_j = G_j W2_{j-1}   = G_j W2_0   - lr sum_{i<j} (G_j G_i^T) A_i
+// The weights are read and written once per block: W -= lr sum_j (gradient of segment j).
+
+// Plain stores of the accumulators times a per-problem scale: problem 0 as T0 [rows][ld0],
+// problem 1 as T1 [rows][ld1] (the token-block products and the pre-update GEMMs).
+template <typename T0, typename T1>
+struct EpiStore : EpiBase {
+  T0* p0; long long ls0; int ld0; float s0;
+  T1* p1; long long ls1; int ld1; float s1;
+  __device__ __forceinline__ float rows8(int pi, int layer, int row, int col, int, int,
+                                         float (&v)[8], const float (&)[8]) const {
+    float o[8];
+    const float sc = pi == 0 ? s0 : s1;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = sc * v[e];
+    if (pi == 0) store8(p0 + (long long)layer * ls0 + (long long)row * ld0 + col, o);
+    else store8(p1 + (long long)layer * ls1 + (long long)row * ld1 + col, o);
+    return 0.0f;
+  }
+};
+
+// Block form, pre-activations of segment j: Z = Z0 - lr acc with acc = (X_j X_<j^T) dZ_<j and
+// Z0 = X_j W1_0^T; stores A = SiLU(Z) (block rows r0 + row, and A^T by columns) and SiLU'(Z).
+template <typename E>
+struct EpiBlkZ : EpiBase {
+  static constexpr bool kPre = true;
+  static constexpr bool kCols = true;
+  static constexpr bool kWriteback = true;
+  const float* z0;     // [L][Btp][h]
+  E* a; E* at; E* sd;  // A [Btp][h], A^T [h][Btp], SiLU'(Z) [Btp][h]
+  long long ls;        // Btp*h
+  int h, Btp, r0;
+  float lr;
+  __device__ __forceinline__ bool has_cols(int) const { return true; }
+  __device__ __forceinline__ void pre8(int, int layer, int row, int col, int, int,
+                                       float (&x)[8]) const {
+    load8(z0 + (long long)layer * ls + (long long)(r0 + row) * h + col, x);
+  }
+  __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
+                                         float (&v)[8], const float (&x)[8]) const {
+    float av[8], dv[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float z = x[e] - lr * v[e];
+      const float sg = sigmoidf_(z);
+      av[e] = z * sg;
+      dv[e] = sg * (1.0f + z * (1.0f - sg));
+    }
+    const long long o = (long long)layer * ls + (long long)(r0 + row) * h + col;
+    store8(a + o, av);
+    store8(sd + o, dv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = av[e];
+    return 0.0f;
+  }
+  __device__ __forceinline__ void cols8(int, int layer, int row, int col, int, int,
+                                        const float (&v)[8]) const {
+    store8(at + (long long)layer * ls + (long long)col * Btp + r0 + row, v);
+  }
+};
+
+// Block form, output layer of segment j at W2_0: problem 0 is A_j (-W2_0)^T = -Y0, stored as
+// the pre-update residual R0 = Y0 - targets (fp32); problem 1 is the token block
+// P = A_j A_<j^T.
+template <typename E>
+struct EpiBlkY0 : EpiBase {
+  static constexpr bool kPre = true;
+  const float* tgt; long long lst;  // targets [L][Btp][D] (block rows)
+  float* rr; long long lsr;         // R0 [L][Tp][D]
+  E* pg; long long lsp;             // P [L][Tp][Btp]
+  int D, Btp, r0;
+  __device__ __forceinline__ void pre8(int pi, int layer, int row, int col, int, int,
+                                       float (&x)[8]) const {
+    if (pi == 0) {
+      load8(tgt + (long long)layer * lst + (long long)(r0 + row) * D + col, x);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+    }
+  }
+  __device__ __forceinline__ float rows8(int pi, int layer, int row, int col, int, int,
+                                         float (&v)[8], const float (&x)[8]) const {
+    if (pi == 0) {
+      float o[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = -v[e] - x[e];
+      store8(rr + (long long)layer * lsr + (long long)row * D + col, o);
+    } else {
+      store8(pg + (long long)layer * lsp + (long long)row * Btp + col, v);
+    }
+    return 0.0f;
+  }
+};
+
+// Block form, loss gradient of segment j: R = R0 - lr acc with acc = P G_<j; stores G = c R
+// (block rows, and G^T by columns) and sums R^2 per wave into the loss partials.
+template <typename E>
+struct EpiBlkG : EpiBase {
+  static constexpr bool kPre = true;
+  static constexpr bool kCols = true;
+  static constexpr bool kWriteback = true;
+  const float* rr; long long lsr;  // R0 [L][Tp][D]
+  E* g; E* gt; long long lsg;      // G [L][Btp][D], G^T [L][D][Btp]
+  float* loss_part;
+  int D, Btp, r0, parts_per_layer;
+  float lr, c;
+  __device__ __forceinline__ bool has_cols(int) const { return true; }
+  __device__ __forceinline__ void pre8(int, int layer, int row, int col, int, int,
+                                       float (&x)[8]) const {
+    load8(rr + (long long)layer * lsr + (long long)row * D + col, x);
+  }
+  __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
+                                         float (&v)[8], const float (&x)[8]) const {
+    float gv[8], sq = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float r = x[e] - lr * v[e];
+      sq += r * r;
+      gv[e] = c * r;
+    }
+    store8(g + (long long)layer * lsg + (long long)(r0 + row) * D + col, gv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = gv[e];
+    return sq;
+  }
+  __device__ __forceinline__ void cols8(int, int layer, int row, int col, int, int,
+                                        const float (&v)[8]) const {
+    store8(gt + (long long)layer * lsg + (long long)col * Btp + r0 + row, v);
+  }
+  __device__ __forceinline__ void finish(int, int layer, int tile, int wave, int lane,
+                                        float sq) const {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off, 64);
+    if (lane == 0) loss_part[(long long)layer * parts_per_layer + tile * 4 + wave] = sq;
+  }
+};
+
+// Block form, backward of segment j: dA = dA0 - lr acc with acc = Q A_<j (Q = G_j G_<j^T) and
+// dA0 = G_j W2_0; stores dZ = dA * SiLU'(Z) by columns into dZ^T (block token columns).
+template <typename E>
+struct EpiBlkDZ : EpiBase {
+  static constexpr bool kPre = true;
+  static constexpr bool kCols = true;
+  static constexpr bool kWriteback = true;
+  const float* da0; long long lsa;  // dA0 [L][Tp][h]
+  const E* sd; E* dzt; long long ls;  // SiLU'(Z) [L][Btp][h], dZ^T [L][h][Btp]
+  int h, Btp, r0;
+  float lr;
+  __device__ __forceinline__ bool has_cols(int) const { return true; }
+  __device__ __forceinline__ void pre8(int, int layer, int row, int col, int, int,
+                                       float (&x)[8]) const {
+    load8(da0 + (long long)layer * lsa + (long long)row * h + col, x);
+  }
+  __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
+                                         float (&v)[8], const float (&x)[8]) const {
+    float sv[8];
+    load8(sd + (long long)layer * ls + (long long)(r0 + row) * h + col, sv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (x[e] - lr * v[e]) * sv[e];
+    return 0.0f;
+  }
+  __device__ __forceinline__ void cols8(int, int layer, int row, int col, int, int,
+                                        const float (&v)[8]) const {
+    store8(dzt + (long long)layer * ls + (long long)col * Btp + r0 + row, v);
+  }
+};
+
+// ------------------------------------------------------------------------------------------
 // Data-movement helpers
 
 // dst[l][c][r] = src[l][r][c] for r < R, 0 for R <= r < Rz; 64x64 tiles through LDS.

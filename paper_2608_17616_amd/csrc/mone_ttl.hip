@@ -57,8 +57,35 @@ struct Layout {
   int loss_per_layer;
   size_t w1c, w2c, w2t, a, at, dst, g, gt, dzt, xt, loss_part, loss_out, split;
   size_t rate, vpart, beta, norm1, norm2, ss1, ss2, scale1, scale2;  // paper optimiser
+  // block form of consecutive segments (mone_ttl_segments): blk segments per block (0: none),
+  // block rows padded to Btp; fp32 pre-update products and activation-dtype block operands
+  int blk, Btp;
+  size_t bz0, btgt, bgram, ba, bat, bsd, bg, bgt, bdzt, bxt, brr, bp, bda0, bq;
   size_t total;
 };
+
+// Block form of consecutive segments.  Short segments rewrite every fast weight for few
+// tokens; a block of segments reads and writes them once, at the cost of the T x T token
+// products of its segments' corrections (which grow with T and with the block).  It covers
+// plain SGD on the squared-error losses with segments of a multiple of 64 tokens (whole K
+// steps of the token products).  By default: 512-token blocks for segments of at most 256
+// tokens, when the fast weights of all layers hold at least 2^24 elements (below that, the
+// weight traffic a block saves is small next to the latency of its extra launches).
+constexpr int kBlockTokens = 512, kMaxBlockTokens = 4096;
+constexpr long long kBlockMinWeights = 1LL << 24;
+
+bool block_form_applies(const mone_ttl_config* c) {
+  return c->optimizer == MONE_OPT_SGD &&
+         (c->loss == MONE_LOSS_MSE_SUM || c->loss == MONE_LOSS_MSE_MEAN) && c->seg_len % 64 == 0;
+}
+
+// Tokens per block (0: no block form); the config has passed check_config.
+int block_tokens(const mone_ttl_config* c) {
+  if (c->block_tokens < 0 || !block_form_applies(c)) return 0;
+  if (c->block_tokens > 0) return c->block_tokens;
+  const long long w = (long long)c->n_layers * c->d_hidden * (c->d_model + 2LL * c->d_kv);
+  return c->seg_len <= kBlockTokens / 2 && w >= kBlockMinWeights ? kBlockTokens : 0;
+}
 
 int check_config(const mone_ttl_config* c) {
   if (!c) return fail(MONE_EINVAL, "config is NULL");
@@ -75,6 +102,15 @@ int check_config(const mone_ttl_config* c) {
   if (c->d_model % 64 || c->d_hidden % 64 || c->d_kv % 64)
     return fail(MONE_EUNSUPPORTED, "d_model, d_hidden and d_kv must be multiples of 64");
   if (c->seg_len > 65536) return fail(MONE_EUNSUPPORTED, "seg_len above 65536");
+  if (c->block_tokens > 0) {
+    if (!block_form_applies(c))
+      return fail(MONE_EUNSUPPORTED, "block_tokens needs plain SGD, a squared-error loss and "
+                  "seg_len a multiple of 64");
+    if (c->block_tokens % c->seg_len || c->block_tokens < 2 * c->seg_len ||
+        c->block_tokens > kMaxBlockTokens)
+      return fail(MONE_EINVAL, "block_tokens %d must be a multiple of seg_len %d from 2 * "
+                  "seg_len to %d", c->block_tokens, c->seg_len, kMaxBlockTokens);
+  }
   const long long Tp = round_up(c->seg_len, 256);
   const long long d = c->d_model, h = c->d_hidden, D = 2LL * c->d_kv;
   const long long mx = d > h ? (d > D ? d : D) : (h > D ? h : D);
@@ -127,6 +163,25 @@ Layout make_layout(const mone_ttl_config* c) {
   L.loss_part = take(nl * (size_t)L.loss_per_layer * 4);
   L.loss_out = take(nl * 4);
   L.split = take(kSplitFloats * 4);  // split-K partial accumulators (short segments, reads)
+  if (const int bt = block_tokens(c)) {
+    L.blk = bt / c->seg_len;
+    L.Btp = (int)round_up((long long)L.blk * c->seg_len, 256);
+    const size_t Bp = L.Btp;
+    L.bz0 = take(nl * Bp * h * 4);
+    L.btgt = take(nl * Bp * D * 4);
+    L.bgram = take(nl * Bp * Bp * E);
+    L.ba = take(nl * Bp * h * E);
+    L.bat = take(nl * h * Bp * E);
+    L.bsd = take(nl * Bp * h * E);
+    L.bg = take(nl * Bp * D * E);
+    L.bgt = take(nl * D * Bp * E);
+    L.bdzt = take(nl * h * Bp * E);
+    L.bxt = take(nl * d * Bp * E);
+    L.brr = take(nl * Tp * D * 4);
+    L.bp = take(nl * Tp * Bp * E);
+    L.bda0 = take(nl * Tp * h * 4);
+    L.bq = take(nl * Tp * Bp * E);
+  }
   if (c->optimizer == MONE_OPT_PAPER) {
     L.rate = take(nl * Tp * 4);
     L.vpart = take(nl * (Tp / kRateTokens) * 4);
@@ -166,8 +221,9 @@ struct mone_ttl {
 
 namespace {
 
+// One segment step of all layers; x [L][n][d] with layer stride lsx elements.
 template <typename E, bool PAPER>
-int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
+int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s) {
   const mone_ttl_config& c = H->cfg;
   const Layout& Ly = H->lay;
   const int Lc = c.n_layers, d = c.d_model, h = c.d_hidden, D = 2 * c.d_kv, Tp = Ly.Tp;
@@ -185,7 +241,6 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
   E* Gt = H->at<E>(Ly.gt);
   E* dZt = H->at<E>(Ly.dzt);
   E* Xt = H->at<E>(Ly.xt);
-  const long long lsx = (long long)n * d;
   const long long lth = (long long)Tp * h, ltd = (long long)Tp * D, ltx = (long long)Tp * d;
   const int nz = (int)round_up(n, 64);  // zero-filled token extent of the transposed copies
   hipError_t e;
@@ -348,6 +403,214 @@ int run_segment(mone_ttl* H, const void* x, int n, hipStream_t s) {
   }
   H->w2t_cur ^= 1;
   H->last_n = n;
+  return MONE_OK;
+}
+
+// Block form: nb consecutive segments of T tokens (nb <= blk) from x [L][nb*T][d], layer stride
+// lsx, as one block.  Results equal nb run_segment calls up to the summation order.
+template <typename E>
+int run_block(mone_ttl* H, const E* x, long long lsx, int nb, hipStream_t s) {
+  const mone_ttl_config& c = H->cfg;
+  const Layout& Ly = H->lay;
+  const int Lc = c.n_layers, d = c.d_model, h = c.d_hidden, D = 2 * c.d_kv, Tp = Ly.Tp;
+  const int T = c.seg_len, Bt = nb * T, Bp = Ly.Btp;
+  const bool bf = sizeof(E) == 2;
+  const E* w1op = bf ? H->at<E>(Ly.w1c) : reinterpret_cast<const E*>(H->w1);
+  const E* w2neg = H->at<E>(Ly.w2c);
+  const size_t w2t_bytes = (size_t)Lc * h * D * sizeof(E);
+  E* w2t_old = H->at<E>(Ly.w2t + (size_t)H->w2t_cur * w2t_bytes);
+  E* w2t_new = H->at<E>(Ly.w2t + (size_t)(H->w2t_cur ^ 1) * w2t_bytes);
+  float* z0 = H->at<float>(Ly.bz0);
+  float* tgt = H->at<float>(Ly.btgt);
+  E* gram = H->at<E>(Ly.bgram);
+  E* ab = H->at<E>(Ly.ba);
+  E* abt = H->at<E>(Ly.bat);
+  E* sdb = H->at<E>(Ly.bsd);
+  E* gb = H->at<E>(Ly.bg);
+  E* gbt = H->at<E>(Ly.bgt);
+  E* dzt = H->at<E>(Ly.bdzt);
+  E* xt = H->at<E>(Ly.bxt);
+  float* rr = H->at<float>(Ly.brr);
+  E* pg = H->at<E>(Ly.bp);
+  float* da0 = H->at<float>(Ly.bda0);
+  E* qg = H->at<E>(Ly.bq);
+  const long long lbh = (long long)Bp * h, lbd = (long long)Bp * D, lbb = (long long)Bp * Bp;
+  const long long lbx = (long long)Bp * d, lth = (long long)Tp * h, ltd = (long long)Tp * D;
+  const long long ltb = (long long)Tp * Bp;
+  const float cmse = c.loss == MONE_LOSS_MSE_SUM ? 2.0f / (float)T
+                                                 : 2.0f / ((float)T * (float)D);
+  hipError_t e;
+
+  // X^T of the block: the B operand of the block's W1 gradient
+  H->timing_begin(MONE_STAGE_XT, s);
+  transpose_vec_kernel<E><<<dim3((d + 63) / 64, (unsigned)(Bt / 64), Lc), dim3(256), 0, s>>>(
+      x, lsx, d, Bt, d, xt, lbx, Bp, Bt);
+  if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch block XT");
+  H->timing_end(MONE_STAGE_XT, s);
+
+  // Block products at the block's starting weights: Z0 = X W1_0^T and the targets X W_kv^T
+  // (two problems), and the token Gram matrix X X^T
+  H->timing_begin(MONE_STAGE_BFWD, s);
+  {
+    Spec sp[2] = {};
+    sp[0].part[0].a = opnd(x, lsx, d, Bt);
+    sp[0].part[0].b = opnd(w1op, (long long)h * d, d, h);
+    sp[0].part[0].k_len = d;
+    sp[0].nparts = 1;
+    sp[0].m_extent = Bt; sp[0].n = h; sp[0].m_store = -1; sp[0].n_store = h;
+    sp[1] = sp[0];
+    sp[1].part[0].b = opnd(H->wkv, (long long)D * d, d, D);
+    sp[1].n = D; sp[1].n_store = D;
+    EpiStore<float, float> epi;
+    epi.p0 = z0; epi.ls0 = lbh; epi.ld0 = h; epi.s0 = 1.0f;
+    epi.p1 = tgt; epi.ls1 = lbd; epi.ld1 = D; epi.s1 = 1.0f;
+    if ((e = launch_gemm<E>(pick_tile(Bt, h, Lc), sp, 2, Lc, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch block forward");
+  }
+  {
+    Spec sp{};
+    sp.part[0].a = opnd(x, lsx, d, Bt);
+    sp.part[0].b = opnd(x, lsx, d, Bt);
+    sp.part[0].k_len = d;
+    sp.nparts = 1;
+    sp.m_extent = Bt; sp.n = Bt; sp.m_store = -1; sp.n_store = Bt;
+    EpiStore<E, E> epi{};
+    epi.p0 = gram; epi.ls0 = lbb; epi.ld0 = Bp; epi.s0 = 1.0f;
+    if ((e = launch_gemm<E>(pick_tile(Bt, Bt, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch token Gram");
+  }
+  H->timing_end(MONE_STAGE_BFWD, s);
+
+  for (int j = 0; j < nb; ++j) {
+    const int r0 = j * T, kp = j * T;  // block rows of segment j; tokens of the earlier ones
+    H->timing_begin(MONE_STAGE_BSEQ, s);
+    // Z_j = Z0_j - lr (X_j X_<j^T) dZ_<j  ->  A, A^T, SiLU'
+    {
+      Spec sp{};
+      sp.part[0].a = opnd(gram + (long long)r0 * Bp, lbb, Bp, T);
+      sp.part[0].b = opnd(dzt, lbh, Bp, h);
+      sp.part[0].k_len = kp;
+      sp.nparts = 1;
+      sp.m_extent = T; sp.n = h; sp.m_store = T; sp.n_store = h;
+      EpiBlkZ<E> epi;
+      epi.z0 = z0; epi.a = ab; epi.at = abt; epi.sd = sdb; epi.ls = lbh;
+      epi.h = h; epi.Btp = Bp; epi.r0 = r0; epi.lr = c.lr;
+      if ((e = launch_gemm<E>(pick_tile(T, h, Lc), &sp, 1, Lc, epi, s, nullptr,
+                              H->at<float>(Ly.split))) != hipSuccess)
+        return hip_fail(e, "launch block Z");
+    }
+    // R0 = A_j W2_0^T - targets_j, and P = A_j A_<j^T
+    {
+      Spec sp[2] = {};
+      sp[0].part[0].a = opnd(ab + (long long)r0 * h, lbh, h, T);
+      sp[0].part[0].b = opnd(w2neg, (long long)D * h, h, D);
+      sp[0].part[0].k_len = h;
+      sp[0].nparts = 1;
+      sp[0].m_extent = T; sp[0].n = D; sp[0].m_store = T; sp[0].n_store = D;
+      sp[1] = sp[0];
+      sp[1].part[0].b = opnd(ab, lbh, h, kp);
+      sp[1].n = kp; sp[1].n_store = kp;
+      EpiBlkY0<E> epi;
+      epi.tgt = tgt; epi.lst = lbd; epi.rr = rr; epi.lsr = ltd; epi.pg = pg; epi.lsp = ltb;
+      epi.D = D; epi.Btp = Bp; epi.r0 = r0;
+      if ((e = launch_gemm<E>(pick_tile(T, D, Lc), sp, j > 0 ? 2 : 1, Lc, epi, s)) !=
+          hipSuccess)
+        return hip_fail(e, "launch block Y");
+    }
+    // R = R0 - lr P G_<j  ->  G = c R, G^T, loss partials
+    {
+      Spec sp{};
+      sp.part[0].a = opnd(pg, ltb, Bp, T);
+      sp.part[0].b = opnd(gbt, lbd, Bp, D);
+      sp.part[0].k_len = kp;
+      sp.nparts = 1;
+      sp.m_extent = T; sp.n = D; sp.m_store = T; sp.n_store = D;
+      EpiBlkG<E> epi;
+      epi.rr = rr; epi.lsr = ltd; epi.g = gb; epi.gt = gbt; epi.lsg = lbd;
+      epi.loss_part = H->at<float>(Ly.loss_part); epi.D = D; epi.Btp = Bp; epi.r0 = r0;
+      epi.parts_per_layer = Ly.loss_per_layer; epi.lr = c.lr; epi.c = cmse;
+      int tiles = 0;
+      if ((e = launch_gemm<E>(pick_tile(T, D, Lc), &sp, 1, Lc, epi, s, &tiles,
+                              H->at<float>(Ly.split))) != hipSuccess)
+        return hip_fail(e, "launch block G");
+      H->last_loss_count = 4 * tiles;
+    }
+    // dA0 = G_j W2_0 (the W2^T copy), and Q = G_j G_<j^T
+    {
+      Spec sp[2] = {};
+      sp[0].part[0].a = opnd(gb + (long long)r0 * D, lbd, D, T);
+      sp[0].part[0].b = opnd(w2t_old, (long long)h * D, D, h);
+      sp[0].part[0].k_len = D;
+      sp[0].nparts = 1;
+      sp[0].m_extent = T; sp[0].n = h; sp[0].m_store = T; sp[0].n_store = h;
+      sp[1] = sp[0];
+      sp[1].part[0].b = opnd(gb, lbd, D, kp);
+      sp[1].n = kp; sp[1].n_store = kp;
+      EpiStore<float, E> epi;
+      epi.p0 = da0; epi.ls0 = lth; epi.ld0 = h; epi.s0 = 1.0f;
+      epi.p1 = qg; epi.ls1 = ltb; epi.ld1 = Bp; epi.s1 = 1.0f;
+      if ((e = launch_gemm<E>(pick_tile(T, h, Lc), sp, j > 0 ? 2 : 1, Lc, epi, s)) !=
+          hipSuccess)
+        return hip_fail(e, "launch block dA");
+    }
+    // dA = dA0 - lr Q A_<j  ->  dZ^T = (dA * SiLU')^T
+    {
+      Spec sp{};
+      sp.part[0].a = opnd(qg, ltb, Bp, T);
+      sp.part[0].b = opnd(abt, lbh, Bp, h);
+      sp.part[0].k_len = kp;
+      sp.nparts = 1;
+      sp.m_extent = T; sp.n = h; sp.m_store = T; sp.n_store = h;
+      EpiBlkDZ<E> epi;
+      epi.da0 = da0; epi.lsa = lth; epi.sd = sdb; epi.dzt = dzt; epi.ls = lbh;
+      epi.h = h; epi.Btp = Bp; epi.r0 = r0; epi.lr = c.lr;
+      if ((e = launch_gemm<E>(pick_tile(T, h, Lc), &sp, 1, Lc, epi, s, nullptr,
+                              H->at<float>(Ly.split))) != hipSuccess)
+        return hip_fail(e, "launch block dZ");
+    }
+    H->timing_end(MONE_STAGE_BSEQ, s);
+  }
+
+  // The block's updates: W2 -= lr G^T A (problem 1 of the backward's epilogue; problem 0
+  // empty) writing -W2 and the other W2^T copy; W1 -= lr dZ^T X writing its copy
+  H->timing_begin(MONE_STAGE_BUPD, s);
+  {
+    Spec sp[2] = {};
+    sp[0].part[0].a = opnd(w2t_old, (long long)h * D, D, 0);
+    sp[0].part[0].b = opnd(gb, lbd, D, 0);
+    sp[0].part[0].k_len = 0;
+    sp[0].nparts = 1;
+    sp[0].m_extent = 0; sp[0].n = 0; sp[0].m_store = 0; sp[0].n_store = 0;
+    sp[1].part[0].a = opnd(gbt, lbd, Bp, D);
+    sp[1].part[0].b = opnd(abt, lbh, Bp, h);
+    sp[1].part[0].k_len = Bt;
+    sp[1].nparts = 1;
+    sp[1].m_extent = D; sp[1].n = h; sp[1].m_store = D; sp[1].n_store = h;
+    EpiBwdW2<E, false> epi{};
+    epi.w2 = H->w2; epi.w2n = H->at<E>(Ly.w2c); epi.w2t = w2t_new;
+    epi.ls2 = (long long)D * h; epi.h = h; epi.D = D; epi.lr = c.lr;
+    epi.loss_part = H->at<float>(Ly.loss_part);
+    epi.parts_per_layer = Ly.loss_per_layer;
+    epi.nip = 0;
+    if ((e = launch_gemm<E>(upd_tile(D, h, Bt, Lc), sp, 2, Lc, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch block W2 update");
+  }
+  {
+    Spec sp{};
+    sp.part[0].a = opnd(dzt, lbh, Bp, h);
+    sp.part[0].b = opnd(xt, lbx, Bp, d);
+    sp.part[0].k_len = Bt;
+    sp.nparts = 1;
+    sp.m_extent = h; sp.n = d; sp.m_store = h; sp.n_store = d;
+    EpiW1<E, false> epi{};
+    epi.w1 = H->w1; epi.w1s = bf ? H->at<E>(Ly.w1c) : nullptr;
+    epi.ls1 = (long long)h * d; epi.d = d; epi.w1_copy = bf ? 1 : 0; epi.lr = c.lr; epi.h = h;
+    if ((e = launch_gemm<E>(upd_tile(h, d, Bt, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch block W1 update");
+  }
+  H->timing_end(MONE_STAGE_BUPD, s);
+  H->w2t_cur ^= 1;
+  H->last_n = T;
   return MONE_OK;
 }
 
@@ -559,11 +822,49 @@ int mone_ttl_segment(mone_ttl* H, const void* x, int32_t n_tokens, void* stream)
   if (!aligned16(x)) return fail(MONE_EINVAL, "x must be 16-byte aligned");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const bool paper = H->cfg.optimizer == MONE_OPT_PAPER;
+  const long long lsx = (long long)n_tokens * H->cfg.d_model;
   if (H->cfg.act_dtype == MONE_BF16)
-    return paper ? run_segment<bf16_t, true>(H, x, n_tokens, s)
-                 : run_segment<bf16_t, false>(H, x, n_tokens, s);
-  return paper ? run_segment<float, true>(H, x, n_tokens, s)
-               : run_segment<float, false>(H, x, n_tokens, s);
+    return paper ? run_segment<bf16_t, true>(H, x, lsx, n_tokens, s)
+                 : run_segment<bf16_t, false>(H, x, lsx, n_tokens, s);
+  return paper ? run_segment<float, true>(H, x, lsx, n_tokens, s)
+               : run_segment<float, false>(H, x, lsx, n_tokens, s);
+}
+
+int mone_ttl_segments(mone_ttl* H, const void* x, int64_t layer_stride, int32_t n_segments,
+                      void* stream) {
+  g_err[0] = 0;
+  if (!H) return fail(MONE_EINVAL, "handle is NULL");
+  if (n_segments < 0) return fail(MONE_EINVAL, "n_segments = %d is negative", n_segments);
+  if (n_segments == 0) return MONE_OK;
+  const mone_ttl_config& c = H->cfg;
+  const long long T = c.seg_len, d = c.d_model;
+  if (layer_stride < (long long)n_segments * T * d)
+    return fail(MONE_EINVAL, "layer_stride %lld below n_segments * seg_len * d_model = %lld",
+                (long long)layer_stride, (long long)n_segments * T * d);
+  if (!x) return fail(MONE_EINVAL, "x is NULL");
+  const long long E = c.act_dtype == MONE_BF16 ? 2 : 4;
+  if (!aligned16(x) || (layer_stride * E) % 16 != 0)
+    return fail(MONE_EINVAL, "x and layer_stride * element size must be 16-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const bool bf = c.act_dtype == MONE_BF16, paper = c.optimizer == MONE_OPT_PAPER;
+  const int blk = H->lay.blk;
+  int done = 0, rc = MONE_OK;
+  while (done < n_segments && rc == MONE_OK) {
+    const int nb = blk > 1 ? (n_segments - done < blk ? n_segments - done : blk) : 1;
+    const unsigned char* xs = reinterpret_cast<const unsigned char*>(x) + done * T * d * E;
+    if (nb > 1) {
+      rc = bf ? run_block<bf16_t>(H, reinterpret_cast<const bf16_t*>(xs), layer_stride, nb, s)
+              : run_block<float>(H, reinterpret_cast<const float*>(xs), layer_stride, nb, s);
+    } else if (bf) {
+      rc = paper ? run_segment<bf16_t, true>(H, xs, layer_stride, (int)T, s)
+                 : run_segment<bf16_t, false>(H, xs, layer_stride, (int)T, s);
+    } else {
+      rc = paper ? run_segment<float, true>(H, xs, layer_stride, (int)T, s)
+                 : run_segment<float, false>(H, xs, layer_stride, (int)T, s);
+    }
+    done += nb;
+  }
+  return rc;
 }
 
 int mone_ttl_step_noalloc(const mone_ttl_config* cfg, const void* wkv, float* w1, float* w2,
@@ -590,8 +891,9 @@ int mone_ttl_step_noalloc(const mone_ttl_config* cfg, const void* wkv, float* w1
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   mone_ttl H;  // on the stack: the handle's state for this one step
   if ((rc = init_state(&H, cfg, Ly, wkv, w1, w2, nullptr, ws, s)) != MONE_OK) return rc;
-  return cfg->act_dtype == MONE_BF16 ? run_segment<bf16_t, false>(&H, x, n_tokens, s)
-                                     : run_segment<float, false>(&H, x, n_tokens, s);
+  const long long lsx = (long long)n_tokens * cfg->d_model;
+  return cfg->act_dtype == MONE_BF16 ? run_segment<bf16_t, false>(&H, x, lsx, n_tokens, s)
+                                     : run_segment<float, false>(&H, x, lsx, n_tokens, s);
 }
 
 int mone_memory_kv(mone_ttl* H, const void* xq, int32_t q, void* kv, int32_t kv_dtype,

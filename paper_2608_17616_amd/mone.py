@@ -21,7 +21,8 @@ MONE_F32, MONE_BF16 = 0, 1
 MONE_LOSS_MSE_SUM, MONE_LOSS_MSE_MEAN, MONE_LOSS_NIP = 0, 1, 2
 MONE_OPT_SGD, MONE_OPT_PAPER = 0, 1
 MONE_ALL_STAGES = 0xFFFFFFFF
-STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2", "rate", "renorm", "attn")
+STAGES = ("xt", "fwd1", "fwd2", "bwd", "upd", "kv1", "kv2", "rate", "renorm", "attn", "bfwd",
+          "bseq", "bupd")
 MONE_N_STAGES = len(STAGES)
 
 SW_STAGES = ("rate", "proj", "keys", "da", "fwd", "upd", "qproj", "qkeys", "qfwd", "qout", "qkv",
@@ -30,7 +31,7 @@ MONE_SW_N_STAGES = len(SW_STAGES)
 
 # every symbol include/mone_ttl.h and include/mone_swiglu.h declare
 EXPORTS = ("mone_ttl_workspace_bytes", "mone_ttl_init", "mone_ttl_init_paper",
-           "mone_ttl_segment", "mone_ttl_step_noalloc", "mone_memory_kv",
+           "mone_ttl_segment", "mone_ttl_segments", "mone_ttl_step_noalloc", "mone_memory_kv",
            "mone_memory_attention",
            "mone_ttl_loss", "mone_ttl_destroy", "mone_ttl_last_error",
            "mone_ttl_set_stage_timing", "mone_ttl_stage_times",
@@ -50,7 +51,7 @@ class mone_ttl_config(ctypes.Structure):
                 ("d_hidden", ctypes.c_int32), ("d_kv", ctypes.c_int32),
                 ("seg_len", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
                 ("loss", ctypes.c_int32), ("lr", ctypes.c_float),
-                ("optimizer", ctypes.c_int32)]
+                ("optimizer", ctypes.c_int32), ("block_tokens", ctypes.c_int32)]
 
 
 class mone_paper_optimizer(ctypes.Structure):
@@ -110,6 +111,7 @@ def lib() -> ctypes.CDLL:
                                           ctypes.POINTER(mone_paper_optimizer), vp,
                                           ctypes.c_size_t, vp]
         L.mone_ttl_segment.argtypes = [vp, vp, i32, vp]
+        L.mone_ttl_segments.argtypes = [vp, vp, ctypes.c_int64, i32, vp]
         L.mone_ttl_step_noalloc.argtypes = [cfgp, vp, vp, vp, vp, i32, vp]
         L.mone_memory_kv.argtypes = [vp, vp, i32, vp, i32, vp]
         L.mone_memory_attention.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, i32, vp]
@@ -169,19 +171,20 @@ def _stream(s) -> int | None:
 
 
 def make_config(n_layers, d_model, d_hidden, d_kv, seg_len, act_dtype, loss, lr,
-                optimizer="sgd"):
+                optimizer="sgd", block_tokens=0):
     dt = {"f32": MONE_F32, "bf16": MONE_BF16}.get(act_dtype, act_dtype)
     ls = {"mse_sum": MONE_LOSS_MSE_SUM, "mse_mean": MONE_LOSS_MSE_MEAN,
           "nip": MONE_LOSS_NIP}.get(loss, loss)
     op = {"sgd": MONE_OPT_SGD, "paper": MONE_OPT_PAPER}.get(optimizer, optimizer)
     return mone_ttl_config(int(n_layers), int(d_model), int(d_hidden), int(d_kv), int(seg_len),
-                           int(dt), int(ls), float(lr), int(op))
+                           int(dt), int(ls), float(lr), int(op), int(block_tokens))
 
 
 def config_from(cfg) -> mone_ttl_config:
     """C config of a configs.MoneConfig."""
     return make_config(cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_kv, cfg.seg_len,
-                       cfg.act_dtype, cfg.loss, cfg.lr, cfg.optimizer)
+                       cfg.act_dtype, cfg.loss, cfg.lr, cfg.optimizer,
+                       getattr(cfg, "block_tokens", 0))
 
 
 def mone_ttl_last_error() -> str:
@@ -219,6 +222,11 @@ def paper_optimizer(rate_w, rate_b, decay_w, decay_b, mom1, mom2) -> mone_paper_
 
 def mone_ttl_segment(handle: int, x, n_tokens: int, stream=None) -> None:
     _check(lib().mone_ttl_segment(handle, _ptr(x), int(n_tokens), _stream(stream)))
+
+
+def mone_ttl_segments(handle: int, x, layer_stride: int, n_segments: int, stream=None) -> None:
+    _check(lib().mone_ttl_segments(handle, _ptr(x), int(layer_stride), int(n_segments),
+                                   _stream(stream)))
 
 
 def mone_ttl_step_noalloc(cfg: mone_ttl_config, wkv, w1, w2, x, n_tokens: int,
@@ -289,6 +297,13 @@ class TtlSession:
     def segment(self, x, n_tokens=None, stream=None):
         n = x.shape[1] if n_tokens is None else n_tokens
         mone_ttl_segment(self.handle, x, n, stream)
+
+    def segments(self, x, n_segments=None, stream=None):
+        """x: [L, S*T, d] (or a view with that layout: each layer's tokens contiguous, layer
+        stride x.stride(0)); runs the first n_segments (default S) segments of T tokens."""
+        T = self.cfg.seg_len
+        n = x.shape[1] // T if n_segments is None else n_segments
+        mone_ttl_segments(self.handle, x, x.stride(0), n, stream)
 
     def memory_kv(self, xq, kv, stream=None):
         import torch

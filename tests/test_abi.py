@@ -276,3 +276,24 @@ def test_noalloc_step_rejects_before_any_hip_call():
     with pytest.raises(mone.MoneError) as e:
         mone.mone_ttl_step_noalloc(small, dummy, dummy, dummy, None, 16, 0)
     assert e.value.code == mone.MONE_EINVAL
+
+
+def test_block_form_workspace_and_config_checks():
+    base = dict(n_layers=2, d_model=128, d_hidden=192, d_kv=64, seg_len=64, act_dtype="bf16",
+                loss="mse_sum", lr=1e-3)
+    ws = lambda **kw: mone.mone_ttl_workspace_bytes(mone.make_config(**dict(base, **kw)))  # noqa
+    none = ws(block_tokens=-1)
+    assert ws() == none  # small memories: no block form by default
+    L, d, h, D, Tp, Bp, E = 2, 128, 192, 128, 256, 512, 2
+    extra = L * (4 * Bp * (h + D) + E * (Bp * Bp + 3 * Bp * h + 2 * Bp * D + h * Bp + d * Bp)
+                 + 4 * Tp * (D + h) + 2 * E * Tp * Bp)
+    assert extra <= ws(block_tokens=512) - none <= extra + 14 * 256
+    # the 64-token workload takes the block form by default
+    st = configs.STRESS
+    assert (mone.mone_ttl_workspace_bytes(mone.config_from(st))
+            > mone.mone_ttl_workspace_bytes(mone.config_from(st.with_(block_tokens=-1))))
+    for bad in (dict(block_tokens=100), dict(block_tokens=64), dict(block_tokens=8192),
+                dict(block_tokens=512, loss="nip"), dict(block_tokens=512, optimizer="paper"),
+                dict(block_tokens=500, seg_len=100)):
+        with pytest.raises(mone.MoneError):
+            ws(**bad)
