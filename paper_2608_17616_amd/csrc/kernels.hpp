@@ -1217,6 +1217,33 @@ struct EpiBlkDZ : EpiBase {
   }
 };
 
+// Block form, the block's updates in one launch: problem 0 is the W2 update (G^T A: the W2
+// update problem of EpiBwdW2, writing -W2 and the next W2^T copy), problem 1 the W1 update
+// (dZ^T X: EpiW1).  Both read-modify-write epilogues stream their masters in one grid.
+template <typename E>
+struct EpiBlkUpd : EpiBase {
+  static constexpr bool kPre = true;
+  static constexpr bool kCols = true;
+  static constexpr bool kWriteback = true;
+  EpiBwdW2<E, false> w2;
+  EpiW1<E, false> w1;
+  __device__ __forceinline__ bool has_cols(int pi) const { return pi == 0; }
+  __device__ __forceinline__ void pre8(int pi, int layer, int row, int col, int M, int N,
+                                       float (&x)[8]) const {
+    if (pi == 0) w2.pre8(1, layer, row, col, M, N, x);
+    else w1.pre8(0, layer, row, col, M, N, x);
+  }
+  __device__ __forceinline__ float rows8(int pi, int layer, int row, int col, int M, int N,
+                                         float (&v)[8], const float (&x)[8]) const {
+    return pi == 0 ? w2.rows8(1, layer, row, col, M, N, v, x)
+                   : w1.rows8(0, layer, row, col, M, N, v, x);
+  }
+  __device__ __forceinline__ void cols8(int, int layer, int row, int col, int M, int N,
+                                        const float (&v)[8]) const {
+    w2.cols8(1, layer, row, col, M, N, v);
+  }
+};
+
 // ------------------------------------------------------------------------------------------
 // Data-movement helpers
 

@@ -571,42 +571,29 @@ int run_block(mone_ttl* H, const E* x, long long lsx, int nb, hipStream_t s) {
     H->timing_end(MONE_STAGE_BSEQ, s);
   }
 
-  // The block's updates: W2 -= lr G^T A (problem 1 of the backward's epilogue; problem 0
-  // empty) writing -W2 and the other W2^T copy; W1 -= lr dZ^T X writing its copy
+  // The block's updates in one launch: W2 -= lr G^T A (writing -W2 and the other W2^T copy)
+  // and W1 -= lr dZ^T X (writing its copy)
   H->timing_begin(MONE_STAGE_BUPD, s);
   {
     Spec sp[2] = {};
-    sp[0].part[0].a = opnd(w2t_old, (long long)h * D, D, 0);
-    sp[0].part[0].b = opnd(gb, lbd, D, 0);
-    sp[0].part[0].k_len = 0;
+    sp[0].part[0].a = opnd(gbt, lbd, Bp, D);
+    sp[0].part[0].b = opnd(abt, lbh, Bp, h);
+    sp[0].part[0].k_len = Bt;
     sp[0].nparts = 1;
-    sp[0].m_extent = 0; sp[0].n = 0; sp[0].m_store = 0; sp[0].n_store = 0;
-    sp[1].part[0].a = opnd(gbt, lbd, Bp, D);
-    sp[1].part[0].b = opnd(abt, lbh, Bp, h);
+    sp[0].m_extent = D; sp[0].n = h; sp[0].m_store = D; sp[0].n_store = h;
+    sp[1].part[0].a = opnd(dzt, lbh, Bp, h);
+    sp[1].part[0].b = opnd(xt, lbx, Bp, d);
     sp[1].part[0].k_len = Bt;
     sp[1].nparts = 1;
-    sp[1].m_extent = D; sp[1].n = h; sp[1].m_store = D; sp[1].n_store = h;
-    EpiBwdW2<E, false> epi{};
-    epi.w2 = H->w2; epi.w2n = H->at<E>(Ly.w2c); epi.w2t = w2t_new;
-    epi.ls2 = (long long)D * h; epi.h = h; epi.D = D; epi.lr = c.lr;
-    epi.loss_part = H->at<float>(Ly.loss_part);
-    epi.parts_per_layer = Ly.loss_per_layer;
-    epi.nip = 0;
-    if ((e = launch_gemm<E>(upd_tile(D, h, Bt, Lc), sp, 2, Lc, epi, s)) != hipSuccess)
-      return hip_fail(e, "launch block W2 update");
-  }
-  {
-    Spec sp{};
-    sp.part[0].a = opnd(dzt, lbh, Bp, h);
-    sp.part[0].b = opnd(xt, lbx, Bp, d);
-    sp.part[0].k_len = Bt;
-    sp.nparts = 1;
-    sp.m_extent = h; sp.n = d; sp.m_store = h; sp.n_store = d;
-    EpiW1<E, false> epi{};
-    epi.w1 = H->w1; epi.w1s = bf ? H->at<E>(Ly.w1c) : nullptr;
-    epi.ls1 = (long long)h * d; epi.d = d; epi.w1_copy = bf ? 1 : 0; epi.lr = c.lr; epi.h = h;
-    if ((e = launch_gemm<E>(upd_tile(h, d, Bt, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
-      return hip_fail(e, "launch block W1 update");
+    sp[1].m_extent = h; sp[1].n = d; sp[1].m_store = h; sp[1].n_store = d;
+    EpiBlkUpd<E> epi{};
+    epi.w2.w2 = H->w2; epi.w2.w2n = H->at<E>(Ly.w2c); epi.w2.w2t = w2t_new;
+    epi.w2.ls2 = (long long)D * h; epi.w2.h = h; epi.w2.D = D; epi.w2.lr = c.lr;
+    epi.w1.w1 = H->w1; epi.w1.w1s = bf ? H->at<E>(Ly.w1c) : nullptr;
+    epi.w1.ls1 = (long long)h * d; epi.w1.d = d; epi.w1.w1_copy = bf ? 1 : 0;
+    epi.w1.lr = c.lr; epi.w1.h = h;
+    if ((e = launch_gemm<E>(upd_tile(h, d, Bt, Lc), sp, 2, Lc, epi, s)) != hipSuccess)
+      return hip_fail(e, "launch block updates");
   }
   H->timing_end(MONE_STAGE_BUPD, s);
   H->w2t_cur ^= 1;
