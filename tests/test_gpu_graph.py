@@ -74,6 +74,43 @@ def test_config_form_segment_pairs_replay_bitwise(cfg):
     eager.close()
 
 
+GRAPH_BLOCK = configs.MoneConfig("graph_block_bf16", n_layers=3, d_model=192, d_hidden=320,
+                                 d_kv=64, seg_len=64, n_context=1024, act_dtype="bf16", lr=2e-2,
+                                 block_tokens=512)
+
+
+def test_block_form_replays_bitwise():
+    # mone_ttl_segments in the block form: 16 segments = two blocks of 8, so the W2^T copies
+    # alternate twice per call and the captured call can be replayed as it is
+    cfg = GRAPH_BLOCK
+    print(f"[graph] block form {cfg.name}", flush=True)
+    prob = DeviceProblem(cfg, [])
+    T, S = cfg.seg_len, 16
+    ctx = [torch.cat([prob.segment(16 * r + s, record=False) for s in range(S)], dim=1)
+           for r in range(3)]
+    w1e, w2e = prob.w1.clone(), prob.w2.clone()
+    eager = mone.TtlSession(cfg, prob.wkv, w1e, w2e)
+    w1g, w2g = prob.w1.clone(), prob.w2.clone()
+    sess = mone.TtlSession(cfg, prob.wkv, w1g, w2g)
+    xg = torch.empty_like(ctx[0])
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        sess.segments(xg)
+    torch.cuda.synchronize()
+    assert torch.equal(w1g, prob.w1) and torch.equal(w2g, prob.w2)  # capture ran nothing
+    for r in range(3):
+        xg.copy_(ctx[r])
+        g.replay()
+        eager.segments(ctx[r])
+        torch.cuda.synchronize()
+        assert torch.equal(w1g, w1e) and torch.equal(w2g, w2e), f"replay {r}"
+        assert np.array_equal(sess.loss(), eager.loss())
+        float((w1g.abs().sum() + w2g.abs().sum()).item())  # eager work between replays
+    sess.close()
+    eager.close()
+
+
 def _sw_session(cfg):
     from test_gpu_swiglu import SwProblem
     return SwProblem(cfg)
