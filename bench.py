@@ -196,10 +196,12 @@ def cpu_baseline(cfg, w1, w2, wkv, xs, budget_s, meta=None):
         return ht.record(done * cfg.seg_len / t / cfg.n_layers, t, done, cfg)
 
 
-def sw_stage_work(cfg):
+def sw_stage_work(cfg, prep=1):
     """Algorithmic FLOPs and bytes of one launch of each stage of the paper-form memory (all
-    layers and heads; B = L H head problems of d_h x d_h; T tokens)."""
+    layers and heads; B = L H head problems of d_h x d_h; T tokens).  RATE, PROJ and KEYS
+    launches cover `prep` segments at a time."""
     L, d, H, dh, T = cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.d_head, cfg.seg_len
+    g = prep
     E = 2 if cfg.act_dtype == "bf16" else 4
     B = L * H
     paper = cfg.optimizer == "paper"
@@ -208,12 +210,12 @@ def sw_stage_work(cfg):
     # in the same epilogue)
     upd_w = 3 * dh * dh * (8 + E + (8 if paper else 0))
     return {
-        "rate": (L * 4 * T * d, L * (T * d * E + 2 * d * 4 + T * 4)),
+        "rate": (g * L * 4 * T * d, g * L * (T * d * E + 2 * d * 4 + T * 4)),
         # the projections with the elementwise preprocessing fused: X and P in; K', dY0 and
         # dY^T out
-        "proj": (L * 2 * T * 2 * d * d, L * (4 * T * d + 2 * d * d) * E),
+        "proj": (g * L * 2 * T * 2 * d * d, L * (4 * g * T * d + 2 * d * d) * E),
         # K' in; K and K^T out
-        "keys": (0, 3 * L * T * d * E),
+        "keys": (0, 3 * g * L * T * d * E),
         "da": (B * 2 * T * dh * dh, B * (dh * dh + 2 * T * dh) * E),
         "fwd": (B * 2 * T * 2 * dh * dh, B * (2 * dh * dh + 5 * T * dh) * E + L * T * 4),
         "upd": (B * 2 * T * 3 * dh * dh, B * (5 * dh * T * E + upd_w)),
@@ -314,14 +316,16 @@ def sw_cpu_baseline(cfg, host, xs, budget_s, meta):
 
 def run_swiglu(args):
     """The paper-form memory (SwiGLU per fast-weight head) at the paper's shape: one step is
-    every segment of the context through mone_swiglu_segment (all layers and heads)."""
+    every segment of the context through one mone_swiglu_segments call (all layers and heads;
+    --call segment: one call per segment)."""
     import numpy as np
     import torch
 
     from paper_2608_17616_amd import configs, inputs, mone
 
     cfg = configs.SW_CONFIGS[args.config if args.config in configs.SW_CONFIGS
-                             else "sw_qwen0.5b"].with_(optimizer=args.optimizer)
+                             else "sw_qwen0.5b"].with_(optimizer=args.optimizer,
+                                                       prep_segments=args.prep_segments)
     L, d, H, dh, T = cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.d_head, cfg.seg_len
     S = args.segments or cfg.n_segments
     dev = torch.device("cuda:0")
@@ -336,9 +340,10 @@ def run_swiglu(args):
     k_shift = inputs.device_normal_(torch.empty(L, d, dtype=f32, device=dev), 0.1, gen)
     w = [inputs.device_normal_(torch.empty(L, H, dh, dh, dtype=f32, device=dev),
                                1 / np.sqrt(dh), gen) for _ in range(3)]
-    ctx = torch.empty(S, L, T, d, dtype=act, device=dev)
+    # each layer's part of the context in one piece: token t of segment s at ctx[l, s*T + t]
+    ctx = torch.empty(L, S * T, d, dtype=act, device=dev)
     for s in range(S):
-        inputs.device_normal_(ctx[s], 1.0, gen)
+        inputs.device_normal_(ctx[:, s * T:(s + 1) * T], 1.0, gen)
     opt = None
     if cfg.optimizer == "paper":
         opt = (inputs.device_normal_(torch.empty(L, d, dtype=f32, device=dev), 1 / np.sqrt(d),
@@ -353,7 +358,8 @@ def run_swiglu(args):
     if n_cpu:
         host = (proj[0].double().cpu().numpy(), k_scale[0].double().cpu().numpy(),
                 k_shift[0].double().cpu().numpy(), tuple(t[0].double().cpu().numpy() for t in w))
-        cpu_in = (host, [ctx[s, 0].double().cpu().numpy() for s in range(n_cpu)])
+        cpu_in = (host, [ctx[0, s * T:(s + 1) * T].double().cpu().numpy()
+                         for s in range(n_cpu)])
 
     # the read: Q query tokens through the memory (Qwen2.5-0.5B's attention: 14 query heads and
     # 2 key/value heads of 64, d_kv = 128), then the memory-injected attention
@@ -385,9 +391,17 @@ def run_swiglu(args):
     Hd = sess.handle
     sptr = stream.cuda_stream
 
+    lstride = ctx.stride(0)
+    # segments per preprocessing batch, as the library's header states the default
+    prep = 1 if args.call == "segment" else (
+        cfg.prep_segments if cfg.prep_segments > 0 else (4 if T % 64 == 0 else 1))
+
     def step():
-        for s in range(S):
-            mone.mone_swiglu_segment(Hd, ctx[s], T, sptr)
+        if args.call == "segments":
+            mone.mone_swiglu_segments(Hd, ctx, lstride, S, sptr)
+        else:
+            for s in range(S):
+                mone.mone_swiglu_segments(Hd, ctx[:, s * T:], lstride, 1, sptr)
         mone.mone_swiglu_read(Hd, crd, xq, Q, kv, mone.MONE_F32, sptr)
         mone.mone_swiglu_attention(Hd, d_kv, aq, ak, av, kv, mone.MONE_F32, Q, hq, hkv, aout,
                                    mone.MONE_F32, sptr)
@@ -411,7 +425,7 @@ def run_swiglu(args):
     value = tokens / elapsed
     flop_tok = cfg.flops_per_token()
     peak = PEAK_BF16_TFLOPS if cfg.act_dtype == "bf16" else PEAK_F32_TFLOPS
-    work = dict(sw_stage_work(cfg), **sw_read_work(cfg, Q, d_kv, hq, hkv))
+    work = dict(sw_stage_work(cfg, prep), **sw_read_work(cfg, Q, d_kv, hq, hkv))
     stages = stage_table(stimes, work)
     dfl, dby = work[dom]
     davg = dms / dcnt / 1e3
@@ -484,6 +498,9 @@ def main():
     ap.add_argument("--block-tokens", type=int, default=0,
                     help="configurations' memory: tokens per block of the block form (0: the "
                          "library's choice, -1: none)")
+    ap.add_argument("--prep-segments", type=int, default=0,
+                    help="paper-form memory: segments per preprocessing batch (0: the "
+                         "library's choice)")
     ap.add_argument("--memory", default="config", choices=("config", "swiglu"),
                     help="config: the configurations' 2-layer memory (default); swiglu: the "
                          "paper-form SwiGLU memory per fast-weight head at the paper's shape")

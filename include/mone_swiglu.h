@@ -48,6 +48,11 @@ typedef struct {
   int32_t optimizer; /* mone_optimizer */
   float lr;          /* learning rate (finite, may be 0); scales the paper optimiser's rates */
   float rope_base;   /* RoPE base (> 0; the usual value is 10000) */
+  int32_t prep_segments; /* segments whose weight-independent preprocessing (rates, projections,
+                            key normalisation and RoPE) mone_swiglu_segments computes in one
+                            batch, in [0, 16]: 0 chooses 4 when seg_len is a multiple of 64
+                            (else 1); above 1 needs seg_len a multiple of 64.  The workspace
+                            holds that many copies of the preprocessing buffers. */
 } mone_swiglu_config;
 
 /* Frozen parameters (borrowed for the handle's lifetime, read only). */
@@ -104,6 +109,21 @@ int mone_swiglu_init(mone_swiglu** out, const mone_swiglu_config* cfg,
  * memset or synchronisation) and keeps no state that alternates between calls, so one call may
  * be captured in a HIP graph (timing hooks off) and replayed once per segment. */
 int mone_swiglu_segment(mone_swiglu* h, const void* x, int32_t n_tokens, void* stream);
+
+/* Several consecutive whole segments of seg_len tokens in one call (Sec. 3.1; each layer's
+ * chain in context order, Sec. 3.4): the same as n_segments calls of mone_swiglu_segment.
+ *   x             token t of segment s of layer l at x + l * layer_stride + (s * seg_len + t)
+ *                 * d_model (elements of act_dtype): each layer's part of the context in one
+ *                 piece.
+ *   layer_stride  elements between layers, >= n_segments * seg_len * d_model; x and
+ *                 layer_stride * element size 16-byte aligned.
+ *   n_segments    >= 0 (0 is a no-op).
+ * The preprocessing that does not depend on the fast weights (the paper optimiser's rates and
+ * decay, the key/value projections with their affine step and SiLU, the keys' normalisation
+ * and segment-local RoPE) runs once for up to prep_segments segments at a time, as larger
+ * launches; each segment's memory step (DA, FWD, UPD) then follows in order. */
+int mone_swiglu_segments(mone_swiglu* h, const void* x, int64_t layer_stride, int32_t n_segments,
+                         void* stream);
 
 /* The segment loss L_s of the last non-empty segment, per layer, at the weights that step
  * started from (unweighted by the rates).  out_host: host float[L].  Synchronises `stream`.

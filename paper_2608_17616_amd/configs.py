@@ -95,6 +95,7 @@ class SwigluConfig:
     rope_base: float = 10000.0
     n_query: int = 64
     seed: int = 0
+    prep_segments: int = 0  # preprocessing batch of multi-segment calls (0: library default)
 
     @property
     def n_segments(self) -> int:

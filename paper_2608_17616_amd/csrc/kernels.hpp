@@ -1354,8 +1354,9 @@ __device__ __forceinline__ float softplusf_(float z) {
 
 // Per-token rates rate[l][j] = lr * softplus(u_l . x_j + b_u[l]) for j < n (0 for n <= j < Tp),
 // and per-block sums of v_l . x_j over the block's kRateTokens tokens (summed in token order),
-// from which decay_kernel forms the momentum decay.  Grid (Tp / kRateTokens, L), 256 threads:
-// each wave takes kRateTokens / 4 consecutive tokens.
+// from which decay_kernel forms the momentum decay.  Grid (Tp / kRateTokens, L, segments), 256
+// threads: each wave takes kRateTokens / 4 consecutive tokens.  Segment z reads x + z * x_ss
+// and writes rate + z * rate_ss and vpart + z * vpart_ss.
 constexpr int kRateTokens = 16;
 template <typename E>
 __global__ __launch_bounds__(256) void rate_kernel(const E* __restrict__ x, long long x_ls, int d,
@@ -1363,11 +1364,16 @@ __global__ __launch_bounds__(256) void rate_kernel(const E* __restrict__ x, long
                                                    const float* __restrict__ bu,
                                                    const float* __restrict__ v, float lr,
                                                    float* __restrict__ rate, int Tp,
-                                                   float* __restrict__ vpart) {
+                                                   float* __restrict__ vpart, long long x_ss = 0,
+                                                   long long rate_ss = 0,
+                                                   long long vpart_ss = 0) {
   constexpr int TW = kRateTokens / 4;
   const int l = blockIdx.y, j0 = blockIdx.x * kRateTokens, wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   __shared__ float wsum[4];
+  x += blockIdx.z * x_ss;
+  rate += blockIdx.z * rate_ss;
+  vpart += blockIdx.z * vpart_ss;
   // This wave's TW tokens side by side: per 8-element chunk of the lane, u and v are read once
   // and the TW tokens' loads are issued together (each token's sums keep the chunk order).
   const E* xl = x + (long long)l * x_ls;
@@ -1422,11 +1428,14 @@ __global__ __launch_bounds__(256) void rate_kernel(const E* __restrict__ x, long
         ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
 }
 
-// beta[l] = sigmoid(mean_j (v_l . x_j) + b_v[l]) = sigmoid(v_l . xbar + b_v[l]).
+// beta[l] = sigmoid(mean_j (v_l . x_j) + b_v[l]) = sigmoid(v_l . xbar + b_v[l]).  Grid
+// (ceil(L / blockDim), segments): segment y reads vpart + y * L * nblk, writes beta + y * L.
 __global__ void decay_kernel(const float* __restrict__ vpart, int nblk, int n,
                              const float* __restrict__ bv, float* __restrict__ beta, int L) {
   const int l = blockIdx.x * blockDim.x + threadIdx.x;
   if (l >= L) return;
+  vpart += (long long)blockIdx.y * L * nblk;
+  beta += (long long)blockIdx.y * L;
   float s = 0.0f;
   for (int b = 0; b < nblk; ++b) s += vpart[(long long)l * nblk + b];
   beta[l] = sigmoidf_(s / (float)n + bv[l]);

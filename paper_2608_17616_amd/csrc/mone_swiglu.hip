@@ -23,6 +23,8 @@
 //                  paper optimiser (fp32): rates [L][Tp], decay block sums
 //                  [L][Tp/kRateTokens], decay [L],
 //                  initial row norms
+// The preprocessing buffers (K', K, K^T, dY0, dY^T, rates, decay) have G copies, so that
+// mone_swiglu_segments runs RATE, PROJ and KEYS once for G consecutive segments.
 // A segment step, each stage one launch grouped over all layers (PROJ) or all B heads:
 //   [RATE]  per-token rates and momentum decay (paper optimiser)
 //   PROJ    [raw K | raw V] = X [P_k ; P_v]^T   epilogue: keys: affine, SiLU -> K';
@@ -48,10 +50,24 @@ namespace {
 
 struct SwLayout {
   int Tp, dhp, parts_max;
+  // G copies of the weight-independent preprocessing outputs (K, K^T, dY0, dY^T, the rates and
+  // the decay), so that mone_swiglu_segments can compute them for G segments in one batch;
+  // their element strides between copies
+  int G;
+  long long kh_ss, kt_ss, dy_ss, dyt_ss, rate_ss, vpart_ss, beta_ss;
   size_t kpre, kh, kt, dy, dyt, dat, at, dzgt, wig, woc, rope, gate, loss_part, loss_out;
   size_t rate, vpart, beta, n_ig, n_out;  // paper optimiser
   size_t total;
 };
+
+constexpr int kMaxPrepSegments = 16;
+
+// Segments per preprocessing batch: cfg->prep_segments, or by default 4 when segments are a
+// multiple of 64 tokens (1 otherwise: the batch maps GEMM rows to segments in 64-row steps).
+int prep_segments(const mone_swiglu_config* c) {
+  if (c->prep_segments > 0) return c->prep_segments;
+  return c->seg_len % 64 == 0 ? 4 : 1;
+}
 
 int check_sw_config(const mone_swiglu_config* c) {
   if (!c) return fail(MONE_EINVAL, "config is NULL");
@@ -73,10 +89,15 @@ int check_sw_config(const mone_swiglu_config* c) {
   if (c->d_head % 16 || c->d_head > 256)
     return fail(MONE_EUNSUPPORTED, "d_head must be a multiple of 16 in [16, 256]");
   if (c->seg_len > 65536) return fail(MONE_EUNSUPPORTED, "seg_len above 65536");
+  if (c->prep_segments < 0 || c->prep_segments > kMaxPrepSegments)
+    return fail(MONE_EINVAL, "prep_segments %d outside [0, %d]", c->prep_segments,
+                kMaxPrepSegments);
+  if (c->prep_segments > 1 && c->seg_len % 64)
+    return fail(MONE_EUNSUPPORTED, "prep_segments > 1 needs seg_len a multiple of 64");
   const long long Tp = round_up(c->seg_len, 256), d = c->d_model;
   const long long E = c->act_dtype == MONE_BF16 ? 2 : 4;
   // per-layer and per-head operand slices are addressed with 32-bit byte offsets
-  if (Tp * d * E >= (1LL << 31) || 2 * d * d * E >= (1LL << 31))
+  if (Tp * d * E * prep_segments(c) >= (1LL << 31) || 2 * d * d * E >= (1LL << 31))
     return fail(MONE_EUNSUPPORTED, "a per-layer matrix exceeds 2^31 bytes");
   return MONE_OK;
 }
@@ -97,11 +118,18 @@ SwLayout make_sw_layout(const mone_swiglu_config* c) {
     off = align_up(off + bytes, kAlign);
     return o;
   };
-  L.kpre = take(nl * Tp * d * E);
-  L.kh = take(B * Tp * dhp * E);
-  L.kt = take(B * dh * Tp * E);
-  L.dy = take(B * Tp * dhp * E);
-  L.dyt = take(B * dh * Tp * E);
+  const size_t G = (size_t)prep_segments(c);
+  L.G = (int)G;
+  L.kh_ss = L.dy_ss = (long long)(B * Tp * dhp);
+  L.kt_ss = L.dyt_ss = (long long)(B * dh * Tp);
+  L.rate_ss = (long long)(nl * Tp);
+  L.vpart_ss = (long long)(nl * (Tp / kRateTokens));
+  L.beta_ss = (long long)nl;
+  L.kpre = take(nl * G * Tp * d * E);
+  L.kh = take(G * B * Tp * dhp * E);
+  L.kt = take(G * B * dh * Tp * E);
+  L.dy = take(G * B * Tp * dhp * E);
+  L.dyt = take(G * B * dh * Tp * E);
   L.dat = take(B * dh * Tp * E);
   L.at = take(B * dh * Tp * E);
   L.dzgt = take(B * 2 * dh * Tp * E);
@@ -112,9 +140,9 @@ SwLayout make_sw_layout(const mone_swiglu_config* c) {
   L.loss_part = take(B * (size_t)L.parts_max * 4);
   L.loss_out = take(nl * 4);
   if (c->optimizer == MONE_OPT_PAPER) {
-    L.rate = take(nl * Tp * 4);
-    L.vpart = take(nl * (Tp / kRateTokens) * 4);
-    L.beta = take(nl * 4);
+    L.rate = take(G * nl * Tp * 4);
+    L.vpart = take(G * nl * (Tp / kRateTokens) * 4);
+    L.beta = take(G * nl * 4);
     L.n_ig = take(B * 2 * dh * 4);
     L.n_out = take(B * dh * 4);
   }
@@ -151,59 +179,56 @@ struct mone_swiglu {
 
 namespace {
 
+// Weight-independent preprocessing of g consecutive segments of n tokens each (g > 1: whole
+// segments of seg_len tokens, seg_len a multiple of 64), into copies 0 .. g-1: RATE (paper
+// optimiser), PROJ and KEYS, each one launch over all g segments.  x [L][g*n][d], layer
+// stride lsx.
 template <typename E, bool PAPER>
-int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
+int run_sw_prep(mone_swiglu* H, const void* x, long long lsx, int n, int g, hipStream_t s) {
   const mone_swiglu_config& c = H->cfg;
   const SwLayout& Ly = H->lay;
-  const int L = c.n_layers, d = c.d_model, NH = c.n_heads, dh = c.d_head, B = L * NH;
+  const int L = c.n_layers, d = c.d_model, NH = c.n_heads, dh = c.d_head;
   const int Tp = Ly.Tp, dhp = Ly.dhp;
-  constexpr int BK = 8 * (16 / (int)sizeof(E));
-  const int nz = (int)round_up(n, 64);   // token extent KEYS writes
-  const int kt = (int)round_up(n, BK);   // token extent of the UPD contractions
-  E* kh = H->at<E>(Ly.kh);
-  E* ktr = H->at<E>(Ly.kt);
-  E* dy = H->at<E>(Ly.dy);
-  E* dyt = H->at<E>(Ly.dyt);
-  E* dat = H->at<E>(Ly.dat);
-  E* At = H->at<E>(Ly.at);
-  E* dzgt = H->at<E>(Ly.dzgt);
-  E* wig = H->at<E>(Ly.wig);
-  E* woc = H->at<E>(Ly.woc);
+  // rows of a segment in the batched launches; one segment keeps its padded extent
+  const int seg_rows = g > 1 ? n : Tp, kpre_rows = Ly.G * Tp;
+  const int nz = g > 1 ? g * n : (int)round_up(n, 64);  // token rows KEYS writes
   float* rate = PAPER ? H->at<float>(Ly.rate) : nullptr;
-  const long long lsx = (long long)n * d, lhT = (long long)dh * Tp, lhP = (long long)Tp * dhp;
   hipError_t e;
 
   if constexpr (PAPER) {
     H->timer.begin(MONE_SW_STAGE_RATE, s);
-    rate_kernel<E><<<dim3(Tp / kRateTokens, L), dim3(256), 0, s>>>(
+    rate_kernel<E><<<dim3(Tp / kRateTokens, L, g), dim3(256), 0, s>>>(
         reinterpret_cast<const E*>(x), lsx, d, n, H->opt.rate_w, H->opt.rate_b, H->opt.decay_w,
-        c.lr, rate, Tp, H->at<float>(Ly.vpart));
-    decay_kernel<<<dim3((L + 63) / 64), dim3(64), 0, s>>>(H->at<float>(Ly.vpart),
-                                                          Tp / kRateTokens, n,
-                                                          H->opt.decay_b, H->at<float>(Ly.beta), L);
+        c.lr, rate, Tp, H->at<float>(Ly.vpart), (long long)n * d, Ly.rate_ss, Ly.vpart_ss);
+    decay_kernel<<<dim3((L + 63) / 64, g), dim3(64), 0, s>>>(H->at<float>(Ly.vpart),
+                                                             Tp / kRateTokens, n,
+                                                             H->opt.decay_b, H->at<float>(Ly.beta),
+                                                             L);
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch RATE");
     H->timer.end(MONE_SW_STAGE_RATE, s);
   }
   // PROJ: [raw K | raw V] = X [P_k ; P_v]^T; epilogue: K', dY0, dY^T
   {
     Spec sp{};
-    sp.part[0].a = opnd(x, lsx, d, n);
+    sp.part[0].a = opnd(x, lsx, d, g * n);
     sp.part[0].b = opnd(H->fz.proj, 2LL * d * d, d, 2 * d);
     sp.part[0].k_len = d;
     sp.nparts = 1;
-    sp.m_extent = n;
+    sp.m_extent = g * n;
     sp.n = 2 * d;
-    sp.m_store = -1;
+    sp.m_store = g > 1 ? g * n : -1;
     sp.n_store = 2 * d;
     EpiSwProj<E> epi;
-    epi.kpre = H->at<E>(Ly.kpre); epi.dy = dy; epi.dyt = dyt;
+    epi.kpre = H->at<E>(Ly.kpre); epi.dy = H->at<E>(Ly.dy); epi.dyt = H->at<E>(Ly.dyt);
     epi.kscale = H->fz.k_scale; epi.kshift = H->fz.k_shift; epi.rate = rate;
     epi.lr = c.lr; epi.inv_n = 1.0f / (float)n;
     epi.d = d; epi.dh = dh; epi.dhp = dhp; epi.H = NH; epi.Tp = Tp; epi.n = n;
+    epi.seg_rows = seg_rows; epi.kpre_rows = kpre_rows;
+    epi.dy_ss = Ly.dy_ss; epi.dyt_ss = Ly.dyt_ss; epi.rate_ss = Ly.rate_ss;
     H->timer.begin(MONE_SW_STAGE_PROJ, s);
     // 128 x 128 tiles (measured faster here than 256 x 256, which leave most CUs idle in
     // their second round); 64-row tiles for short segments
-    const TileShape tp = n <= 64 ? TILE_64x256 : TILE_128x128;
+    const TileShape tp = g * n <= 64 ? TILE_64x256 : TILE_128x128;
     if ((e = launch_gemm<E>(tp, &sp, 1, L, epi, s)) != hipSuccess)
       return hip_fail(e, "launch PROJ");
     H->timer.end(MONE_SW_STAGE_PROJ, s);
@@ -212,10 +237,37 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
   {
     H->timer.begin(MONE_SW_STAGE_KEYS, s);
     sw_keys_kernel<E><<<dim3(nz / 64, NH, L), dim3(256), 0, s>>>(
-        H->at<E>(Ly.kpre), d, NH, dh, dhp, Tp, H->at<float2>(Ly.rope), kh, ktr);
+        H->at<E>(Ly.kpre), d, NH, dh, dhp, Tp, H->at<float2>(Ly.rope), H->at<E>(Ly.kh),
+        H->at<E>(Ly.kt), seg_rows, kpre_rows, Ly.kh_ss, Ly.kt_ss);
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch KEYS");
     H->timer.end(MONE_SW_STAGE_KEYS, s);
   }
+  return MONE_OK;
+}
+
+// The weight-dependent part of the step of one segment of n tokens whose preprocessing is in
+// copy `cp`: DA, FWD and UPD.
+template <typename E, bool PAPER>
+int run_sw_update(mone_swiglu* H, int n, int cp, hipStream_t s) {
+  const mone_swiglu_config& c = H->cfg;
+  const SwLayout& Ly = H->lay;
+  const int L = c.n_layers, NH = c.n_heads, dh = c.d_head, B = L * NH;
+  const int Tp = Ly.Tp, dhp = Ly.dhp;
+  constexpr int BK = 8 * (16 / (int)sizeof(E));
+  const int kt = (int)round_up(n, BK);   // token extent of the UPD contractions
+  E* kh = H->at<E>(Ly.kh) + cp * Ly.kh_ss;
+  E* ktr = H->at<E>(Ly.kt) + cp * Ly.kt_ss;
+  E* dy = H->at<E>(Ly.dy) + cp * Ly.dy_ss;
+  E* dyt = H->at<E>(Ly.dyt) + cp * Ly.dyt_ss;
+  E* dat = H->at<E>(Ly.dat);
+  E* At = H->at<E>(Ly.at);
+  E* dzgt = H->at<E>(Ly.dzgt);
+  E* wig = H->at<E>(Ly.wig);
+  E* woc = H->at<E>(Ly.woc);
+  float* rate = PAPER ? H->at<float>(Ly.rate) + cp * Ly.rate_ss : nullptr;
+  float* beta = PAPER ? H->at<float>(Ly.beta) + cp * Ly.beta_ss : nullptr;
+  const long long lhT = (long long)dh * Tp, lhP = (long long)Tp * dhp;
+  hipError_t e;
   // DA: dA0^T = W_out dY0^T (A operand W_out [d_h][d_hp], B operand dY0 [tokens][d_hp])
   {
     Spec sp{};
@@ -281,7 +333,7 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
     epi.m_gate = PAPER ? H->opt.mom_gate : nullptr;
     epi.m_out = PAPER ? H->opt.mom_out : nullptr;
     epi.wig = wig; epi.woc = woc;
-    epi.beta = PAPER ? H->at<float>(Ly.beta) : nullptr;
+    epi.beta = beta;
     epi.n_ig = PAPER ? H->at<float>(Ly.n_ig) : nullptr;
     epi.n_out = PAPER ? H->at<float>(Ly.n_out) : nullptr;
     epi.lsw = (long long)dh * dh; epi.dh = dh; epi.dhp = dhp; epi.H = NH;
@@ -296,6 +348,31 @@ int run_sw_segment(mone_swiglu* H, const void* x, int n, hipStream_t s) {
     H->timer.end(MONE_SW_STAGE_UPD, s);
   }
   H->last_n = n;
+  return MONE_OK;
+}
+
+// One segment of n tokens: its preprocessing into copy 0, then its update.  x [L][n][d], layer
+// stride lsx.
+template <typename E, bool PAPER>
+int run_sw_segment(mone_swiglu* H, const void* x, long long lsx, int n, hipStream_t s) {
+  const int rc = run_sw_prep<E, PAPER>(H, x, lsx, n, 1, s);
+  return rc != MONE_OK ? rc : run_sw_update<E, PAPER>(H, n, 0, s);
+}
+
+// S whole segments from x [L][S*T][d] (layer stride lsx): preprocessing in batches of up to G
+// segments, then each segment's update in order.
+template <typename E, bool PAPER>
+int run_sw_segments(mone_swiglu* H, const void* x, long long lsx, int S, hipStream_t s) {
+  const int T = H->cfg.seg_len, G = H->lay.G;
+  const long long d = H->cfg.d_model;
+  for (int done = 0; done < S;) {
+    const int g = S - done < G ? S - done : G;
+    const E* xs = reinterpret_cast<const E*>(x) + (long long)done * T * d;
+    int rc = run_sw_prep<E, PAPER>(H, xs, lsx, T, g, s);
+    for (int cp = 0; cp < g && rc == MONE_OK; ++cp) rc = run_sw_update<E, PAPER>(H, T, cp, s);
+    if (rc != MONE_OK) return rc;
+    done += g;
+  }
   return MONE_OK;
 }
 
@@ -339,7 +416,7 @@ int run_sw_read(mone_swiglu* H, const mone_swiglu_reader* rd, const void* xq, in
   // QKEYS: per-head L2 norm and RoPE at positions 0 .. q-1
   H->timer.begin(MONE_SW_STAGE_QKEYS, s);
   sw_keys_kernel<E><<<dim3(qz / 64, NH, L), dim3(256), 0, s>>>(
-      qpre, d, NH, dh, dhp, Tp, H->at<float2>(Ly.rope), kq, H->at<E>(Ly.kt));
+      qpre, d, NH, dh, dhp, Tp, H->at<float2>(Ly.rope), kq, H->at<E>(Ly.kt), Tp, Tp, 0LL, 0LL);
   if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch QKEYS");
   H->timer.end(MONE_SW_STAGE_QKEYS, s);
   // QFWD: A = SiLU(Z) * G with [Z | G] = K_q W_ig^T; and the W_out^T copy for QOUT
@@ -504,11 +581,35 @@ int mone_swiglu_segment(mone_swiglu* H, const void* x, int32_t n_tokens, void* s
   if (!aligned16(x)) return fail(MONE_EINVAL, "x must be 16-byte aligned");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const bool paper = H->cfg.optimizer == MONE_OPT_PAPER;
+  const long long lsx = (long long)n_tokens * H->cfg.d_model;
   if (H->cfg.act_dtype == MONE_BF16)
-    return paper ? run_sw_segment<bf16_t, true>(H, x, n_tokens, s)
-                 : run_sw_segment<bf16_t, false>(H, x, n_tokens, s);
-  return paper ? run_sw_segment<float, true>(H, x, n_tokens, s)
-               : run_sw_segment<float, false>(H, x, n_tokens, s);
+    return paper ? run_sw_segment<bf16_t, true>(H, x, lsx, n_tokens, s)
+                 : run_sw_segment<bf16_t, false>(H, x, lsx, n_tokens, s);
+  return paper ? run_sw_segment<float, true>(H, x, lsx, n_tokens, s)
+               : run_sw_segment<float, false>(H, x, lsx, n_tokens, s);
+}
+
+int mone_swiglu_segments(mone_swiglu* H, const void* x, int64_t layer_stride,
+                         int32_t n_segments, void* stream) {
+  g_err[0] = 0;
+  if (!H) return fail(MONE_EINVAL, "handle is NULL");
+  if (n_segments < 0) return fail(MONE_EINVAL, "n_segments = %d is negative", n_segments);
+  if (n_segments == 0) return MONE_OK;
+  const mone_swiglu_config& c = H->cfg;
+  const long long T = c.seg_len, d = c.d_model, E = c.act_dtype == MONE_BF16 ? 2 : 4;
+  if (layer_stride < (long long)n_segments * T * d)
+    return fail(MONE_EINVAL, "layer_stride %lld below n_segments * seg_len * d_model = %lld",
+                (long long)layer_stride, (long long)n_segments * T * d);
+  if (!x) return fail(MONE_EINVAL, "x is NULL");
+  if (!aligned16(x) || (layer_stride * E) % 16 != 0)
+    return fail(MONE_EINVAL, "x and layer_stride * element size must be 16-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const bool paper = c.optimizer == MONE_OPT_PAPER;
+  if (c.act_dtype == MONE_BF16)
+    return paper ? run_sw_segments<bf16_t, true>(H, x, layer_stride, n_segments, s)
+                 : run_sw_segments<bf16_t, false>(H, x, layer_stride, n_segments, s);
+  return paper ? run_sw_segments<float, true>(H, x, layer_stride, n_segments, s)
+               : run_sw_segments<float, false>(H, x, layer_stride, n_segments, s);
 }
 
 int mone_swiglu_loss(mone_swiglu* H, float* out_host, void* stream) {

@@ -21,6 +21,10 @@ namespace {
 //                  dY^T = -eta v / n [B][d_h][Tp] (column pass, from v left in the staging)
 // Tokens >= n are stored as 0.  d and d_h are multiples of 8, so a chunk never straddles the
 // key/value boundary or a head.
+// Several consecutive segments in one launch: GEMM row r is token t = r % seg_rows of segment
+// s = r / seg_rows (seg_rows a multiple of 64, so a chunk of 8 rows stays in one segment);
+// segment s's outputs go to its own copies (K' rows s * Tp + t of kpre_rows per layer; dY0,
+// dY^T and the rates at strides dy_ss, dyt_ss, rate_ss).  One segment: seg_rows = Tp.
 template <typename E>
 struct EpiSwProj : EpiBase {
   static constexpr bool kCols = true;
@@ -30,9 +34,12 @@ struct EpiSwProj : EpiBase {
   const float* rate;                          // [L][Tp] per-token rates, or null (lr)
   float lr, inv_n;
   int d, dh, dhp, H, Tp, n;
+  int seg_rows, kpre_rows;
+  long long dy_ss, dyt_ss, rate_ss;
   __device__ __forceinline__ bool has_cols(int) const { return true; }
   __device__ __forceinline__ float rows8(int, int l, int row, int col, int, int, float (&v)[8],
                                          const float (&)[8]) const {
+    const int sg = row / seg_rows, t = row - sg * seg_rows;
     float o[8];
     if (col < d) {
       const float* sc = kscale + (long long)l * d + col;
@@ -40,32 +47,34 @@ struct EpiSwProj : EpiBase {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float u = sc[e] * v[e] + sh[e];
-        o[e] = row < n ? u * sigmoidf_(u) : 0.0f;
+        o[e] = t < n ? u * sigmoidf_(u) : 0.0f;
       }
-      store8(kpre + ((long long)l * Tp + row) * d + col, o);
+      store8(kpre + ((long long)l * kpre_rows + (long long)sg * Tp + t) * d + col, o);
     } else {
       const int c = col - d, e = c / dh, ch = c - e * dh;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const float sv = row < n ? v[i] * sigmoidf_(v[i]) : 0.0f;
+        const float sv = t < n ? v[i] * sigmoidf_(v[i]) : 0.0f;
         v[i] = sv;
         o[i] = -sv * inv_n;
       }
-      store8(dy + (((long long)l * H + e) * Tp + row) * dhp + ch, o);
+      store8(dy + sg * dy_ss + (((long long)l * H + e) * Tp + t) * dhp + ch, o);
     }
     return 0.0f;
   }
   __device__ __forceinline__ void cols8(int, int l, int row, int col, int, int,
                                         const float (&v)[8]) const {
     if (col < d) return;
+    const int sg = row / seg_rows, t = row - sg * seg_rows;
     const int c = col - d, e = c / dh, ch = c - e * dh;
+    const float* rt = rate ? rate + sg * rate_ss + (long long)l * Tp + t : nullptr;
     float o[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const float eta = rate ? rate[(long long)l * Tp + row + i] : lr;
+      const float eta = rt ? rt[i] : lr;
       o[i] = -eta * v[i] * inv_n;
     }
-    store8(dyt + (((long long)l * H + e) * dh + ch) * Tp + row, o);
+    store8(dyt + sg * dyt_ss + (((long long)l * H + e) * dh + ch) * Tp + t, o);
   }
 };
 
@@ -375,9 +384,17 @@ template <typename E>
 __global__ __launch_bounds__(256) void sw_keys_kernel(const E* __restrict__ kpre, int d, int H,
                                                       int dh, int dhp, int Tp,
                                                       const float2* __restrict__ rope,
-                                                      E* __restrict__ kh, E* __restrict__ kt) {
+                                                      E* __restrict__ kh, E* __restrict__ kt,
+                                                      int seg_rows, int kpre_rows,
+                                                      long long kh_ss, long long kt_ss) {
   __shared__ float tile[64][257];  // [token][channel]
-  const int j0 = blockIdx.x * 64, e = blockIdx.y, l = blockIdx.z, b = l * H + e;
+  // several consecutive segments: block x covers tokens j0.. of segment sg (seg_rows a multiple
+  // of 64); K' rows sg * Tp + j of kpre_rows per layer, and segment sg's copies of K and K^T
+  const int gx = blockIdx.x * 64, sg = gx / seg_rows, j0 = gx - sg * seg_rows;
+  const int e = blockIdx.y, l = blockIdx.z, b = l * H + e;
+  const E* kl = kpre + ((long long)l * kpre_rows + (long long)sg * Tp) * d;
+  kh += sg * kh_ss;
+  kt += sg * kt_ss;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int li = lane & 31, hw = lane >> 5;  // vector index, half-wave
   const int nv = dh / 8, hv = dh / 16, half = dh / 2, c = 8 * li;
@@ -386,7 +403,7 @@ __global__ __launch_bounds__(256) void sw_keys_kernel(const E* __restrict__ kpre
   for (int t = 2 * wave + hw; t < 64; t += 8) {
     const int j = j0 + t;
     float x[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
-    if (act) load8(kpre + ((long long)l * Tp + j) * d + (long long)e * dh + c, x);
+    if (act) load8(kl + (long long)j * d + (long long)e * dh + c, x);
     float ss = 0.0f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) ss += x[i] * x[i];

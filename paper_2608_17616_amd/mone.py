@@ -36,6 +36,7 @@ EXPORTS = ("mone_ttl_workspace_bytes", "mone_ttl_init", "mone_ttl_init_paper",
            "mone_ttl_loss", "mone_ttl_destroy", "mone_ttl_last_error",
            "mone_ttl_set_stage_timing", "mone_ttl_stage_times",
            "mone_swiglu_workspace_bytes", "mone_swiglu_init", "mone_swiglu_segment",
+           "mone_swiglu_segments",
            "mone_swiglu_loss", "mone_swiglu_read", "mone_swiglu_attention",
            "mone_swiglu_destroy", "mone_swiglu_set_stage_timing", "mone_swiglu_stage_times")
 
@@ -65,7 +66,7 @@ class mone_swiglu_config(ctypes.Structure):
                 ("n_heads", ctypes.c_int32), ("d_head", ctypes.c_int32),
                 ("seg_len", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
                 ("optimizer", ctypes.c_int32), ("lr", ctypes.c_float),
-                ("rope_base", ctypes.c_float)]
+                ("rope_base", ctypes.c_float), ("prep_segments", ctypes.c_int32)]
 
 
 class mone_swiglu_frozen(ctypes.Structure):
@@ -131,6 +132,7 @@ def lib() -> ctypes.CDLL:
                                        ctypes.POINTER(mone_swiglu_optimizer), vp, ctypes.c_size_t,
                                        vp]
         L.mone_swiglu_segment.argtypes = [vp, vp, i32, vp]
+        L.mone_swiglu_segments.argtypes = [vp, vp, ctypes.c_int64, i32, vp]
         L.mone_swiglu_loss.argtypes = [vp, ctypes.POINTER(ctypes.c_float), vp]
         L.mone_swiglu_read.argtypes = [vp, ctypes.POINTER(mone_swiglu_reader), vp, i32, vp, i32,
                                        vp]
@@ -329,17 +331,19 @@ class TtlSession:
 # ---------------------------------------------------------------- paper-form (SwiGLU) memory
 
 def make_swiglu_config(n_layers, d_model, n_heads, d_head, seg_len, act_dtype, optimizer, lr,
-                       rope_base=10000.0) -> mone_swiglu_config:
+                       rope_base=10000.0, prep_segments=0) -> mone_swiglu_config:
     dt = {"f32": MONE_F32, "bf16": MONE_BF16}.get(act_dtype, act_dtype)
     op = {"sgd": MONE_OPT_SGD, "paper": MONE_OPT_PAPER}.get(optimizer, optimizer)
     return mone_swiglu_config(int(n_layers), int(d_model), int(n_heads), int(d_head),
-                              int(seg_len), int(dt), int(op), float(lr), float(rope_base))
+                              int(seg_len), int(dt), int(op), float(lr), float(rope_base),
+                              int(prep_segments))
 
 
 def swiglu_config_from(cfg) -> mone_swiglu_config:
     """C config of a configs.SwigluConfig."""
     return make_swiglu_config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.d_head, cfg.seg_len,
-                              cfg.act_dtype, cfg.optimizer, cfg.lr, cfg.rope_base)
+                              cfg.act_dtype, cfg.optimizer, cfg.lr, cfg.rope_base,
+                              getattr(cfg, "prep_segments", 0))
 
 
 def mone_swiglu_workspace_bytes(cfg: mone_swiglu_config) -> int:
@@ -363,6 +367,12 @@ def mone_swiglu_init(cfg: mone_swiglu_config, frozen: mone_swiglu_frozen,
 
 def mone_swiglu_segment(handle: int, x, n_tokens: int, stream=None) -> None:
     _check(lib().mone_swiglu_segment(handle, _ptr(x), int(n_tokens), _stream(stream)))
+
+
+def mone_swiglu_segments(handle: int, x, layer_stride: int, n_segments: int,
+                         stream=None) -> None:
+    _check(lib().mone_swiglu_segments(handle, _ptr(x), int(layer_stride), int(n_segments),
+                                      _stream(stream)))
 
 
 def mone_swiglu_loss(handle: int, n_layers: int, stream=None) -> list[float]:
@@ -434,6 +444,11 @@ class SwigluSession:
     def segment(self, x, n_tokens=None, stream=None):
         n = x.shape[1] if n_tokens is None else n_tokens
         mone_swiglu_segment(self.handle, x, n, stream)
+
+    def segments(self, x, n_segments=None, stream=None):
+        """x: [L, S*T, d] (or a view with that layout, layer stride x.stride(0))."""
+        n = x.shape[1] // self.cfg.seg_len if n_segments is None else n_segments
+        mone_swiglu_segments(self.handle, x, x.stride(0), n, stream)
 
     def loss(self, stream=None):
         return mone_swiglu_loss(self.handle, self.cfg.n_layers, stream)

@@ -66,6 +66,19 @@ class SwProblem:
         self.sess.segment(x, n)
         return x
 
+    def segments(self, s0, S):
+        """Segments s0 .. s0+S-1 (whole) through one mone_swiglu_segments call, the context
+        of each layer in one piece [L, S*T, d]."""
+        cfg = self.cfg
+        T = cfg.seg_len
+        xs = [[inputs.segment_x(cfg, l, s0 + s, T) for l in range(cfg.n_layers)]
+              for s in range(S)]
+        self.segs.extend(xs)
+        x = torch.from_numpy(np.stack([np.concatenate([xs[s][l] for s in range(S)])
+                                       for l in range(cfg.n_layers)])).to("cuda", self.act)
+        self.sess.segments(x)
+        return x
+
     def frozen(self, l):
         proj, scale, shift, _ = self.host[l]
         d = self.cfg.d_model
@@ -358,3 +371,56 @@ def test_full_context_paper_shape_last_step():
         n_end = np.linalg.norm(got_w[k], axis=-1)
         n_0 = np.linalg.norm(w0[k], axis=-1)
         assert np.max(np.abs(n_end - n_0) / n_0) < 1e-4
+
+
+# ------------------------------------------------------------------------------------------
+# Several segments per call (mone_swiglu_segments): the weight-independent preprocessing of up
+# to prep_segments segments runs as one batch; each segment's memory step follows in order.
+
+@pytest.mark.parametrize("optimizer", ["sgd", "paper"])
+def test_segments_tiny_f32(optimizer):
+    # 7 segments: a batch of 4 (the default) and one of 3
+    cfg = configs.SW_TINY.with_(optimizer=optimizer)
+    p = SwProblem(cfg)
+    p.segments(0, 7)
+    _check(p, range(cfg.n_layers), 1e-4, 1e-4)
+
+
+def test_segments_tiny_bf16_batches_of_3_then_single_then_batch():
+    cfg = configs.SW_TINY.with_(name="sw_tiny_b3", act_dtype="bf16", optimizer="paper",
+                                prep_segments=3)
+    p = SwProblem(cfg)
+    p.segments(0, 5)                 # 3 + 2
+    p.segment(5, cfg.seg_len)        # one call per segment in between
+    p.segments(6, 3)
+    _check(p, range(cfg.n_layers), 2e-2, 1e-2)
+
+
+def test_segments_odd_head_width_f32():
+    cfg = configs.SwigluConfig("sw_odd_seg", n_layers=1, d_model=192, n_heads=2, d_head=96,
+                               seg_len=192, n_context=960, act_dtype="f32", lr=2.0,
+                               optimizer="paper", prep_segments=2)
+    p = SwProblem(cfg)
+    p.segments(0, 5)                 # 2 + 2 + 1
+    _check(p, [0], 1e-4, 1e-4)
+
+
+def test_segments_paper_shape_bf16():
+    cfg = configs.SW_PAPER.with_(optimizer="paper")
+    p = SwProblem(cfg)
+    p.segments(0, 6)                 # 4 + 2
+    _check(p, [0, cfg.n_layers - 1], 2e-2, 1e-2)
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_segments_bitwise_equal_to_one_call_per_segment(act):
+    # the batch computes every token's preprocessing with the same arithmetic as one segment
+    cfg = configs.SW_TINY.with_(name=f"sw_tiny_{act}", act_dtype=act, optimizer="paper")
+    a, b = SwProblem(cfg), SwProblem(cfg)
+    a.segments(0, 6)
+    for s in range(6):
+        b.segment(s, cfg.seg_len)
+    torch.cuda.synchronize()
+    for m in range(3):
+        assert torch.equal(a.w[m], b.w[m]) and torch.equal(a.mom[m], b.mom[m]), m
+    assert np.array_equal(a.sess.loss(), b.sess.loss())
