@@ -387,7 +387,9 @@ __global__ __launch_bounds__(256) void sw_keys_kernel(const E* __restrict__ kpre
                                                       E* __restrict__ kh, E* __restrict__ kt,
                                                       int seg_rows, int kpre_rows,
                                                       long long kh_ss, long long kt_ss) {
-  __shared__ float tile[64][257];  // [token][channel]
+  // [token][channel] in the output dtype (the values K^T stores), odd row stride in 32-bit words
+  constexpr int TS = sizeof(E) == 2 ? 258 : 257;
+  __shared__ E tile[64][TS];
   // several consecutive segments: block x covers tokens j0.. of segment sg (seg_rows a multiple
   // of 64); K' rows sg * Tp + j of kpre_rows per layer, and segment sg's copies of K and K^T
   const int gx = blockIdx.x * 64, sg = gx / seg_rows, j0 = gx - sg * seg_rows;
@@ -400,10 +402,22 @@ __global__ __launch_bounds__(256) void sw_keys_kernel(const E* __restrict__ kpre
   const int nv = dh / 8, hv = dh / 16, half = dh / 2, c = 8 * li;
   const bool act = li < nv, lo = li < hv;
   const int src = (lane & 32) + (act ? (lo ? li + hv : li - hv) : li);
-  for (int t = 2 * wave + hw; t < 64; t += 8) {
-    const int j = j0 + t;
-    float x[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
-    if (act) load8(kl + (long long)j * d + (long long)e * dh + c, x);
+  // the 8 tokens of this half-wave: all loads issued first, then the arithmetic
+  constexpr int IT = 8;
+  float xs[IT][8];
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    if (act) {
+      load8(kl + (long long)(j0 + 2 * wave + hw + 8 * it) * d + (long long)e * dh + c, xs[it]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) xs[it][i] = 0.0f;
+    }
+  }
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int t = 2 * wave + hw + 8 * it, j = j0 + t;
+    const float (&x)[8] = xs[it];
     float ss = 0.0f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) ss += x[i] * x[i];
@@ -427,7 +441,7 @@ __global__ __launch_bounds__(256) void sw_keys_kernel(const E* __restrict__ kpre
                            : y[2 * i + 1] * s1 + x[2 * i + 1] * c1) * inv;
       }
 #pragma unroll
-      for (int i = 0; i < 8; ++i) tile[t][c + i] = o[i];
+      for (int i = 0; i < 8; ++i) tile[t][c + i] = from_f32<E>(o[i]);
     }
     if (c < dhp) store8(kh + ((long long)b * Tp + j) * dhp + c, o);
   }
@@ -437,7 +451,7 @@ __global__ __launch_bounds__(256) void sw_keys_kernel(const E* __restrict__ kpre
     const int ch = i >> 3, t0 = (i & 7) * 8;
     float v[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = tile[t0 + k][ch];
+    for (int k = 0; k < 8; ++k) v[k] = to_f32(tile[t0 + k][ch]);
     store8(kt + ((long long)b * dh + ch) * Tp + j0 + t0, v);
   }
 }
