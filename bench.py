@@ -394,7 +394,7 @@ def run_swiglu(args):
     lstride = ctx.stride(0)
     # segments per preprocessing batch, as the library's header states the default
     prep = 1 if args.call == "segment" else (
-        cfg.prep_segments if cfg.prep_segments > 0 else (4 if T % 64 == 0 else 1))
+        cfg.prep_segments if cfg.prep_segments > 0 else (8 if T % 64 == 0 else 1))
 
     def step():
         if args.call == "segments":

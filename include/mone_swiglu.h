@@ -50,9 +50,10 @@ typedef struct {
   float rope_base;   /* RoPE base (> 0; the usual value is 10000) */
   int32_t prep_segments; /* segments whose weight-independent preprocessing (rates, projections,
                             key normalisation and RoPE) mone_swiglu_segments computes in one
-                            batch, in [0, 16]: 0 chooses 4 when seg_len is a multiple of 64
+                            batch, in [0, 16]: 0 chooses 8 when seg_len is a multiple of 64
                             (else 1); above 1 needs seg_len a multiple of 64.  The workspace
-                            holds that many copies of the preprocessing buffers. */
+                            holds that many copies of the preprocessing buffers, and above 1
+                            two sets of the copies the memory steps read. */
 } mone_swiglu_config;
 
 /* Frozen parameters (borrowed for the handle's lifetime, read only). */
@@ -121,7 +122,12 @@ int mone_swiglu_segment(mone_swiglu* h, const void* x, int32_t n_tokens, void* s
  * The preprocessing that does not depend on the fast weights (the paper optimiser's rates and
  * decay, the key/value projections with their affine step and SiLU, the keys' normalisation
  * and segment-local RoPE) runs once for up to prep_segments segments at a time, as larger
- * launches; each segment's memory step (DA, FWD, UPD) then follows in order. */
+ * launches; each segment's memory step (DA, FWD, UPD) then follows in order.  With more than
+ * one such batch, the preprocessing of the next batch runs on an internal stream of the handle
+ * (default priority) beside the memory steps of the current one; the internal stream starts
+ * after the work queued on `stream` before the call and `stream` waits for it before the call's
+ * end, so the call orders like one stream and can be captured in a HIP graph.  Calls on one
+ * handle must not overlap. */
 int mone_swiglu_segments(mone_swiglu* h, const void* x, int64_t layer_stride, int32_t n_segments,
                          void* stream);
 

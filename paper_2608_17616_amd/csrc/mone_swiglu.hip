@@ -52,8 +52,11 @@ struct SwLayout {
   int Tp, dhp, parts_max;
   // G copies of the weight-independent preprocessing outputs (K, K^T, dY0, dY^T, the rates and
   // the decay), so that mone_swiglu_segments can compute them for G segments in one batch;
-  // their element strides between copies
-  int G;
+  // their element strides between copies.  With G > 1 there are two sets of G copies: one
+  // batch's preprocessing fills one set while the segments of the batch before it read the
+  // other (the raw keys and the rates' partial sums, used only inside the preprocessing, keep
+  // one set).
+  int G, sets;
   long long kh_ss, kt_ss, dy_ss, dyt_ss, rate_ss, vpart_ss, beta_ss;
   size_t kpre, kh, kt, dy, dyt, dat, at, dzgt, wig, woc, rope, gate, loss_part, loss_out;
   size_t rate, vpart, beta, n_ig, n_out;  // paper optimiser
@@ -62,11 +65,11 @@ struct SwLayout {
 
 constexpr int kMaxPrepSegments = 16;
 
-// Segments per preprocessing batch: cfg->prep_segments, or by default 4 when segments are a
+// Segments per preprocessing batch: cfg->prep_segments, or by default 8 when segments are a
 // multiple of 64 tokens (1 otherwise: the batch maps GEMM rows to segments in 64-row steps).
 int prep_segments(const mone_swiglu_config* c) {
   if (c->prep_segments > 0) return c->prep_segments;
-  return c->seg_len % 64 == 0 ? 4 : 1;
+  return c->seg_len % 64 == 0 ? 8 : 1;
 }
 
 int check_sw_config(const mone_swiglu_config* c) {
@@ -119,17 +122,19 @@ SwLayout make_sw_layout(const mone_swiglu_config* c) {
     return o;
   };
   const size_t G = (size_t)prep_segments(c);
+  const size_t NS = G > 1 ? 2 : 1;
   L.G = (int)G;
+  L.sets = (int)NS;
   L.kh_ss = L.dy_ss = (long long)(B * Tp * dhp);
   L.kt_ss = L.dyt_ss = (long long)(B * dh * Tp);
   L.rate_ss = (long long)(nl * Tp);
   L.vpart_ss = (long long)(nl * (Tp / kRateTokens));
   L.beta_ss = (long long)nl;
   L.kpre = take(nl * G * Tp * d * E);
-  L.kh = take(G * B * Tp * dhp * E);
-  L.kt = take(G * B * dh * Tp * E);
-  L.dy = take(G * B * Tp * dhp * E);
-  L.dyt = take(G * B * dh * Tp * E);
+  L.kh = take(NS * G * B * Tp * dhp * E);
+  L.kt = take(NS * G * B * dh * Tp * E);
+  L.dy = take(NS * G * B * Tp * dhp * E);
+  L.dyt = take(NS * G * B * dh * Tp * E);
   L.dat = take(B * dh * Tp * E);
   L.at = take(B * dh * Tp * E);
   L.dzgt = take(B * 2 * dh * Tp * E);
@@ -140,9 +145,9 @@ SwLayout make_sw_layout(const mone_swiglu_config* c) {
   L.loss_part = take(B * (size_t)L.parts_max * 4);
   L.loss_out = take(nl * 4);
   if (c->optimizer == MONE_OPT_PAPER) {
-    L.rate = take(G * nl * Tp * 4);
+    L.rate = take(NS * G * nl * Tp * 4);
     L.vpart = take(G * nl * (Tp / kRateTokens) * 4);
-    L.beta = take(G * nl * 4);
+    L.beta = take(NS * G * nl * 4);
     L.n_ig = take(B * 2 * dh * 4);
     L.n_out = take(B * dh * 4);
   }
@@ -172,6 +177,10 @@ struct mone_swiglu {
   int last_n;      // tokens of the last non-empty segment (0: none yet)
   int last_parts;  // loss partials per head written by that segment
   StageTimer timer;
+  // With two sets of preprocessing copies: the internal stream that runs the preprocessing of
+  // a multi-segment call beside its memory steps (default priority), and its events
+  hipStream_t side;
+  hipEvent_t ev_fork, ev_join, ev_prep[2], ev_chain[2];
 
   template <typename T>
   T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
@@ -180,11 +189,12 @@ struct mone_swiglu {
 namespace {
 
 // Weight-independent preprocessing of g consecutive segments of n tokens each (g > 1: whole
-// segments of seg_len tokens, seg_len a multiple of 64), into copies 0 .. g-1: RATE (paper
+// segments of seg_len tokens, seg_len a multiple of 64), into copies c0 .. c0+g-1: RATE (paper
 // optimiser), PROJ and KEYS, each one launch over all g segments.  x [L][g*n][d], layer
 // stride lsx.
 template <typename E, bool PAPER>
-int run_sw_prep(mone_swiglu* H, const void* x, long long lsx, int n, int g, hipStream_t s) {
+int run_sw_prep(mone_swiglu* H, const void* x, long long lsx, int n, int g, int c0,
+                hipStream_t s) {
   const mone_swiglu_config& c = H->cfg;
   const SwLayout& Ly = H->lay;
   const int L = c.n_layers, d = c.d_model, NH = c.n_heads, dh = c.d_head;
@@ -192,7 +202,7 @@ int run_sw_prep(mone_swiglu* H, const void* x, long long lsx, int n, int g, hipS
   // rows of a segment in the batched launches; one segment keeps its padded extent
   const int seg_rows = g > 1 ? n : Tp, kpre_rows = Ly.G * Tp;
   const int nz = g > 1 ? g * n : (int)round_up(n, 64);  // token rows KEYS writes
-  float* rate = PAPER ? H->at<float>(Ly.rate) : nullptr;
+  float* rate = PAPER ? H->at<float>(Ly.rate) + c0 * Ly.rate_ss : nullptr;
   hipError_t e;
 
   if constexpr (PAPER) {
@@ -202,7 +212,8 @@ int run_sw_prep(mone_swiglu* H, const void* x, long long lsx, int n, int g, hipS
         c.lr, rate, Tp, H->at<float>(Ly.vpart), (long long)n * d, Ly.rate_ss, Ly.vpart_ss);
     decay_kernel<<<dim3((L + 63) / 64, g), dim3(64), 0, s>>>(H->at<float>(Ly.vpart),
                                                              Tp / kRateTokens, n,
-                                                             H->opt.decay_b, H->at<float>(Ly.beta),
+                                                             H->opt.decay_b,
+                                                             H->at<float>(Ly.beta) + c0 * Ly.beta_ss,
                                                              L);
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch RATE");
     H->timer.end(MONE_SW_STAGE_RATE, s);
@@ -219,7 +230,9 @@ int run_sw_prep(mone_swiglu* H, const void* x, long long lsx, int n, int g, hipS
     sp.m_store = g > 1 ? g * n : -1;
     sp.n_store = 2 * d;
     EpiSwProj<E> epi;
-    epi.kpre = H->at<E>(Ly.kpre); epi.dy = H->at<E>(Ly.dy); epi.dyt = H->at<E>(Ly.dyt);
+    epi.kpre = H->at<E>(Ly.kpre);
+    epi.dy = H->at<E>(Ly.dy) + c0 * Ly.dy_ss;
+    epi.dyt = H->at<E>(Ly.dyt) + c0 * Ly.dyt_ss;
     epi.kscale = H->fz.k_scale; epi.kshift = H->fz.k_shift; epi.rate = rate;
     epi.lr = c.lr; epi.inv_n = 1.0f / (float)n;
     epi.d = d; epi.dh = dh; epi.dhp = dhp; epi.H = NH; epi.Tp = Tp; epi.n = n;
@@ -237,8 +250,9 @@ int run_sw_prep(mone_swiglu* H, const void* x, long long lsx, int n, int g, hipS
   {
     H->timer.begin(MONE_SW_STAGE_KEYS, s);
     sw_keys_kernel<E><<<dim3(nz / 64, NH, L), dim3(256), 0, s>>>(
-        H->at<E>(Ly.kpre), d, NH, dh, dhp, Tp, H->at<float2>(Ly.rope), H->at<E>(Ly.kh),
-        H->at<E>(Ly.kt), seg_rows, kpre_rows, Ly.kh_ss, Ly.kt_ss);
+        H->at<E>(Ly.kpre), d, NH, dh, dhp, Tp, H->at<float2>(Ly.rope),
+        H->at<E>(Ly.kh) + c0 * Ly.kh_ss, H->at<E>(Ly.kt) + c0 * Ly.kt_ss, seg_rows, kpre_rows,
+        Ly.kh_ss, Ly.kt_ss);
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch KEYS");
     H->timer.end(MONE_SW_STAGE_KEYS, s);
   }
@@ -355,25 +369,72 @@ int run_sw_update(mone_swiglu* H, int n, int cp, hipStream_t s) {
 // stride lsx.
 template <typename E, bool PAPER>
 int run_sw_segment(mone_swiglu* H, const void* x, long long lsx, int n, hipStream_t s) {
-  const int rc = run_sw_prep<E, PAPER>(H, x, lsx, n, 1, s);
+  const int rc = run_sw_prep<E, PAPER>(H, x, lsx, n, 1, 0, s);
   return rc != MONE_OK ? rc : run_sw_update<E, PAPER>(H, n, 0, s);
 }
 
 // S whole segments from x [L][S*T][d] (layer stride lsx): preprocessing in batches of up to G
-// segments, then each segment's update in order.
+// segments, then each segment's update in order.  With two or more batches the preprocessing
+// runs on the handle's internal stream, one batch ahead, into alternating sets of copies: batch
+// k+1's preprocessing (which reads only x and the frozen parameters) overlaps batch k's memory
+// steps on `s`.  Batch k's steps wait for its preprocessing; batch k+2's preprocessing waits for
+// batch k's steps (the last readers of that set); the internal stream starts after the work
+// queued on `s` before the call and `s` waits for it at the end, so the call keeps the ordering
+// of a single stream (and can be captured in a graph).
 template <typename E, bool PAPER>
 int run_sw_segments(mone_swiglu* H, const void* x, long long lsx, int S, hipStream_t s) {
   const int T = H->cfg.seg_len, G = H->lay.G;
   const long long d = H->cfg.d_model;
-  for (int done = 0; done < S;) {
-    const int g = S - done < G ? S - done : G;
-    const E* xs = reinterpret_cast<const E*>(x) + (long long)done * T * d;
-    int rc = run_sw_prep<E, PAPER>(H, xs, lsx, T, g, s);
-    for (int cp = 0; cp < g && rc == MONE_OK; ++cp) rc = run_sw_update<E, PAPER>(H, T, cp, s);
-    if (rc != MONE_OK) return rc;
-    done += g;
+  const int nb = (S + G - 1) / G;
+  auto xs = [&](int b) { return reinterpret_cast<const E*>(x) + (long long)b * G * T * d; };
+  auto gsz = [&](int b) { return S - b * G < G ? S - b * G : G; };
+  auto steps = [&](int b, int c0) {
+    int rc = MONE_OK;
+    for (int cp = 0; cp < gsz(b) && rc == MONE_OK; ++cp)
+      rc = run_sw_update<E, PAPER>(H, T, c0 + cp, s);
+    return rc;
+  };
+  if (nb < 2 || H->lay.sets < 2) {
+    for (int b = 0; b < nb; ++b) {
+      int rc = run_sw_prep<E, PAPER>(H, xs(b), lsx, T, gsz(b), 0, s);
+      if (rc == MONE_OK) rc = steps(b, 0);
+      if (rc != MONE_OK) return rc;
+    }
+    return MONE_OK;
   }
-  return MONE_OK;
+  hipStream_t q = H->side;
+  hipError_t e = hipEventRecord(H->ev_fork, s);
+  if (e == hipSuccess) e = hipStreamWaitEvent(q, H->ev_fork, 0);
+  if (e != hipSuccess) return hip_fail(e, "fork the preprocessing stream");
+  auto prep = [&](int b) {
+    int rc = run_sw_prep<E, PAPER>(H, xs(b), lsx, T, gsz(b), (b & 1) * G, q);
+    if (rc != MONE_OK) return rc;
+    const hipError_t er = hipEventRecord(H->ev_prep[b & 1], q);
+    return er == hipSuccess ? MONE_OK : hip_fail(er, "record the preprocessing event");
+  };
+  int rc = prep(0);
+  for (int b = 0; b < nb && rc == MONE_OK; ++b) {
+    if (b + 1 < nb) {
+      // set (b+1)&1 was last read by batch b-1's steps
+      if (b >= 1 && (e = hipStreamWaitEvent(q, H->ev_chain[(b + 1) & 1], 0)) != hipSuccess) {
+        rc = hip_fail(e, "wait for the steps");
+        break;
+      }
+      if ((rc = prep(b + 1)) != MONE_OK) break;
+    }
+    if ((e = hipStreamWaitEvent(s, H->ev_prep[b & 1], 0)) != hipSuccess) {
+      rc = hip_fail(e, "wait for the preprocessing");
+      break;
+    }
+    if ((rc = steps(b, (b & 1) * G)) != MONE_OK) break;
+    if ((e = hipEventRecord(H->ev_chain[b & 1], s)) != hipSuccess)
+      rc = hip_fail(e, "record the steps event");
+  }
+  // join, also after an error, so that no work of the call is left outside `s`
+  e = hipEventRecord(H->ev_join, q);
+  if (e == hipSuccess) e = hipStreamWaitEvent(s, H->ev_join, 0);
+  if (rc == MONE_OK && e != hipSuccess) rc = hip_fail(e, "join the preprocessing stream");
+  return rc;
 }
 
 template <typename E>
@@ -480,6 +541,22 @@ int run_sw_read(mone_swiglu* H, const mone_swiglu_reader* rd, const void* xq, in
   return MONE_OK;
 }
 
+// The internal stream and events (those created so far); the stream is drained first.
+void release_side(mone_swiglu* H) {
+  if (H->side) {
+    (void)hipStreamSynchronize(H->side);
+    (void)hipStreamDestroy(H->side);
+    H->side = nullptr;
+  }
+  hipEvent_t* evs[6] = {&H->ev_fork, &H->ev_join, &H->ev_prep[0], &H->ev_prep[1],
+                        &H->ev_chain[0], &H->ev_chain[1]};
+  for (hipEvent_t* ev : evs)
+    if (*ev) {
+      (void)hipEventDestroy(*ev);
+      *ev = nullptr;
+    }
+}
+
 template <typename E>
 hipError_t build_copies(mone_swiglu* H, hipStream_t s) {
   const mone_swiglu_config& c = H->cfg;
@@ -566,6 +643,18 @@ int mone_swiglu_init(mone_swiglu** out, const mone_swiglu_config* cfg,
   if (e != hipSuccess) {
     delete H;
     return hip_fail(e, "building the handle's copies");
+  }
+  if (Ly.sets > 1) {
+    e = hipStreamCreateWithFlags(&H->side, hipStreamNonBlocking);
+    hipEvent_t* evs[6] = {&H->ev_fork, &H->ev_join, &H->ev_prep[0], &H->ev_prep[1],
+                          &H->ev_chain[0], &H->ev_chain[1]};
+    for (int i = 0; i < 6 && e == hipSuccess; ++i)
+      e = hipEventCreateWithFlags(evs[i], hipEventDisableTiming);
+    if (e != hipSuccess) {
+      release_side(H);
+      delete H;
+      return hip_fail(e, "creating the preprocessing stream and its events");
+    }
   }
   *out = H;
   return MONE_OK;
@@ -680,6 +769,7 @@ int mone_swiglu_destroy(mone_swiglu* H) {
   g_err[0] = 0;
   if (!H) return MONE_OK;
   H->timer.destroy();
+  release_side(H);
   delete H;
   return MONE_OK;
 }

@@ -149,3 +149,33 @@ def test_paper_form_segment_replays_bitwise(cfg):
     assert np.array_equal(pg.sess.loss(), pe.sess.loss())
     pg.sess.close()
     pe.sess.close()
+
+
+def test_paper_form_multi_batch_call_replays_bitwise():
+    # one mone_swiglu_segments call of 6 segments in batches of 2: the preprocessing runs on the
+    # handle's internal stream, forked from and joined to the captured stream
+    cfg = configs.SW_TINY.with_(name="graph_sw_multi", optimizer="paper", prep_segments=2)
+    print(f"[graph] paper form multi-batch call {cfg.name}", flush=True)
+    pe, pg = _sw_session(cfg), _sw_session(cfg)
+    L, T, S = cfg.n_layers, cfg.seg_len, 6
+    act = torch.bfloat16 if cfg.act_dtype == "bf16" else torch.float32
+    xg = torch.empty(L, S * T, cfg.d_model, dtype=act, device="cuda")
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        pg.sess.segments(xg)
+    torch.cuda.synchronize()
+    for m in range(3):
+        assert torch.equal(pg.w[m], pg.w0[m])  # capture ran nothing
+    for r in range(3):
+        x = pe.segments(r * S, S)
+        xg.copy_(x)
+        g.replay()
+        torch.cuda.synchronize()
+        for m in range(3):
+            assert torch.equal(pg.w[m], pe.w[m]), f"replay {r}, matrix {m}"
+            assert torch.equal(pg.mom[m], pe.mom[m]), f"replay {r}, momentum {m}"
+        assert np.array_equal(pg.sess.loss(), pe.sess.loss())
+        float(sum(w.abs().sum() for w in pg.w).item())  # eager work between replays
+    pg.sess.close()
+    pe.sess.close()

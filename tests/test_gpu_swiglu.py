@@ -379,10 +379,10 @@ def test_full_context_paper_shape_last_step():
 
 @pytest.mark.parametrize("optimizer", ["sgd", "paper"])
 def test_segments_tiny_f32(optimizer):
-    # 7 segments: a batch of 4 (the default) and one of 3
+    # 11 segments: a batch of 8 (the default) and one of 3
     cfg = configs.SW_TINY.with_(optimizer=optimizer)
     p = SwProblem(cfg)
-    p.segments(0, 7)
+    p.segments(0, 11)
     _check(p, range(cfg.n_layers), 1e-4, 1e-4)
 
 
@@ -408,7 +408,7 @@ def test_segments_odd_head_width_f32():
 def test_segments_paper_shape_bf16():
     cfg = configs.SW_PAPER.with_(optimizer="paper")
     p = SwProblem(cfg)
-    p.segments(0, 6)                 # 4 + 2
+    p.segments(0, 10)                # 8 + 2
     _check(p, [0, cfg.n_layers - 1], 2e-2, 1e-2)
 
 
@@ -424,3 +424,27 @@ def test_segments_bitwise_equal_to_one_call_per_segment(act):
     for m in range(3):
         assert torch.equal(a.w[m], b.w[m]) and torch.equal(a.mom[m], b.mom[m]), m
     assert np.array_equal(a.sess.loss(), b.sess.loss())
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_segments_overlapped_batches_bitwise(act):
+    # 11 segments in batches of 2: six batches, whose preprocessing runs on the handle's own
+    # stream one batch ahead and alternates between two sets of copies; every set is reused
+    # while later segments are still queued, so a missing wait would change the result
+    cfg = configs.SW_TINY.with_(name=f"sw_tiny_ov_{act}", act_dtype=act, optimizer="paper",
+                                prep_segments=2)
+    a, b = SwProblem(cfg), SwProblem(cfg)
+    a.segments(0, 11)
+    for s in range(11):
+        b.segment(s, cfg.seg_len)
+    torch.cuda.synchronize()
+    for m in range(3):
+        assert torch.equal(a.w[m], b.w[m]) and torch.equal(a.mom[m], b.mom[m]), m
+    assert np.array_equal(a.sess.loss(), b.sess.loss())
+    a.segments(11, 3)                # a second call on the same handle: 2 + 1
+    for s in range(11, 14):
+        b.segment(s, cfg.seg_len)
+    torch.cuda.synchronize()
+    for m in range(3):
+        assert torch.equal(a.w[m], b.w[m]) and torch.equal(a.mom[m], b.mom[m]), m
+    _check(a, range(cfg.n_layers), 1e-4 if act == "f32" else 2e-2, 1e-4 if act == "f32" else 1e-2)
