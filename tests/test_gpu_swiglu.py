@@ -373,6 +373,52 @@ def test_full_context_paper_shape_last_step():
         assert np.max(np.abs(n_end - n_0) / n_0) < 1e-4
 
 
+
+def test_full_context_one_multi_segment_call():
+    """The benchmark's call at the paper's shape: the whole 128K-token context (256 segments)
+    through one mone_swiglu_segments call, 32 batches whose preprocessing runs beside the memory
+    steps, bitwise equal to one call per segment on the same inputs; the last of those steps
+    against the oracle's step from the GPU's own state before it (first and last layers)."""
+    cfg = configs.SW_PAPER.with_(optimizer="paper")
+    L, T, d, H, S = cfg.n_layers, cfg.seg_len, cfg.d_model, cfg.n_heads, cfg.n_segments
+    a, b = SwProblem(cfg), SwProblem(cfg)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(11)
+    ctx = inputs.device_normal_(torch.empty(L, S * T, d, dtype=a.act, device="cuda"), 1.0, gen)
+    checked = [0, L - 1]
+    xh = {}
+    for l in checked:  # the last segment of the checked layers from the host generator
+        xh[l] = inputs.segment_x(cfg, l, S - 1)
+        ctx[l, (S - 1) * T:].copy_(torch.from_numpy(xh[l]))
+    print(f"[swiglu] one call of {S} segments", flush=True)
+    a.sess.segments(ctx)
+    for s in range(S - 1):
+        b.sess.segment(ctx[:, s * T:(s + 1) * T].contiguous(), T)
+    torch.cuda.synchronize()
+    snap_w = [w.cpu().numpy().astype(np.float64) for w in b.w]
+    snap_m = [m.cpu().numpy().astype(np.float64) for m in b.mom]
+    b.sess.segment(ctx[:, (S - 1) * T:].contiguous(), T)
+    torch.cuda.synchronize()
+    for m in range(3):
+        assert torch.equal(a.w[m], b.w[m]) and torch.equal(a.mom[m], b.mom[m]), m
+        assert bool(torch.isfinite(a.w[m]).all())
+    assert np.array_equal(a.sess.loss(), b.sess.loss())
+    got_w = [w.cpu().numpy().astype(np.float64) for w in a.w]
+    got_m = [m.cpu().numpy().astype(np.float64) for m in a.mom]
+    w0 = [w.cpu().numpy().astype(np.float64) for w in a.w0]
+    errs = {}
+    for l in checked:
+        fast = tuple(w[l] for w in snap_w)
+        mom = tuple(m[l] for m in snap_m)
+        norms0 = sw.initial_norms(tuple(w[l] for w in w0))
+        new, new_m, _, _ = sw.paper_step(xh[l].astype(np.float64), fast, mom, a.frozen(l),
+                                         a.meta[l], norms0, cfg.lr, H, cfg.rope_base)
+        for k, name in enumerate(("w_in", "w_gate", "w_out")):
+            errs[f"d{name}[{l}]"] = rel_l2(got_w[k][l] - fast[k], new[k] - fast[k])
+            errs[f"mom_{name}[{l}]"] = rel_l2(got_m[k][l], new_m[k])
+    print("max errors:", {k: f"{v:.2e}" for k, v in sorted(errs.items(), key=lambda t: -t[1])[:4]})
+    assert max(errs.values()) < 2e-2, errs
+
 # ------------------------------------------------------------------------------------------
 # Several segments per call (mone_swiglu_segments): the weight-independent preprocessing of up
 # to prep_segments segments runs as one batch; each segment's memory step follows in order.
