@@ -105,6 +105,43 @@ __device__ __forceinline__ void load8(const bf16_t* p, float (&v)[8]) {
   }
 }
 
+// Split row chunks.  Lane q (0..7) of the 8 lanes covering a 64-column row segment holds
+// columns 4q..4q+3 (v[0..3]) and 32+4q..32+4q+3 (v[4..7]); p points at column 4q.  Each 16-byte
+// fp32 access instruction then covers 128 contiguous bytes across the 8 lanes: a non-temporal
+// store of two 16-byte halves per lane 32 bytes apart (the unsplit chunk) leaves every line
+// half written by each instruction, and measured 2.1 TB/s on its own against 5.4 TB/s.
+__device__ __forceinline__ void load8_split(const float* p, float (&v)[8]) {
+  const f32x4v a = __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(p));
+  const f32x4v b = __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(p + 32));
+  v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
+  v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
+}
+__device__ __forceinline__ void store8_split(float* p, const float (&v)[8]) {
+  f32x4v a, b;
+  a[0] = v[0]; a[1] = v[1]; a[2] = v[2]; a[3] = v[3];
+  b[0] = v[4]; b[1] = v[5]; b[2] = v[6]; b[3] = v[7];
+  __builtin_nontemporal_store(a, reinterpret_cast<f32x4v*>(p));
+  __builtin_nontemporal_store(b, reinterpret_cast<f32x4v*>(p + 32));
+}
+// bf16: lanes 2m and 2m+1 exchange halves (a DPP move within each pair of lanes), then lane 2m
+// stores columns 8m..8m+7 and lane 2m+1 columns 32+8m..32+8m+7, 16 bytes each.  Both lanes of a
+// pair must execute this together (they always share a row, hence its bounds checks).
+__device__ __forceinline__ void store8_split(bf16_t* p, const float (&v)[8]) {
+  const uint32_t a0 = pack_bf16(v[0], v[1]), a1 = pack_bf16(v[2], v[3]);
+  const uint32_t b0 = pack_bf16(v[4], v[5]), b1 = pack_bf16(v[6], v[7]);
+  const bool odd = (__lane_id() & 1) != 0;
+  // the half the partner keeps: the even lane sends columns 32+, the odd lane columns 0..3
+  constexpr int kSwapPairs = 0xB1;  // quad_perm [1, 0, 3, 2]
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_mov_dpp((int)(odd ? a0 : b0), kSwapPairs, 0xF,
+                                                         0xF, false);
+  const uint32_t r1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)(odd ? a1 : b1), kSwapPairs, 0xF,
+                                                         0xF, false);
+  u32x4 w;
+  if (odd) { w[0] = r0; w[1] = r1; w[2] = b0; w[3] = b1; }
+  else { w[0] = a0; w[1] = a1; w[2] = r0; w[3] = r1; }
+  __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(odd ? p + 28 : p));
+}
+
 // Logistic function with the hardware exponential and reciprocal (about 1 ulp each; an IEEE
 // division would cost ten instructions per element in the epilogues).
 __device__ __forceinline__ float sigmoidf_(float z) {
@@ -614,13 +651,21 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
                 "paired rows: row pass only");
   static_assert(!Epi::kRowScale || (Epi::kWriteback && !Epi::kRowNorm && !Epi::kCols),
                 "row scale: row pass with write-back, then the scale pass");
+  static_assert(!Epi::kSplitCols || (!Epi::kPairRows && !Epi::kRowScale),
+                "split row chunks: plain row pass");
   float aux[2][NCH][NAUX];
   const int rl = lane >> 3, ql = lane & 7;      // row-chunk lane coordinates
+  // Split row chunks (split_cols(pi)): lane ql's chunk is columns 4ql..4ql+3 and
+  // 32+4ql..32+4ql+3 of its 64-column row segment, passed as the chunk's first column (the
+  // problem's N is then a multiple of 64, so a segment is stored whole or not at all).
+  const bool split = Epi::kSplitCols && G.epi.split_cols(pi);
+  const int cq = split ? 4 * ql : 8 * ql;        // first column of this lane's chunks
+  const int cq2 = split ? 4 * ql + 32 : 8 * ql + 4;  // first column of their second half
   auto issue_pre = [&](int sb, float (&ax)[NCH][NAUX]) {
     const int grow = m0 + wm * WM + (sb / NSN) * SB, gcol = n0 + wn * WN + (sb % NSN) * SB;
 #pragma unroll
     for (int b = 0; b < NCH; ++b) {
-      const int row = grow + RS * (rl + 8 * b), col = gcol + 8 * ql;
+      const int row = grow + RS * (rl + 8 * b), col = gcol + cq;
       if (row + RS - 1 < P.M && col < P.N) G.epi.pre8(pi, layer, row, col, P.M, P.N, ax[b]);
     }
   };
@@ -646,9 +691,9 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     }
 #pragma unroll
     for (int b = 0; b < NCH; ++b) {
-      const int r = RS * (rl + 8 * b), c = 8 * ql;
+      const int r = RS * (rl + 8 * b), c = cq;
       float* s0 = stw + sidx(r, c);
-      float* s1 = stw + sidx(r, c + 4);
+      float* s1 = stw + sidx(r, cq2);
       float v[8];
       const float4 x0 = *reinterpret_cast<const float4*>(s0);
       const float4 x1 = *reinterpret_cast<const float4*>(s1);
@@ -659,7 +704,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       if constexpr (Epi::kPairRows) {
         // the partner row r + 1 (r is even: sub-blocks start at even rows)
         const float4 y0 = *reinterpret_cast<const float4*>(stw + sidx(r + 1, c));
-        const float4 y1 = *reinterpret_cast<const float4*>(stw + sidx(r + 1, c + 4));
+        const float4 y1 = *reinterpret_cast<const float4*>(stw + sidx(r + 1, cq2));
         const float w[8] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
         if (ok) val = G.epi.rows8p(pi, layer, grow + r, gcol + c, P.M, P.N, v, w, aux[sb & 1][b]);
         partial += val;
@@ -749,6 +794,10 @@ struct EpiBase {
   static constexpr bool kCols = false;
   static constexpr bool kWriteback = false;
   __device__ __forceinline__ bool has_cols(int) const { return false; }
+  // pre8/rows8 of problem pi take split row chunks (columns c..c+3 and c+32..c+35; N a multiple
+  // of 64): the fp32 read-modify-write epilogues, whose 16-byte accesses then coalesce
+  static constexpr bool kSplitCols = false;
+  __device__ __forceinline__ bool split_cols(int) const { return false; }
   __device__ __forceinline__ void pre8(int, int, int, int, int, int, float (&)[8]) const {}
   __device__ __forceinline__ void cols8(int, int, int, int, int, int, const float (&)[8]) const {}
   __device__ __forceinline__ void finish(int, int, int, int, int, float) const {}
@@ -886,6 +935,8 @@ struct EpiBwdW2 : EpiBase {
   int parts_per_layer;
   int nip;
   __device__ __forceinline__ bool has_cols(int pi) const { return !PAPER && pi == 1; }
+  static constexpr bool kSplitCols = true;  // problem 1: split row chunks (h is a multiple of 64)
+  __device__ __forceinline__ bool split_cols(int pi) const { return pi == 1; }
   __device__ __forceinline__ void pre8(int pi, int layer, int row, int col, int, int,
                                        float (&x)[kAux]) const {
     float (&x0)[8] = *reinterpret_cast<float(*)[8]>(&x[0]);
@@ -893,7 +944,7 @@ struct EpiBwdW2 : EpiBase {
       load8(dst + (long long)layer * lst + (long long)row * Tp + col, x0);
     } else {
       const long long o = (long long)layer * ls2 + (long long)row * h + col;
-      load8(w2 + o, x0);
+      load8_split(w2 + o, x0);
     }
   }
   __device__ __forceinline__ float rows8(int pi, int layer, int row, int col, int, int,
@@ -909,15 +960,15 @@ struct EpiBwdW2 : EpiBase {
     if constexpr (PAPER) {
       const float b = beta[layer];
       float m[8], nw[8], ss = 0.0f;
-      load8(mom2 + o, m);
+      load8_split(mom2 + o, m);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         m[e] = b * m[e] + v[e];
         nw[e] = x[e] - m[e];
         ss += nw[e] * nw[e];
       }
-      store8(mom2 + o, m);
-      store8(w2 + o, nw);
+      store8_split(mom2 + o, m);
+      store8_split(w2 + o, nw);
       return ss;
     } else {
       float nw[8], cp[8], ip = 0.0f;
@@ -927,8 +978,8 @@ struct EpiBwdW2 : EpiBase {
         nw[e] = x[e] - lr * v[e];
         cp[e] = -nw[e];
       }
-      store8(w2 + o, nw);
-      store8(w2n + o, cp);
+      store8_split(w2 + o, nw);
+      store8_split(w2n + o, cp);
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = nw[e];
       return nip ? ip : 0.0f;
@@ -968,10 +1019,12 @@ struct EpiW1 : EpiBase {
   const float* beta;   // PAPER: [L]
   float* ss1;          // PAPER: [L][h][d/64] row-segment sums of squares
   int h;
+  static constexpr bool kSplitCols = true;  // split row chunks (d is a multiple of 64)
+  __device__ __forceinline__ bool split_cols(int) const { return true; }
   __device__ __forceinline__ void pre8(int, int layer, int row, int col, int, int,
                                        float (&w)[kAux]) const {
     const long long o = (long long)layer * ls1 + (long long)row * d + col;
-    load8(w1 + o, w);
+    load8_split(w1 + o, w);
   }
   __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
                                          float (&v)[8], const float (&w)[kAux]) const {
@@ -979,22 +1032,22 @@ struct EpiW1 : EpiBase {
     if constexpr (PAPER) {
       const float b = beta[layer];
       float m[8], nw[8], ss = 0.0f;
-      load8(mom1 + o, m);
+      load8_split(mom1 + o, m);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         m[e] = b * m[e] + v[e];
         nw[e] = w[e] - m[e];
         ss += nw[e] * nw[e];
       }
-      store8(mom1 + o, m);
-      store8(w1 + o, nw);
+      store8_split(mom1 + o, m);
+      store8_split(w1 + o, nw);
       return ss;
     } else {
       float nw[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) nw[e] = w[e] - lr * v[e];
-      store8(w1 + o, nw);
-      if (w1_copy) store8(w1s + o, nw);
+      store8_split(w1 + o, nw);
+      if (w1_copy) store8_split(w1s + o, nw);
       return 0.0f;
     }
   }
@@ -1228,6 +1281,8 @@ struct EpiBlkUpd : EpiBase {
   EpiBwdW2<E, false> w2;
   EpiW1<E, false> w1;
   __device__ __forceinline__ bool has_cols(int pi) const { return pi == 0; }
+  static constexpr bool kSplitCols = true;  // both problems: as w2's problem 1 and w1
+  __device__ __forceinline__ bool split_cols(int) const { return true; }
   __device__ __forceinline__ void pre8(int pi, int layer, int row, int col, int M, int N,
                                        float (&x)[8]) const {
     if (pi == 0) w2.pre8(1, layer, row, col, M, N, x);
