@@ -110,23 +110,26 @@ __device__ __forceinline__ void load8(const bf16_t* p, float (&v)[8]) {
 // fp32 access instruction then covers 128 contiguous bytes across the 8 lanes: a non-temporal
 // store of two 16-byte halves per lane 32 bytes apart (the unsplit chunk) leaves every line
 // half written by each instruction, and measured 2.1 TB/s on its own against 5.4 TB/s.
-__device__ __forceinline__ void load8_split(const float* p, float (&v)[8]) {
+// hi: the second half lies inside the row (false where a row ends within the segment; the row
+// length is then a multiple of 8, so both lanes of a pair below are inside or both outside).
+__device__ __forceinline__ void load8_split(const float* p, float (&v)[8], bool hi = true) {
   const f32x4v a = __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(p));
-  const f32x4v b = __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(p + 32));
+  f32x4v b = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (hi) b = __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(p + 32));
   v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
   v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
 }
-__device__ __forceinline__ void store8_split(float* p, const float (&v)[8]) {
+__device__ __forceinline__ void store8_split(float* p, const float (&v)[8], bool hi = true) {
   f32x4v a, b;
   a[0] = v[0]; a[1] = v[1]; a[2] = v[2]; a[3] = v[3];
   b[0] = v[4]; b[1] = v[5]; b[2] = v[6]; b[3] = v[7];
   __builtin_nontemporal_store(a, reinterpret_cast<f32x4v*>(p));
-  __builtin_nontemporal_store(b, reinterpret_cast<f32x4v*>(p + 32));
+  if (hi) __builtin_nontemporal_store(b, reinterpret_cast<f32x4v*>(p + 32));
 }
 // bf16: lanes 2m and 2m+1 exchange halves (a DPP move within each pair of lanes), then lane 2m
-// stores columns 8m..8m+7 and lane 2m+1 columns 32+8m..32+8m+7, 16 bytes each.  Both lanes of a
-// pair must execute this together (they always share a row, hence its bounds checks).
-__device__ __forceinline__ void store8_split(bf16_t* p, const float (&v)[8]) {
+// stores columns 8m..8m+7 and lane 2m+1 columns 32+8m..32+8m+7 (if hi), 16 bytes each.  Both
+// lanes of a pair must execute this together (they always share a row, hence its bounds checks).
+__device__ __forceinline__ void store8_split(bf16_t* p, const float (&v)[8], bool hi = true) {
   const uint32_t a0 = pack_bf16(v[0], v[1]), a1 = pack_bf16(v[2], v[3]);
   const uint32_t b0 = pack_bf16(v[4], v[5]), b1 = pack_bf16(v[6], v[7]);
   const bool odd = (__lane_id() & 1) != 0;
@@ -139,7 +142,7 @@ __device__ __forceinline__ void store8_split(bf16_t* p, const float (&v)[8]) {
   u32x4 w;
   if (odd) { w[0] = r0; w[1] = r1; w[2] = b0; w[3] = b1; }
   else { w[0] = a0; w[1] = a1; w[2] = r0; w[3] = r1; }
-  __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(odd ? p + 28 : p));
+  if (!odd || hi) __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(odd ? p + 28 : p));
 }
 
 // Logistic function with the hardware exponential and reciprocal (about 1 ulp each; an IEEE
@@ -651,16 +654,19 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
                 "paired rows: row pass only");
   static_assert(!Epi::kRowScale || (Epi::kWriteback && !Epi::kRowNorm && !Epi::kCols),
                 "row scale: row pass with write-back, then the scale pass");
-  static_assert(!Epi::kSplitCols || (!Epi::kPairRows && !Epi::kRowScale),
-                "split row chunks: plain row pass");
+  static_assert(!Epi::kSplitCols || !Epi::kPairRows, "split row chunks: no paired rows");
   float aux[2][NCH][NAUX];
   const int rl = lane >> 3, ql = lane & 7;      // row-chunk lane coordinates
   // Split row chunks (split_cols(pi)): lane ql's chunk is columns 4ql..4ql+3 and
-  // 32+4ql..32+4ql+3 of its 64-column row segment, passed as the chunk's first column (the
-  // problem's N is then a multiple of 64, so a segment is stored whole or not at all).
+  // 32+4ql..32+4ql+3 of its 64-column row segment, passed as the chunk's first column.  The
+  // problem's N is then a multiple of 8, the chunk is handled when its first half is inside N,
+  // and the epilogue masks a second half at or beyond N.
   const bool split = Epi::kSplitCols && G.epi.split_cols(pi);
   const int cq = split ? 4 * ql : 8 * ql;        // first column of this lane's chunks
   const int cq2 = split ? 4 * ql + 32 : 8 * ql + 4;  // first column of their second half
+  // staging halves in the other order on odd rows (256 x 256 tiles; measured slower with the
+  // two workgroups per CU of 128 x 128 tiles)
+  const bool sflip = BM == 256 && BN == 256 && split && (rl & 1);
   auto issue_pre = [&](int sb, float (&ax)[NCH][NAUX]) {
     const int grow = m0 + wm * WM + (sb / NSN) * SB, gcol = n0 + wn * WN + (sb % NSN) * SB;
 #pragma unroll
@@ -694,11 +700,19 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       const int r = RS * (rl + 8 * b), c = cq;
       float* s0 = stw + sidx(r, c);
       float* s1 = stw + sidx(r, cq2);
+      // Split chunks put each half of a row's 8 lanes on 32 of the staging's banks, the same
+      // 32 for every row: with sflip, odd rows access their halves in the other order, so that
+      // each 16-byte access instruction of two adjacent rows covers all banks (as unsplit
+      // chunks do).
+      float* sa = sflip ? s1 : s0;
+      float* sb2 = sflip ? s0 : s1;
       float v[8];
-      const float4 x0 = *reinterpret_cast<const float4*>(s0);
-      const float4 x1 = *reinterpret_cast<const float4*>(s1);
-      v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
-      v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
+      const float4 xa = *reinterpret_cast<const float4*>(sa);
+      const float4 xb = *reinterpret_cast<const float4*>(sb2);
+      v[0] = sflip ? xb.x : xa.x; v[1] = sflip ? xb.y : xa.y;
+      v[2] = sflip ? xb.z : xa.z; v[3] = sflip ? xb.w : xa.w;
+      v[4] = sflip ? xa.x : xb.x; v[5] = sflip ? xa.y : xb.y;
+      v[6] = sflip ? xa.z : xb.z; v[7] = sflip ? xa.w : xb.w;
       const bool ok = grow + r + RS - 1 < P.M && gcol + c < P.N;
       float val = 0.0f;
       if constexpr (Epi::kPairRows) {
@@ -711,8 +725,12 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       } else if (ok) {
         val = G.epi.rows8(pi, layer, grow + r, gcol + c, P.M, P.N, v, aux[sb & 1][b]);
         if constexpr (Epi::kWriteback) {
-          *reinterpret_cast<float4*>(s0) = make_float4(v[0], v[1], v[2], v[3]);
-          *reinterpret_cast<float4*>(s1) = make_float4(v[4], v[5], v[6], v[7]);
+          *reinterpret_cast<float4*>(sa) =
+              make_float4(sflip ? v[4] : v[0], sflip ? v[5] : v[1], sflip ? v[6] : v[2],
+                          sflip ? v[7] : v[3]);
+          *reinterpret_cast<float4*>(sb2) =
+              make_float4(sflip ? v[0] : v[4], sflip ? v[1] : v[5], sflip ? v[2] : v[6],
+                          sflip ? v[3] : v[7]);
         }
       }
       if constexpr (Epi::kRowScale) {
@@ -757,13 +775,15 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
     const int grow = m0, gcol = n0 + wave * SB;
 #pragma unroll
     for (int b = 0; b < CPL; ++b) {
-      const int r = rl + 8 * b, c = 8 * ql;
+      const int r = rl + 8 * b, c = cq;
       if (grow + r >= P.M || gcol + c >= P.N) continue;
       const float tot = ((rss[r] + rss[SB + r]) + rss[2 * SB + r]) + rss[3 * SB + r];
-      const float4 x0 = *reinterpret_cast<const float4*>(stw + sidx(r, c));
-      const float4 x1 = *reinterpret_cast<const float4*>(stw + sidx(r, c + 4));
-      const float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-      G.epi.scale8(pi, layer, grow + r, gcol + c, tot, v);
+      const float4 xa = *reinterpret_cast<const float4*>(stw + sidx(r, sflip ? cq2 : c));
+      const float4 xb = *reinterpret_cast<const float4*>(stw + sidx(r, sflip ? c : cq2));
+      const float v[8] = {sflip ? xb.x : xa.x, sflip ? xb.y : xa.y, sflip ? xb.z : xa.z,
+                          sflip ? xb.w : xa.w, sflip ? xa.x : xb.x, sflip ? xa.y : xb.y,
+                          sflip ? xa.z : xb.z, sflip ? xa.w : xb.w};
+      G.epi.scale8(pi, layer, grow + r, gcol + c, P.N, tot, v);
     }
   }
   G.epi.finish(pi, layer, t, wave, lane, partial);
@@ -789,13 +809,15 @@ struct EpiBase {
   static constexpr bool kRowScale = false; // rows8 writes its results back and returns their
                                            // sum of squares; after a workgroup barrier
                                            // scale8 gets each whole row's sum (64 x 256 tiles)
-  __device__ __forceinline__ void scale8(int, int, int, int, float, const float (&)[8]) const {}
+  __device__ __forceinline__ void scale8(int, int, int, int, int, float,
+                                         const float (&)[8]) const {}
   __device__ __forceinline__ void row_partial(int, int, int, int, float) const {}
   static constexpr bool kCols = false;
   static constexpr bool kWriteback = false;
   __device__ __forceinline__ bool has_cols(int) const { return false; }
-  // pre8/rows8 of problem pi take split row chunks (columns c..c+3 and c+32..c+35; N a multiple
-  // of 64): the fp32 read-modify-write epilogues, whose 16-byte accesses then coalesce
+  // pre8/rows8 (and scale8) of problem pi take split row chunks (columns c..c+3 and
+  // c+32..c+35; N a multiple of 8; the second half may lie at or beyond N): the fp32
+  // read-modify-write epilogues, whose 16-byte accesses then coalesce
   static constexpr bool kSplitCols = false;
   __device__ __forceinline__ bool split_cols(int) const { return false; }
   __device__ __forceinline__ void pre8(int, int, int, int, int, int, float (&)[8]) const {}
