@@ -1129,9 +1129,13 @@ struct EpiKv2 : EpiBase {
 // The weights are read and written once per block: W -= lr sum_j (gradient of segment j).
 
 // Plain stores of the accumulators times a per-problem scale: problem 0 as T0 [rows][ld0],
-// problem 1 as T1 [rows][ld1] (the token-block products and the pre-update GEMMs).
+// problem 1 as T1 [rows][ld1] (the token-block products and the pre-update GEMMs).  Split row
+// chunks (every column count here is a multiple of 64), so the fp32 outputs are stored with
+// 16-byte accesses contiguous across lanes.
 template <typename T0, typename T1>
 struct EpiStore : EpiBase {
+  static constexpr bool kSplitCols = true;
+  __device__ __forceinline__ bool split_cols(int) const { return true; }
   T0* p0; long long ls0; int ld0; float s0;
   T1* p1; long long ls1; int ld1; float s1;
   __device__ __forceinline__ float rows8(int pi, int layer, int row, int col, int, int,
@@ -1140,8 +1144,8 @@ struct EpiStore : EpiBase {
     const float sc = pi == 0 ? s0 : s1;
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[e] = sc * v[e];
-    if (pi == 0) store8(p0 + (long long)layer * ls0 + (long long)row * ld0 + col, o);
-    else store8(p1 + (long long)layer * ls1 + (long long)row * ld1 + col, o);
+    if (pi == 0) store8_split(p0 + (long long)layer * ls0 + (long long)row * ld0 + col, o);
+    else store8_split(p1 + (long long)layer * ls1 + (long long)row * ld1 + col, o);
     return 0.0f;
   }
 };
