@@ -151,12 +151,17 @@ def test_paper_shape_bf16(optimizer):
     _check(p, [0, cfg.n_layers - 1], 2e-2, 1e-2)
 
 
-def test_fp32_odd_head_width_and_short_segments():
+@pytest.mark.parametrize("d_head,optimizer", [(96, "paper"), (96, "sgd"), (48, "sgd"),
+                                              (48, "paper")])
+def test_fp32_odd_head_width_and_short_segments(d_head, optimizer):
     """A head width that is not a multiple of 64 (padded contraction) and segments shorter than
-    one K step."""
-    cfg = configs.SwigluConfig("sw_odd", n_layers=1, d_model=192, n_heads=2, d_head=96,
-                               seg_len=300, n_context=900, act_dtype="f32", lr=2.0,
-                               optimizer="paper")
+    one K step.  With SGD the update's row chunks are split (columns 4q.. and 32+4q..): at 96
+    the second half of every last-segment chunk is outside the row, at 48 only that of lanes
+    4..7, so a lane pair's exchanged bf16 copy store is masked on one side."""
+    n_heads = 192 // d_head
+    cfg = configs.SwigluConfig(f"sw_odd{d_head}_{optimizer}", n_layers=1, d_model=192,
+                               n_heads=n_heads, d_head=d_head, seg_len=300, n_context=900,
+                               act_dtype="f32", lr=2.0, optimizer=optimizer)
     p = SwProblem(cfg)
     for s, n in enumerate([300, 5, 259]):
         p.segment(s, n)
