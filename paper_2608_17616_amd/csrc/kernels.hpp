@@ -33,6 +33,9 @@
 // column pass (8 rows of one column).  An epilogue may also take its rows in pairs (rows 2i and
 // 2i + 1 of a sub-block reach the same lane), for results that combine two interleaved output
 // rows, or, on 64 x 256 tiles, scale whole rows after a workgroup-wide sum of their squares.
+// The fp32 read-modify-write epilogues take split row chunks (columns 4q..4q+3 and 32+4q..
+// 32+4q+3 of a 64-column segment for lane q), so that each 16-byte fp32 access instruction
+// covers whole lines across its lanes.
 #pragma once
 
 #include <hip/hip_runtime.h>
