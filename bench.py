@@ -50,10 +50,12 @@ def block_segments(cfg):
     return 512 // T if T <= 256 and weights >= 1 << 24 else 1
 
 
-def stage_work(cfg, q, blk=1):
+def stage_work(cfg, q, blk=1, per_call=1):
     """Algorithmic FLOPs and bytes of one launch of each stage (all layers).  With the block
     form (blk segments per block) the staging and the block stages cover a block of blk*T
-    tokens, and BSEQ one segment (its corrections averaged over the block)."""
+    tokens, and BSEQ one segment (its corrections averaged over the block).  With the paper's
+    optimiser and per_call segments per call, W1's renormalisation pass runs once per call (the
+    other segments' updates write W1's copy instead); the figures are averages per launch."""
     L, d, h, D, T = cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out, cfg.seg_len
     E = 2 if cfg.act_dtype == "bf16" else 4
     hkv = max(1, cfg.d_kv // 128)
@@ -78,8 +80,10 @@ def stage_work(cfg, q, blk=1):
             "attn": attn,
         }
     if cfg.optimizer == "paper":
-        # momentum read-modify-write in the update epilogues; the copies move to RENORM
+        # momentum read-modify-write in the update epilogues; the copies move to RENORM, except
+        # W1's between the segments of one call (written by the update, renormalised once)
         cp1 = E if cfg.act_dtype == "bf16" else 0
+        defer = (per_call - 1) / per_call
         return {
             "xt": (0, L * T * d * E * 2),
             "rate": (L * 4 * T * d, L * (T * d * E + 2 * d * 4 + T * 4)),
@@ -88,8 +92,8 @@ def stage_work(cfg, q, blk=1):
                                                    + T * 4)),
             "bwd": (L * (2 * T * D * h + 2 * T * D * h),
                     L * ((T * D + h * D + 2 * T * h + D * T + h * T) * E + D * h * 16)),
-            "upd": (L * 2 * T * h * d, L * ((h * T + d * T) * E + h * d * 16)),
-            "renorm": (0, L * (h * d * (8 + cp1) + D * h * (8 + 2 * E))),
+            "upd": (L * 2 * T * h * d, L * ((h * T + d * T) * E + h * d * (16 + cp1 * defer))),
+            "renorm": (0, L * (h * d * (8 + cp1) * (1 - defer) + D * h * (8 + 2 * E))),
             "kv1": (L * 2 * q * d * h, L * (q * d + h * d + q * h) * E),
             "kv2": (L * 2 * q * h * D, L * (q * h + D * h) * E + L * q * D * 4),
             "attn": attn,
@@ -641,7 +645,7 @@ def main():
     flop_tok = cfg.flops_per_token()
     peak = PEAK_BF16_TFLOPS if cfg.act_dtype == "bf16" else PEAK_F32_TFLOPS
     mfma_pct = 100.0 * value * flop_tok / (peak * 1e12)
-    work = stage_work(cfg, Q, blk)
+    work = stage_work(cfg, Q, blk, S if args.call == "segments" else 1)
     stages = stage_table(stimes, work)
     dfl, dby = work[dom]
     davg = dms / dcnt / 1e3

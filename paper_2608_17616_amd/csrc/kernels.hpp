@@ -839,9 +839,17 @@ struct EpiFwd1 : EpiBase {
   E* a; E* at; E* dst;
   long long ls;  // layer stride of a, at and dst (Tp*h)
   int h, Tp, n;
+  // [L][h] or null: the W1 operand holds diag(1/cs) times the weights (a row renormalisation
+  // of W1 not yet applied to it), so column j of Z is the accumulator times cs[j]
+  const float* cs;
   __device__ __forceinline__ bool has_cols(int) const { return true; }
   __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
                                          float (&z)[8], const float (&)[8]) const {
+    if (cs) {
+      const float* c = cs + (long long)layer * h + col;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) z[e] *= c[e];
+    }
     float av[8], dv[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -859,6 +867,8 @@ struct EpiFwd1 : EpiBase {
   __device__ __forceinline__ void cols8(int, int layer, int row, int col, int, int,
                                         const float (&z)[8]) const {
     float av[8], dv[8];
+    // fp32 (no write-back): the column pass recomputes from the staged accumulators
+    const float c = !kWriteback && cs ? cs[(long long)layer * h + col] : 1.0f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       if constexpr (kWriteback) {
@@ -866,10 +876,11 @@ struct EpiFwd1 : EpiBase {
         av[e] = __uint_as_float(w << 16);
         dv[e] = __uint_as_float(w & 0xffff0000u);
       } else {
-        const float s = sigmoidf_(z[e]);
+        const float zc = z[e] * c;
+        const float s = sigmoidf_(zc);
         const bool ok = row + e < n;
-        av[e] = ok ? z[e] * s : 0.0f;
-        dv[e] = ok ? s * (1.0f + z[e] * (1.0f - s)) : 0.0f;
+        av[e] = ok ? zc * s : 0.0f;
+        dv[e] = ok ? s * (1.0f + zc * (1.0f - s)) : 0.0f;
       }
     }
     const long long o = (long long)layer * ls + (long long)col * Tp + row;
@@ -1044,6 +1055,11 @@ struct EpiW1 : EpiBase {
   const float* beta;   // PAPER: [L]
   float* ss1;          // PAPER: [L][h][d/64] row-segment sums of squares
   int h;
+  // PAPER: [L][h] or null: the stored master is diag(1/rs) times the weights (a row
+  // renormalisation not yet applied to it), so the update reads rs[row] times the master; with
+  // copy_pending the update also writes the copy of its (not yet renormalised) result
+  const float* rs;
+  int copy_pending;
   static constexpr bool kSplitCols = true;  // split row chunks (d is a multiple of 64)
   __device__ __forceinline__ bool split_cols(int) const { return true; }
   __device__ __forceinline__ void pre8(int, int layer, int row, int col, int, int,
@@ -1056,16 +1072,18 @@ struct EpiW1 : EpiBase {
     const long long o = (long long)layer * ls1 + (long long)row * d + col;
     if constexpr (PAPER) {
       const float b = beta[layer];
+      const float sr = rs ? rs[(long long)layer * h + row] : 1.0f;
       float m[8], nw[8], ss = 0.0f;
       load8_split(mom1 + o, m);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         m[e] = b * m[e] + v[e];
-        nw[e] = w[e] - m[e];
+        nw[e] = sr * w[e] - m[e];
         ss += nw[e] * nw[e];
       }
       store8_split(mom1 + o, m);
       store8_split(w1 + o, nw);
+      if (copy_pending) store8_split(w1s + o, nw);
       return ss;
     } else {
       float nw[8];

@@ -222,8 +222,16 @@ struct mone_ttl {
 namespace {
 
 // One segment step of all layers; x [L][n][d] with layer stride lsx elements.
+// One segment step.  With the paper's optimiser, a multi-segment call defers the row
+// renormalisation of W1 between its segments: w1_pending says that the stored master (and its
+// copy) is diag(1/scale1) times the weights, so FWD1 scales Z's columns by scale1 and the W1
+// update reads scale1 times the master; w1_finish applies this segment's renormalisation to the
+// master and its copy (the last segment of a call), otherwise the update writes the copy of its
+// result and scale1 is left pending.  The weights equal those of one call per segment up to
+// rounding; W2's renormalisation runs every segment.
 template <typename E, bool PAPER>
-int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s) {
+int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s,
+                bool w1_pending = false, bool w1_finish = true) {
   const mone_ttl_config& c = H->cfg;
   const Layout& Ly = H->lay;
   const int Lc = c.n_layers, d = c.d_model, h = c.d_hidden, D = 2 * c.d_kv, Tp = Ly.Tp;
@@ -278,6 +286,7 @@ int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s)
     sp.n_store = h;
     EpiFwd1<E> epi;
     epi.a = A; epi.at = At; epi.dst = dSt; epi.ls = lth; epi.h = h; epi.Tp = Tp; epi.n = n;
+    epi.cs = PAPER && w1_pending ? H->at<float>(Ly.scale1) : nullptr;
     H->timing_begin(MONE_STAGE_FWD1, s);
     if ((e = launch_gemm<E>(pick_tile(n, h, Lc), &sp, 1, Lc, epi, s, nullptr,
                             H->at<float>(Ly.split))) != hipSuccess)
@@ -379,6 +388,8 @@ int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s)
     epi.beta = PAPER ? H->at<float>(Ly.beta) : nullptr;
     epi.ss1 = PAPER ? H->at<float>(Ly.ss1) : nullptr;
     epi.h = h;
+    epi.rs = PAPER && w1_pending ? H->at<float>(Ly.scale1) : nullptr;
+    epi.copy_pending = PAPER && bf && !w1_finish ? 1 : 0;
     H->timing_begin(MONE_STAGE_UPD, s);
     if ((e = launch_gemm<E>(upd_tile(h, d, n, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
       return hip_fail(e, "launch UPD");
@@ -394,8 +405,9 @@ int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s)
     row_scale_kernel<<<dim3((unsigned)((r2 + 255) / 256)), dim3(256), 0, s>>>(
         H->at<float>(Ly.ss2), h / 64, H->at<float>(Ly.norm2), H->at<float>(Ly.scale2), r2);
     const long long hd = (long long)h * d;
-    renorm_w1_kernel<E><<<dim3((unsigned)((hd + 2047) / 2048), Lc), dim3(256), 0, s>>>(
-        H->w1, bf ? H->at<E>(Ly.w1c) : nullptr, H->at<float>(Ly.scale1), h, d);
+    if (w1_finish)
+      renorm_w1_kernel<E><<<dim3((unsigned)((hd + 2047) / 2048), Lc), dim3(256), 0, s>>>(
+          H->w1, bf ? H->at<E>(Ly.w1c) : nullptr, H->at<float>(Ly.scale1), h, d);
     renorm_w2_kernel<E><<<dim3(h / 64, D / 64, Lc), dim3(256), 0, s>>>(
         H->w2, H->at<E>(Ly.w2c), w2t_new, H->at<float>(Ly.scale2), D, h);
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch RENORM");
@@ -842,12 +854,15 @@ int mone_ttl_segments(mone_ttl* H, const void* x, int64_t layer_stride, int32_t 
     if (nb > 1) {
       rc = bf ? run_block<bf16_t>(H, reinterpret_cast<const bf16_t*>(xs), layer_stride, nb, s)
               : run_block<float>(H, reinterpret_cast<const float*>(xs), layer_stride, nb, s);
-    } else if (bf) {
-      rc = paper ? run_segment<bf16_t, true>(H, xs, layer_stride, (int)T, s)
-                 : run_segment<bf16_t, false>(H, xs, layer_stride, (int)T, s);
     } else {
-      rc = paper ? run_segment<float, true>(H, xs, layer_stride, (int)T, s)
-                 : run_segment<float, false>(H, xs, layer_stride, (int)T, s);
+      // paper's optimiser: W1's renormalisation deferred to the call's last segment
+      const bool pending = done > 0, finish = done + 1 == n_segments;
+      if (bf)
+        rc = paper ? run_segment<bf16_t, true>(H, xs, layer_stride, (int)T, s, pending, finish)
+                   : run_segment<bf16_t, false>(H, xs, layer_stride, (int)T, s);
+      else
+        rc = paper ? run_segment<float, true>(H, xs, layer_stride, (int)T, s, pending, finish)
+                   : run_segment<float, false>(H, xs, layer_stride, (int)T, s);
     }
     done += nb;
   }

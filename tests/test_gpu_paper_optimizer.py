@@ -63,6 +63,12 @@ def test_paper_optimizer_matches_oracle(torch_cuda, name):
     sess = mone.TtlSession(cfg, prob.wkv, prob.w1, prob.w2, opt=opt)
     for s, n in enumerate(ns):
         sess.segment(prob.segment(s, n), n)
+    _check_against_oracle(torch, cfg, checked, prob, opt, sess)
+
+
+def _check_against_oracle(torch, cfg, checked, prob, opt, sess):
+    """The session's final weights, their change, momenta, read and last loss against the
+    oracle's run over the recorded segments of the checked layers."""
     if cfg.loss == "nip":  # only the rate-weighted gradient is formed, not the plain loss
         with pytest.raises(mone.MoneError) as err:
             sess.loss()
@@ -98,6 +104,31 @@ def test_paper_optimizer_matches_oracle(torch_cuda, name):
         assert max(errs.values()) <= bar, errs
 
 
+# One multi-segment call: the row renormalisation of W1 is deferred between the call's segments
+# (Z's columns and the next update take the pending scale) and applied after its last one.
+SEG_CASES = {
+    "tiny_paper": (TINY_P, [0], 6),
+    "full_f32_paper": (RAGGED_F32_P.with_(name="full_f32_paper"), [0, 2], 5),
+    "full_bf16_paper": (RAGGED_BF16_P.with_(name="full_bf16_paper"), [0, 2], 5),
+    "short_f32_paper": (SHORT_F32_P, [0, 2], 4),
+    "1b_paper": (configs.ONE_B.with_(name="1b_paper", optimizer="paper", lr=2e-2), [0, 15], 4),
+}
+
+
+@pytest.mark.parametrize("name", list(SEG_CASES))
+def test_paper_optimizer_one_multi_segment_call(torch_cuda, name):
+    torch = torch_cuda
+    cfg, checked, n_seg = SEG_CASES[name]
+    print(f"[paper-segments] case={name} L={cfg.n_layers} d={cfg.d_model} h={cfg.d_hidden} "
+          f"D={cfg.d_out} T={cfg.seg_len} segs={n_seg} act={cfg.act_dtype}", flush=True)
+    prob = DeviceProblem(cfg, checked)
+    opt = prob.paper_state()
+    sess = mone.TtlSession(cfg, prob.wkv, prob.w1, prob.w2, opt=opt)
+    x = torch.cat([prob.segment(s) for s in range(n_seg)], dim=1).contiguous()
+    sess.segments(x)
+    _check_against_oracle(torch, cfg, checked, prob, opt, sess)
+
+
 SMALL_P = C("inv_paper_bf16", n_layers=3, d_model=128, d_hidden=192, d_kv=64, seg_len=160,
             n_context=640, act_dtype="bf16", lr=5e-2, optimizer="paper")
 SMALL_P_F32 = SMALL_P.with_(name="inv_paper_f32", act_dtype="f32")
@@ -114,14 +145,18 @@ def _clone_opt(opt):
 
 
 @pytest.mark.parametrize("cfg", [SMALL_P, SMALL_P_F32], ids=lambda c: c.name)
-def test_row_norms_stay_at_their_initial_values(torch_cuda, cfg):
+@pytest.mark.parametrize("call", ["segment", "segments"])
+def test_row_norms_stay_at_their_initial_values(torch_cuda, cfg, call):
     torch = torch_cuda
-    print(f"[paper-inv] row norms {cfg.name}", flush=True)
+    print(f"[paper-inv] row norms {cfg.name} {call}", flush=True)
     prob = DeviceProblem(cfg, [0])
     opt = prob.paper_state()
     sess, w1, w2 = _session(cfg, prob, opt)
-    for s in range(5):
-        sess.segment(prob.segment(s))
+    if call == "segment":
+        for s in range(5):
+            sess.segment(prob.segment(s))
+    else:  # one call: W1's renormalisation deferred to its last segment
+        sess.segments(torch.cat([prob.segment(s) for s in range(5)], dim=1).contiguous())
     torch.cuda.synchronize()
     n1 = torch.linalg.vector_norm(w1.double(), dim=2)
     n2 = torch.linalg.vector_norm(w2.double(), dim=2)
