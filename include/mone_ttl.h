@@ -194,11 +194,12 @@ int mone_ttl_step_noalloc(const mone_ttl_config* cfg, const void* wkv, float* w1
  * chain, summed in another order), and writes the fast weights once per block (a last
  * block may hold fewer segments; a single one runs alone).  Otherwise the segments run one by
  * one.  The workspace of such configurations includes the block's buffers
- * (mone_ttl_workspace_bytes).  With the paper's optimiser the row renormalisation of W1
- * is carried between the call's segments as a pending row scale (applied to Z's columns and
- * in the next update) and written into w1 and its copy after the last segment, so w1 holds
- * the renormalised weights when the call's work completes, equal to those of one call per
- * segment up to rounding.  mone_ttl_loss then reports the last segment's loss. */
+ * (mone_ttl_workspace_bytes).  With the paper's optimiser the row renormalisations of W1
+ * and W2 are carried between the call's segments as pending row scales (applied to the
+ * forward products, the stored loss gradient and the next updates) and written into w1, w2
+ * and their copies after the last segment, so w1 and w2 hold the renormalised weights when
+ * the call's work completes, equal to those of one call per segment up to rounding.
+ * mone_ttl_loss then reports the last segment's loss. */
 int mone_ttl_segments(mone_ttl* h, const void* x, int64_t layer_stride, int32_t n_segments,
                       void* stream);
 

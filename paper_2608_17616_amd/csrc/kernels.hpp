@@ -436,6 +436,25 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       }
   };
 
+  // Part 0's contribution times a per-column factor (kPart0Scale): applied once, after the
+  // last K step of part 0 this workgroup computes.  Lane l's accumulators of MFMA block j all
+  // lie in column n0 + wn*WN + 32j + l%32.
+  auto part0_scale = [&] {
+    if constexpr (Epi::kPart0Scale) {
+      if (G.epi.has_part0_scale()) {
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int col = n0 + wn * WN + 32 * j + (lane & 31);
+          const float f = col < P.N ? G.epi.part0_scale(layer, col) : 1.0f;
+#pragma unroll
+          for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] *= f;
+        }
+      }
+    }
+  };
+
   // Pipeline.  K step kt reads A slot kt % NA and B slot kt % NB in four sub-steps.  The
   // fragments of each sub-step are read while the MFMAs of the previous one run: sub-step 0 of
   // step kt+1 is read right after the synchronisation that ends step kt, and sub-step 3 of
@@ -503,11 +522,17 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       if constexpr (NP == 1) {
         for (int kt = kbeg; kt < nk; ++kt) dstep(kt, Part0{});
       } else {
-        // both operands switch part when the loaded step reaches nk0
+        // both operands switch part when the loaded step reaches nk0; part 0's computed steps
+        // end at c
         const int sw = nk0 - (DEPTH - 1);
         const int e1 = sw < kbeg ? kbeg : (sw > nk ? nk : sw);
+        const int c = nk0 < kbeg ? kbeg : (nk0 > nk ? nk : nk0);
         int kt = kbeg;
         for (; kt < e1; ++kt) dstep(kt, Part0{});
+        if constexpr (Epi::kPart0Scale) {
+          for (; kt < c; ++kt) dstep(kt, Part1{});
+          if (kbeg < c) part0_scale();
+        }
         for (; kt < nk; ++kt) dstep(kt, Part1{});
       }
       __builtin_amdgcn_s_waitcnt(0);  // the last (out-of-range) loads have retired
@@ -582,9 +607,14 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       // the part a compile-time choice (no per-step selects of offsets).
       const int e1 = nk0 - (NA - 1) < 0 ? 0 : (nk0 - (NA - 1) > nk ? nk : nk0 - (NA - 1));
       const int e2 = nk0 - 1 < e1 ? e1 : (nk0 - 1 > nk ? nk : nk0 - 1);
+      const int c = nk0 < e2 ? e2 : (nk0 > nk ? nk : nk0);  // part 0's computed steps end
       int kt = 0;
       for (; kt < e1; ++kt) step(kt, Part0{}, Part0{});  // A and B loads in part 0
       for (; kt < e2; ++kt) step(kt, Part1{}, Part0{});  // A loads reach part 1 first
+      if constexpr (Epi::kPart0Scale) {
+        for (; kt < c; ++kt) step(kt, Part1{}, Part1{});
+        if (c > 0) part0_scale();
+      }
       for (; kt < nk; ++kt) step(kt, Part1{}, Part1{});
     }
     __builtin_amdgcn_s_waitcnt(0);  // the last (out-of-range) loads have retired
@@ -818,6 +848,11 @@ struct EpiBase {
   static constexpr bool kCols = false;
   static constexpr bool kWriteback = false;
   __device__ __forceinline__ bool has_cols(int) const { return false; }
+  // part 0 of a K-concatenated contraction contributes part0_scale(layer, col) times its
+  // product to column col (when has_part0_scale())
+  static constexpr bool kPart0Scale = false;
+  __device__ __forceinline__ bool has_part0_scale() const { return false; }
+  __device__ __forceinline__ float part0_scale(int, int) const { return 1.0f; }
   // pre8/rows8 (and scale8) of problem pi take split row chunks (columns c..c+3 and
   // c+32..c+35; N a multiple of 8; the second half may lie at or beyond N): the fp32
   // read-modify-write epilogues, whose 16-byte accesses then coalesce
@@ -894,18 +929,30 @@ struct EpiFwd1 : EpiBase {
 // Stores G = c R [Tp][D] (rows) and G^T [D][Tp] (columns); sums R^2 per wave into the loss
 // partials (sq).  For the negative inner product the GEMM is X W_kv^T alone (the targets T)
 // and the same formula gives G = -c T; its loss comes from the W2 update's epilogue instead.
-template <typename E>
+// PSCALE: a row renormalisation of W2 not yet applied to its copy (ps, gs: [L][D], or null):
+// the copy is diag(1/s) times -W2, so part 0's product is scaled by column (ps), and the
+// stored G, which the backward contracts with the unscaled W2^T copy, is G diag(s) (gs); G^T
+// is not.  (A separate instantiation: the scale between the parts costs the 256 x 256 tile
+// some spilled registers around it.)
+template <typename E, bool PSCALE = false>
 struct EpiFwd2 : EpiBase {
   static constexpr int kParts = 2;
   static constexpr bool kCols = true;
+  static constexpr bool kPart0Scale = PSCALE;
   E* g; E* gt;
   float* loss_part;       // [L][parts_per_layer]
   const float* rate;      // [L][Tp] per-token rates (the paper's optimiser), or null
+  const float* ps;
+  const float* gs;
   long long ls;           // Tp*D
   int D, Tp, n, parts_per_layer;
   int sq;                 // write the sum-of-squares loss partials
   float c;
   __device__ __forceinline__ bool has_cols(int) const { return true; }
+  __device__ __forceinline__ bool has_part0_scale() const { return PSCALE && ps != nullptr; }
+  __device__ __forceinline__ float part0_scale(int layer, int col) const {
+    return ps[(long long)layer * D + col];
+  }
   __device__ __forceinline__ float rows8(int, int layer, int row, int col, int, int,
                                          float (&v)[8], const float (&)[8]) const {
     const float cr = rate ? c * rate[(long long)layer * Tp + row] : c;
@@ -915,6 +962,11 @@ struct EpiFwd2 : EpiBase {
       const float r = row < n ? -v[e] : 0.0f;
       s += r * r;
       gv[e] = cr * r;
+    }
+    if (PSCALE && gs) {
+      const float* f = gs + (long long)layer * D + col;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) gv[e] *= f[e];
     }
     store8(g + (long long)layer * ls + (long long)row * D + col, gv);
     return s;
@@ -946,7 +998,10 @@ struct EpiFwd2 : EpiBase {
 // weights the step started from; the update writes the other copy of a ping-pong pair.
 // With the paper's optimiser (PAPER), problem 1 updates the momentum, mu2 = beta mu2 + G^T A
 // (the rates are already in G), and the master, W2 - mu2, both fp32; it returns each row
-// chunk's sum of squares for the renormalisation, which writes the copies afterwards.
+// chunk's sum of squares for the renormalisation, which writes the copies afterwards.  With a
+// renormalisation pending (rs: [L][D], or null) the stored master is diag(1/rs) times the
+// weights, so the update reads rs[row] times it; with copy_pending it writes the copies of its
+// (not yet renormalised) result itself.
 // For the negative inner product (nip, SGD only) problem 1 also sums <W2_{s-1}, G^T A> per
 // wave into the loss partials: with G = -T/n that is -(1/n) sum_j t_j . y_j = L_s.
 template <typename E, bool PAPER = false>
@@ -955,8 +1010,8 @@ struct EpiBwdW2 : EpiBase {
   static constexpr int kAux = 8;  // the master (PAPER: the momentum is read in the row pass,
                                   // which keeps the 256 x 256 tile within its registers)
   static constexpr bool kRowNorm = PAPER;
-  static constexpr bool kCols = !PAPER;
-  static constexpr bool kWriteback = !PAPER;
+  static constexpr bool kCols = true;
+  static constexpr bool kWriteback = true;
   const E* dst; E* dzt;
   long long lst;       // Tp*h
   int Tp, n;
@@ -967,10 +1022,14 @@ struct EpiBwdW2 : EpiBase {
   float* mom2;         // PAPER: [L][D][h] momentum
   const float* beta;   // PAPER: [L] momentum decay of this segment
   float* ss2;          // PAPER: [L][D][h/64] row-segment sums of squares
+  const float* rs;     // PAPER: pending row scale of the master, or null
+  int copy_pending;    // PAPER: write the copies of the result
   float* loss_part;    // nip: [L][parts_per_layer]
   int parts_per_layer;
   int nip;
-  __device__ __forceinline__ bool has_cols(int pi) const { return !PAPER && pi == 1; }
+  __device__ __forceinline__ bool has_cols(int pi) const {
+    return pi == 1 && (!PAPER || copy_pending);
+  }
   static constexpr bool kSplitCols = true;  // problem 1: split row chunks (h is a multiple of 64)
   __device__ __forceinline__ bool split_cols(int pi) const { return pi == 1; }
   __device__ __forceinline__ void pre8(int pi, int layer, int row, int col, int, int,
@@ -995,16 +1054,25 @@ struct EpiBwdW2 : EpiBase {
     const long long o = (long long)layer * ls2 + (long long)row * h + col;
     if constexpr (PAPER) {
       const float b = beta[layer];
+      const float sr = rs ? rs[(long long)layer * D + row] : 1.0f;
       float m[8], nw[8], ss = 0.0f;
       load8_split(mom2 + o, m);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         m[e] = b * m[e] + v[e];
-        nw[e] = x[e] - m[e];
+        nw[e] = sr * x[e] - m[e];
         ss += nw[e] * nw[e];
       }
       store8_split(mom2 + o, m);
       store8_split(w2 + o, nw);
+      if (copy_pending) {
+        float cp[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cp[e] = -nw[e];
+        store8_split(w2n + o, cp);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = nw[e];
       return ss;
     } else {
       float nw[8], cp[8], ip = 0.0f;

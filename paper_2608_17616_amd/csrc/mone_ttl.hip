@@ -223,15 +223,16 @@ namespace {
 
 // One segment step of all layers; x [L][n][d] with layer stride lsx elements.
 // One segment step.  With the paper's optimiser, a multi-segment call defers the row
-// renormalisation of W1 between its segments: w1_pending says that the stored master (and its
-// copy) is diag(1/scale1) times the weights, so FWD1 scales Z's columns by scale1 and the W1
-// update reads scale1 times the master; w1_finish applies this segment's renormalisation to the
-// master and its copy (the last segment of a call), otherwise the update writes the copy of its
-// result and scale1 is left pending.  The weights equal those of one call per segment up to
-// rounding; W2's renormalisation runs every segment.
+// renormalisations between its segments: pending says that the stored masters (and their
+// copies) are diag(1/scale1) and diag(1/scale2) times the weights, so FWD1 scales Z's columns
+// by scale1, FWD2 scales the A W2^T part of its product by scale2 and stores G diag(scale2)
+// for the backward, and the updates read the scale times the master; finish applies this
+// segment's renormalisations to the masters and their copies (the last segment of a call),
+// otherwise the updates write the copies of their results and the scales are left pending.
+// The weights equal those of one call per segment up to rounding.
 template <typename E, bool PAPER>
 int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s,
-                bool w1_pending = false, bool w1_finish = true) {
+                bool pending = false, bool finish = true) {
   const mone_ttl_config& c = H->cfg;
   const Layout& Ly = H->lay;
   const int Lc = c.n_layers, d = c.d_model, h = c.d_hidden, D = 2 * c.d_kv, Tp = Ly.Tp;
@@ -286,7 +287,7 @@ int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s,
     sp.n_store = h;
     EpiFwd1<E> epi;
     epi.a = A; epi.at = At; epi.dst = dSt; epi.ls = lth; epi.h = h; epi.Tp = Tp; epi.n = n;
-    epi.cs = PAPER && w1_pending ? H->at<float>(Ly.scale1) : nullptr;
+    epi.cs = PAPER && pending ? H->at<float>(Ly.scale1) : nullptr;
     H->timing_begin(MONE_STAGE_FWD1, s);
     if ((e = launch_gemm<E>(pick_tile(n, h, Lc), &sp, 1, Lc, epi, s, nullptr,
                             H->at<float>(Ly.split))) != hipSuccess)
@@ -315,7 +316,7 @@ int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s,
     sp.n = D;
     sp.m_store = -1;
     sp.n_store = D;
-    EpiFwd2<E> epi;
+    EpiFwd2<E, PAPER> epi;
     epi.g = Gm; epi.gt = Gt; epi.loss_part = H->at<float>(Ly.loss_part); epi.ls = ltd;
     epi.D = D; epi.Tp = Tp; epi.n = n; epi.parts_per_layer = Ly.loss_per_layer;
     epi.c = c.loss == MONE_LOSS_MSE_SUM   ? 2.0f / (float)n
@@ -323,6 +324,8 @@ int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s,
                                            : 1.0f / (float)n;
     epi.sq = nip ? 0 : 1;
     epi.rate = PAPER ? H->at<float>(Ly.rate) : nullptr;
+    epi.gs = PAPER && pending ? H->at<float>(Ly.scale2) : nullptr;
+    epi.ps = nip ? nullptr : epi.gs;
     int tiles = 0;
     H->timing_begin(MONE_STAGE_FWD2, s);
     if ((e = launch_gemm<E>(pick_tile(n, D, Lc), &sp, 1, Lc, epi, s, &tiles,
@@ -359,6 +362,8 @@ int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s,
     epi.mom2 = PAPER ? H->opt.mom2 : nullptr;
     epi.beta = PAPER ? H->at<float>(Ly.beta) : nullptr;
     epi.ss2 = PAPER ? H->at<float>(Ly.ss2) : nullptr;
+    epi.rs = PAPER && pending ? H->at<float>(Ly.scale2) : nullptr;
+    epi.copy_pending = PAPER && !finish ? 1 : 0;
     epi.loss_part = H->at<float>(Ly.loss_part);
     epi.parts_per_layer = Ly.loss_per_layer;
     epi.nip = c.loss == MONE_LOSS_NIP ? 1 : 0;
@@ -388,15 +393,16 @@ int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s,
     epi.beta = PAPER ? H->at<float>(Ly.beta) : nullptr;
     epi.ss1 = PAPER ? H->at<float>(Ly.ss1) : nullptr;
     epi.h = h;
-    epi.rs = PAPER && w1_pending ? H->at<float>(Ly.scale1) : nullptr;
-    epi.copy_pending = PAPER && bf && !w1_finish ? 1 : 0;
+    epi.rs = PAPER && pending ? H->at<float>(Ly.scale1) : nullptr;
+    epi.copy_pending = PAPER && bf && !finish ? 1 : 0;
     H->timing_begin(MONE_STAGE_UPD, s);
     if ((e = launch_gemm<E>(upd_tile(h, d, n, Lc), &sp, 1, Lc, epi, s)) != hipSuccess)
       return hip_fail(e, "launch UPD");
     H->timing_end(MONE_STAGE_UPD, s);
   }
-  // RENORM (paper optimiser): rows of W1 and W2 back to their initial norms; the copies the
-  // next segment reads (W1 in bf16 mode, -W2, and W2^T into the other ping-pong copy)
+  // RENORM (paper optimiser): the row scales that bring W1 and W2 back to their initial norms;
+  // on finish, the rows rescaled and the copies the next segment reads (W1 in bf16 mode, -W2,
+  // and W2^T into the other ping-pong copy)
   if constexpr (PAPER) {
     H->timing_begin(MONE_STAGE_RENORM, s);
     const long long r1 = (long long)Lc * h, r2 = (long long)Lc * D;
@@ -405,11 +411,12 @@ int run_segment(mone_ttl* H, const void* x, long long lsx, int n, hipStream_t s,
     row_scale_kernel<<<dim3((unsigned)((r2 + 255) / 256)), dim3(256), 0, s>>>(
         H->at<float>(Ly.ss2), h / 64, H->at<float>(Ly.norm2), H->at<float>(Ly.scale2), r2);
     const long long hd = (long long)h * d;
-    if (w1_finish)
+    if (finish) {
       renorm_w1_kernel<E><<<dim3((unsigned)((hd + 2047) / 2048), Lc), dim3(256), 0, s>>>(
           H->w1, bf ? H->at<E>(Ly.w1c) : nullptr, H->at<float>(Ly.scale1), h, d);
-    renorm_w2_kernel<E><<<dim3(h / 64, D / 64, Lc), dim3(256), 0, s>>>(
-        H->w2, H->at<E>(Ly.w2c), w2t_new, H->at<float>(Ly.scale2), D, h);
+      renorm_w2_kernel<E><<<dim3(h / 64, D / 64, Lc), dim3(256), 0, s>>>(
+          H->w2, H->at<E>(Ly.w2c), w2t_new, H->at<float>(Ly.scale2), D, h);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "launch RENORM");
     H->timing_end(MONE_STAGE_RENORM, s);
   }
@@ -855,7 +862,7 @@ int mone_ttl_segments(mone_ttl* H, const void* x, int64_t layer_stride, int32_t 
       rc = bf ? run_block<bf16_t>(H, reinterpret_cast<const bf16_t*>(xs), layer_stride, nb, s)
               : run_block<float>(H, reinterpret_cast<const float*>(xs), layer_stride, nb, s);
     } else {
-      // paper's optimiser: W1's renormalisation deferred to the call's last segment
+      // paper's optimiser: the row renormalisations deferred to the call's last segment
       const bool pending = done > 0, finish = done + 1 == n_segments;
       if (bf)
         rc = paper ? run_segment<bf16_t, true>(H, xs, layer_stride, (int)T, s, pending, finish)
