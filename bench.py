@@ -54,8 +54,9 @@ def stage_work(cfg, q, blk=1, per_call=1):
     """Algorithmic FLOPs and bytes of one launch of each stage (all layers).  With the block
     form (blk segments per block) the staging and the block stages cover a block of blk*T
     tokens, and BSEQ one segment (its corrections averaged over the block).  With the paper's
-    optimiser and per_call segments per call, W1's renormalisation pass runs once per call (the
-    other segments' updates write W1's copy instead); the figures are averages per launch."""
+    optimiser and per_call segments per call, the renormalisation pass runs once per call (the
+    other segments' updates write the weight copies instead); the figures are averages per
+    launch."""
     L, d, h, D, T = cfg.n_layers, cfg.d_model, cfg.d_hidden, cfg.d_out, cfg.seg_len
     E = 2 if cfg.act_dtype == "bf16" else 4
     hkv = max(1, cfg.d_kv // 128)
@@ -81,7 +82,7 @@ def stage_work(cfg, q, blk=1, per_call=1):
         }
     if cfg.optimizer == "paper":
         # momentum read-modify-write in the update epilogues; the copies move to RENORM, except
-        # W1's between the segments of one call (written by the update, renormalised once)
+        # between the segments of one call (written by the updates, renormalised once per call)
         cp1 = E if cfg.act_dtype == "bf16" else 0
         defer = (per_call - 1) / per_call
         return {
@@ -91,9 +92,13 @@ def stage_work(cfg, q, blk=1, per_call=1):
             "fwd2": (L * 2 * T * D * (h + d), L * ((T * h + D * h + T * d + D * d + 2 * T * D) * E
                                                    + T * 4)),
             "bwd": (L * (2 * T * D * h + 2 * T * D * h),
-                    L * ((T * D + h * D + 2 * T * h + D * T + h * T) * E + D * h * 16)),
+                    L * ((T * D + h * D + 2 * T * h + D * T + h * T) * E
+                         + D * h * (16 + 2 * E * defer))),
             "upd": (L * 2 * T * h * d, L * ((h * T + d * T) * E + h * d * (16 + cp1 * defer))),
-            "renorm": (0, L * (h * d * (8 + cp1) * (1 - defer) + D * h * (8 + 2 * E))),
+            # every segment: the row scales from the row-segment sums of squares; once per
+            # call: the rescaled masters and their copies
+            "renorm": (0, L * (4 * (h * d + D * h) // 64
+                               + (h * d * (8 + cp1) + D * h * (8 + 2 * E)) * (1 - defer))),
             "kv1": (L * 2 * q * d * h, L * (q * d + h * d + q * h) * E),
             "kv2": (L * 2 * q * h * D, L * (q * h + D * h) * E + L * q * D * 4),
             "attn": attn,

@@ -104,14 +104,20 @@ def _check_against_oracle(torch, cfg, checked, prob, opt, sess):
         assert max(errs.values()) <= bar, errs
 
 
-# One multi-segment call: the row renormalisation of W1 is deferred between the call's segments
-# (Z's columns and the next update take the pending scale) and applied after its last one.
+# One multi-segment call: the row renormalisations of W1 and W2 are deferred between the call's
+# segments (the forward products, the stored G and the next updates take the pending scales)
+# and applied after its last one.  The cases cover both forward-2 forms (A W2^T + X W_kv^T, and
+# the targets alone for the negative inner product), split contractions (64-token segments)
+# and the 256 x 256 tiles of the 8B-class shape.
 SEG_CASES = {
     "tiny_paper": (TINY_P, [0], 6),
     "full_f32_paper": (RAGGED_F32_P.with_(name="full_f32_paper"), [0, 2], 5),
     "full_bf16_paper": (RAGGED_BF16_P.with_(name="full_bf16_paper"), [0, 2], 5),
+    "nip_f32_paper": (RAGGED_F32_P.with_(name="nip_seg_f32_paper", loss="nip", lr=5e-3), [0, 2], 5),
     "short_f32_paper": (SHORT_F32_P, [0, 2], 4),
+    "short_bf16_paper": (SHORT_F32_P.with_(name="short_bf16_paper", act_dtype="bf16"), [0, 2], 4),
     "1b_paper": (configs.ONE_B.with_(name="1b_paper", optimizer="paper", lr=2e-2), [0, 15], 4),
+    "8b_paper": (configs.EIGHT_B.with_(name="8b_seg_paper", optimizer="paper", lr=2e-2), [0, 31], 2),
 }
 
 
@@ -155,7 +161,7 @@ def test_row_norms_stay_at_their_initial_values(torch_cuda, cfg, call):
     if call == "segment":
         for s in range(5):
             sess.segment(prob.segment(s))
-    else:  # one call: W1's renormalisation deferred to its last segment
+    else:  # one call: the renormalisations deferred to its last segment
         sess.segments(torch.cat([prob.segment(s) for s in range(5)], dim=1).contiguous())
     torch.cuda.synchronize()
     n1 = torch.linalg.vector_norm(w1.double(), dim=2)
