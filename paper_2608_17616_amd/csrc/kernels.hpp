@@ -708,7 +708,30 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
       if (row + RS - 1 < P.M && col < P.N) G.epi.pre8(pi, layer, row, col, P.M, P.N, ax[b]);
     }
   };
-  if constexpr (Epi::kPre) issue_pre(0, aux[0]);
+  // packed problems: sub-block q's chunk b in dwords 4(q&1)..4(q&1)+3 of aux[q>>1][b]
+  const bool pack_all = Epi::kPackAll && G.epi.pack_all(pi);
+  static_assert(!Epi::kPackAll || (NSB <= 4 && NAUX == 8), "packed aux: 4 sub-blocks");
+  auto issue_pre_packed = [&](int q) {
+    const int grow = m0 + wm * WM + (q / NSN) * SB, gcol = n0 + wn * WN + (q % NSN) * SB;
+#pragma unroll
+    for (int b = 0; b < NCH; ++b) {
+      const int row = grow + RS * (rl + 8 * b), col = gcol + cq;
+      float (&w)[4] = *reinterpret_cast<float(*)[4]>(&aux[q >> 1][b][4 * (q & 1)]);
+      if (row + RS - 1 < P.M && col < P.N) G.epi.pre4p(pi, layer, row, col, w);
+    }
+  };
+  if constexpr (Epi::kPre) {
+    if constexpr (Epi::kPackAll) {
+      if (pack_all) {
+#pragma unroll
+        for (int q = 0; q < NSB; ++q) issue_pre_packed(q);
+      } else {
+        issue_pre(0, aux[0]);
+      }
+    } else {
+      issue_pre(0, aux[0]);
+    }
+  }
 #pragma unroll
   for (int sb = 0; sb < NSB; ++sb) {
     const int sm = sb / NSN, sn = sb % NSN;
@@ -726,7 +749,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
                 acc[2 * sm + ii][2 * sn + jj][4 * g + e];
     wave_sync();
     if constexpr (Epi::kPre) {
-      if (sb + 1 < NSB) issue_pre(sb + 1, aux[(sb + 1) & 1]);
+      if (sb + 1 < NSB && !pack_all) issue_pre(sb + 1, aux[(sb + 1) & 1]);
     }
 #pragma unroll
     for (int b = 0; b < NCH; ++b) {
@@ -756,7 +779,19 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
         if (ok) val = G.epi.rows8p(pi, layer, grow + r, gcol + c, P.M, P.N, v, w, aux[sb & 1][b]);
         partial += val;
       } else if (ok) {
-        val = G.epi.rows8(pi, layer, grow + r, gcol + c, P.M, P.N, v, aux[sb & 1][b]);
+        if (pack_all) {
+          float x[NAUX];
+          const float* w = &aux[sb >> 1][b][4 * (sb & 1)];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t u = __float_as_uint(w[e]);
+            x[2 * e] = __uint_as_float(u << 16);
+            x[2 * e + 1] = __uint_as_float(u & 0xffff0000u);
+          }
+          val = G.epi.rows8(pi, layer, grow + r, gcol + c, P.M, P.N, v, x);
+        } else {
+          val = G.epi.rows8(pi, layer, grow + r, gcol + c, P.M, P.N, v, aux[sb & 1][b]);
+        }
         if constexpr (Epi::kWriteback) {
           *reinterpret_cast<float4*>(sa) =
               make_float4(sflip ? v[4] : v[0], sflip ? v[5] : v[1], sflip ? v[6] : v[2],
@@ -859,6 +894,13 @@ struct EpiBase {
   static constexpr bool kSplitCols = false;
   __device__ __forceinline__ bool split_cols(int) const { return false; }
   __device__ __forceinline__ void pre8(int, int, int, int, int, int, float (&)[8]) const {}
+  // kPackAll: problem pi with pack_all(pi) reads 16-bit values (pre4p: 8 of them, packed in 4
+  // dwords held as float bits, widened by the kernel before rows8), and the loads of all of a
+  // wave's sub-blocks (at most 4) are issued before its first staging, in the registers of the
+  // two buffers: more loads in flight than one sub-block ahead
+  static constexpr bool kPackAll = false;
+  __device__ __forceinline__ bool pack_all(int) const { return false; }
+  __device__ __forceinline__ void pre4p(int, int, int, int, float (&)[4]) const {}
   __device__ __forceinline__ void cols8(int, int, int, int, int, int, const float (&)[8]) const {}
   __device__ __forceinline__ void finish(int, int, int, int, int, float) const {}
 };
@@ -1032,6 +1074,15 @@ struct EpiBwdW2 : EpiBase {
   }
   static constexpr bool kSplitCols = true;  // problem 1: split row chunks (h is a multiple of 64)
   __device__ __forceinline__ bool split_cols(int pi) const { return pi == 1; }
+  // problem 0 (bf16): SiLU' of all sub-blocks loaded at once, packed
+  static constexpr bool kPackAll = sizeof(E) == 2;
+  __device__ __forceinline__ bool pack_all(int pi) const { return sizeof(E) == 2 && pi == 0; }
+  __device__ __forceinline__ void pre4p(int, int layer, int row, int col, float (&w)[4]) const {
+    const u32x4 u =
+        *reinterpret_cast<const u32x4*>(dst + (long long)layer * lst + (long long)row * Tp + col);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = __uint_as_float(u[e]);
+  }
   __device__ __forceinline__ void pre8(int pi, int layer, int row, int col, int, int,
                                        float (&x)[kAux]) const {
     float (&x0)[8] = *reinterpret_cast<float(*)[8]>(&x[0]);
