@@ -59,6 +59,14 @@ CASES = {
     # the negative inner product: K2 is the targets alone (one K part), split in two
     "short_nip_f32": (SHORT_F32.with_(name="short_nip_f32", loss="nip", lr=5e-3), [0, 2],
                       [64, 64, 37, 64, 5]),
+    # 256 x 256 tiles for FWD1 and BWD (contractions of 2048 tokens or more, 288 tiles) with
+    # ragged token extents: partial tiles of the backward's packed SiLU' prefetch
+    "big_tile_ragged_bf16": (C("big_tile_ragged_bf16", n_layers=8, d_model=256, d_hidden=1024,
+                               d_kv=128, seg_len=2304, n_context=6912, act_dtype="bf16",
+                               lr=2e-3), [0, 7], [2304, 2100, 2250]),
+    "big_tile_ragged_f32": (C("big_tile_ragged_f32", n_layers=8, d_model=256, d_hidden=1024,
+                              d_kv=128, seg_len=2304, n_context=6912, act_dtype="f32",
+                              lr=2e-3), [0, 7], [2304, 2100, 2250]),
 }
 
 
