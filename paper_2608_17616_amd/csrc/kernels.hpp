@@ -656,7 +656,9 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
   // 8 lanes cover a 64-column row segment); column pass, if the epilogue has one: column
   // chunks (8 consecutive rows of one column; 8 lanes cover the 64 rows of a column).  The
   // memory reads an epilogue needs per row chunk (pre8: the fp32 master, SiLU') are issued one
-  // sub-block ahead, the first before the first staging.  Staging layout: row r, column c at
+  // sub-block ahead (after the staging of the current one, or with kPreLate after its row
+  // pass), the first before the first staging; 16-bit inputs (kPackAll) all at once.  Staging
+  // layout: row r, column c at
   // r*64 + (c ^ sw(r)) with sw(r) = ((r ^ r/8) & 7) * 4, which keeps 4-column groups intact
   // (16-byte reads) and spreads the 8 rows of a column chunk over distinct banks.
   constexpr int SB = 64;                        // sub-block edge
@@ -748,7 +750,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
             stw[sidx(ii * 32 + g * 8 + (lane >> 5) * 4 + e, jj * 32 + (lane & 31))] =
                 acc[2 * sm + ii][2 * sn + jj][4 * g + e];
     wave_sync();
-    if constexpr (Epi::kPre) {
+    if constexpr (Epi::kPre && !Epi::kPreLate) {
       if (sb + 1 < NSB && !pack_all) issue_pre(sb + 1, aux[(sb + 1) & 1]);
     }
 #pragma unroll
@@ -819,6 +821,9 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
         }
       }
     }
+    if constexpr (Epi::kPre && Epi::kPreLate) {
+      if (sb + 1 < NSB && !pack_all) issue_pre(sb + 1, aux[(sb + 1) & 1]);
+    }
     if constexpr (Epi::kCols) {
       if (G.epi.has_cols(pi)) {
         if constexpr (Epi::kWriteback) wave_sync();
@@ -869,6 +874,8 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmLaunch<Epi> G) {
 struct EpiBase {
   static constexpr int kParts = 1;  // K-concatenated operand parts the problems may have
   static constexpr bool kPre = false;  // pre8 reads memory (loads are issued a batch ahead)
+  static constexpr bool kPreLate = false;  // ... after this sub-block's row pass rather than
+                                           // before it (shorter lead, fewer live registers)
   static constexpr int kAux = 8;       // floats pre8 reads per row chunk
   static constexpr bool kRowNorm = false;  // rows8 returns the chunk's sum of squares, which
                                            // is reduced per 64-column row segment
@@ -1049,6 +1056,7 @@ struct EpiFwd2 : EpiBase {
 template <typename E, bool PAPER = false>
 struct EpiBwdW2 : EpiBase {
   static constexpr bool kPre = true;
+  static constexpr bool kPreLate = true;  // measured faster on 256 x 256 tiles (fewer spills)
   static constexpr int kAux = 8;  // the master (PAPER: the momentum is read in the row pass,
                                   // which keeps the 256 x 256 tile within its registers)
   static constexpr bool kRowNorm = PAPER;
