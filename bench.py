@@ -47,7 +47,7 @@ def block_segments(cfg):
     if cfg.block_tokens > 0:
         return cfg.block_tokens // T
     weights = cfg.n_layers * cfg.d_hidden * (cfg.d_model + cfg.d_out)
-    return 512 // T if T <= 256 and weights >= 1 << 24 else 1
+    return min(8, 1024 // T) if T <= 256 and weights >= 1 << 24 else 1
 
 
 def stage_work(cfg, q, blk=1, per_call=1):

@@ -82,12 +82,13 @@ typedef struct {
   float lr;          /* learning rate (finite, may be 0); with MONE_OPT_PAPER it scales the
                         per-token rates */
   int32_t optimizer; /* mone_optimizer */
-  int32_t block_tokens; /* block form of mone_ttl_segments: tokens per block.  0 chooses: 512
-                           when the block form applies (plain SGD, a squared-error loss, seg_len
-                           a multiple of 64 of at most 256) and the fast weights of all layers
-                           hold at least 2^24 elements, else none.  Negative: none.  Positive:
-                           a multiple of seg_len, from 2 * seg_len to 4096, where the block form
-                           applies (else MONE_EUNSUPPORTED). */
+  int32_t block_tokens; /* block form of mone_ttl_segments: tokens per block.  0 chooses:
+                           8 segments, at most 1024 tokens (512 at seg_len 64, 1024 at 128 and
+                           256), when the block form applies (plain SGD, a squared-error loss,
+                           seg_len a multiple of 64 of at most 256) and the fast weights of all
+                           layers hold at least 2^24 elements, else none.  Negative: none.
+                           Positive: a multiple of seg_len, from 2 * seg_len to 4096, where the
+                           block form applies (else MONE_EUNSUPPORTED). */
 } mone_ttl_config;
 
 typedef struct mone_ttl mone_ttl; /* opaque host object */

@@ -68,10 +68,13 @@ struct Layout {
 // tokens; a block of segments reads and writes them once, at the cost of the T x T token
 // products of its segments' corrections (which grow with T and with the block).  It covers
 // plain SGD on the squared-error losses with segments of a multiple of 64 tokens (whole K
-// steps of the token products).  By default: 512-token blocks for segments of at most 256
-// tokens, when the fast weights of all layers hold at least 2^24 elements (below that, the
-// weight traffic a block saves is small next to the latency of its extra launches).
-constexpr int kBlockTokens = 512, kMaxBlockTokens = 4096;
+// steps of the token products).  By default, for segments of at most 256 tokens when the fast
+// weights of all layers hold at least 2^24 elements (below that, the weight traffic a block
+// saves is small next to the latency of its extra launches): 8 segments per block, at most
+// 1024 tokens (measured at 16 layers of 2048 -> 2048 -> 1024: T = 64 in 512-token blocks,
+// T = 128 and 256 in 1024-token blocks; 512 segments of T = 512 ran faster one by one).
+constexpr int kBlockMaxSeg = 256, kBlockSegs = 8, kBlockMaxDefault = 1024;
+constexpr int kMaxBlockTokens = 4096;
 constexpr long long kBlockMinWeights = 1LL << 24;
 
 bool block_form_applies(const mone_ttl_config* c) {
@@ -84,7 +87,10 @@ int block_tokens(const mone_ttl_config* c) {
   if (c->block_tokens < 0 || !block_form_applies(c)) return 0;
   if (c->block_tokens > 0) return c->block_tokens;
   const long long w = (long long)c->n_layers * c->d_hidden * (c->d_model + 2LL * c->d_kv);
-  return c->seg_len <= kBlockTokens / 2 && w >= kBlockMinWeights ? kBlockTokens : 0;
+  if (c->seg_len > kBlockMaxSeg || w < kBlockMinWeights) return 0;
+  const int segs = kBlockMaxDefault / c->seg_len < kBlockSegs ? kBlockMaxDefault / c->seg_len
+                                                              : kBlockSegs;
+  return segs * c->seg_len;  // at least 4 segments: seg_len <= 256
 }
 
 int check_config(const mone_ttl_config* c) {

@@ -6,6 +6,8 @@ import re
 
 import pytest
 
+import bench
+
 from paper_2608_17616_amd import configs, mone
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -292,6 +294,15 @@ def test_block_form_workspace_and_config_checks():
     st = configs.STRESS
     assert (mone.mone_ttl_workspace_bytes(mone.config_from(st))
             > mone.mone_ttl_workspace_bytes(mone.config_from(st.with_(block_tokens=-1))))
+    # the default block: 8 segments, at most 1024 tokens, for segments of at most 256 tokens
+    big = dict(base, n_layers=16, d_model=2048, d_hidden=2048, d_kv=512)
+    wsb = lambda **kw: mone.mone_ttl_workspace_bytes(mone.make_config(**dict(big, **kw)))  # noqa
+    for T, default in ((64, 512), (128, 1024), (192, 960), (256, 1024)):
+        assert wsb(seg_len=T) == wsb(seg_len=T, block_tokens=default) != wsb(seg_len=T,
+                                                                           block_tokens=-1)
+        assert bench.block_segments(configs.STRESS.with_(seg_len=T)) == default // T
+    assert wsb(seg_len=320) == wsb(seg_len=320, block_tokens=-1)
+    assert bench.block_segments(configs.STRESS.with_(seg_len=320)) == 1
     for bad in (dict(block_tokens=100), dict(block_tokens=64), dict(block_tokens=8192),
                 dict(block_tokens=512, loss="nip"), dict(block_tokens=512, optimizer="paper"),
                 dict(block_tokens=500, seg_len=100)):

@@ -34,6 +34,12 @@ CASES = {
     # T = 192: blocks of 2 (384 tokens); 5 = 2 + 2 + 1 (the last one alone)
     "t192_f32": (C("t192_f32", n_layers=2, d_model=256, d_hidden=384, d_kv=128, seg_len=192,
                    n_context=960, act_dtype="f32", lr=1e-2, block_tokens=384), [0, 1], 5),
+    # T = 256 in blocks of 4 (1024 tokens, the library's default size there); 9 = 4 + 4 + 1
+    "t256_bf16": (C("t256_bf16", n_layers=2, d_model=256, d_hidden=512, d_kv=128, seg_len=256,
+                    n_context=2304, act_dtype="bf16", lr=1e-2, block_tokens=1024), [0, 1], 9),
+    # T = 128 in blocks of 8 (1024 tokens, the default size there); 10 = 8 + 2
+    "t128_f32": (C("t128_f32", n_layers=2, d_model=256, d_hidden=384, d_kv=64, seg_len=128,
+                   n_context=1280, act_dtype="f32", lr=1e-2, block_tokens=1024), [0, 1], 10),
     # T = 512 in blocks of 2 (1024 tokens)
     "t512_bf16": (C("t512_bf16", n_layers=2, d_model=256, d_hidden=512, d_kv=128, seg_len=512,
                     n_context=2560, act_dtype="bf16", lr=1e-2, block_tokens=1024), [1], 5),
